@@ -1,0 +1,181 @@
+/*
+ * mca.h - Monte-Carlo Attention (MCA) forward pass for AMD Instinct MI355X (gfx950).
+ *
+ * Kim & Ko, "Fast Monte-Carlo Approximation of the Attention Mechanism" (AAAI-22).
+ * One attention layer Y = A (X W_v) (Eq. 1, Sec. "Self-Attention Mechanisms") in which
+ * the encoding X W_v is replaced by the randomised estimator of Eq. 5: every token j
+ * gets its own sample count r_j from the attention it receives (Eq. 9,
+ * Sec. "Determining Sample Size from Attention") and is encoded with r_j importance
+ * sampled rows of W_v (Eq. 2 with the optimal probability of Eq. 4).
+ *
+ * Plain C ABI: pointers, sizes and a stream handle; no C++ or framework types.
+ *
+ * Conventions shared by every entry point
+ *  - "device" pointers point to memory of the current HIP device; "host" pointers to
+ *    host memory. The caller owns every buffer; the library allocates no device memory
+ *    and keeps no state between calls apart from optional profiler objects.
+ *  - `stream` is a hipStream_t (NULL = the null stream). All device work is enqueued on
+ *    it; nothing synchronises the host. Outputs are valid once the caller has
+ *    synchronised the stream.
+ *  - Arguments are checked on the host before anything is enqueued; a failed check
+ *    returns a non-zero mca_status and enqueues nothing. mca_last_error() then gives a
+ *    readable reason (thread-local). Nothing throws across this ABI and nothing aborts.
+ *  - Layouts are row-major with the last index contiguous. Device pointers must be
+ *    16-byte aligned.
+ *  - Determinism: identical inputs, alpha and seed give bitwise-identical r, sample
+ *    indices and Y.
+ *  - Concurrent calls are safe when they use distinct workspaces and outputs.
+ */
+#ifndef MCA_H_
+#define MCA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum mca_status {
+  MCA_OK = 0,
+  MCA_ERR_INVALID_ARGUMENT = 1,   /* null pointer, bad size, bad alpha, misalignment */
+  MCA_ERR_UNSUPPORTED = 2,        /* valid, but outside what the kernels implement */
+  MCA_ERR_WORKSPACE_TOO_SMALL = 3,
+  MCA_ERR_HIP = 4                 /* a HIP runtime call or kernel launch failed */
+} mca_status;
+
+typedef enum mca_dtype {
+  MCA_F32 = 0,   /* float32 inputs; fp32 MFMA and fp32 accumulation */
+  MCA_BF16 = 1   /* bfloat16 inputs; bf16 MFMA with fp32 accumulation */
+} mca_dtype;
+
+/* Stages of the forward pass, in launch order (profiler slots). */
+typedef enum mca_stage {
+  MCA_STAGE_CLEAR = 0,          /* zero the column-max and saturated-token counters */
+  MCA_STAGE_SCORES_COLMAX = 1,  /* softmax(Q K^T / 8) row statistics and column max */
+  MCA_STAGE_ENCODE = 2,         /* count rule, sampler and gather-accumulate */
+  MCA_STAGE_DENSE_ENCODE = 3,   /* exact x_j W_v for saturated tokens (MFMA) */
+  MCA_STAGE_ATTN_OUT = 4,       /* Y = A H~ (MFMA) */
+  MCA_NUM_STAGES = 5
+} mca_stage;
+
+/*
+ * Description of one forward call.
+ *
+ * Shapes: B = batch, n = seq (padded length), H = heads, d_head = 64,
+ * d_out = H * 64, d_in = width of X.
+ *   Q, K : [B, n, d_out], head h in columns h*64 .. h*64+63
+ *   X    : [B, n, d_in]
+ *   W_v  : [d_in, d_out]; row i belongs to input feature i (the X W convention of
+ *          Eq. 1). A framework Linear weight [d_out, d_in] must be transposed.
+ *   Y    : [B, n, d_out] float32
+ *   r    : [B, n] int32
+ */
+typedef struct mca_forward_desc {
+  int64_t batch;     /* B >= 1 */
+  int64_t seq;       /* n >= 1 */
+  int64_t heads;     /* H >= 1; d_out = 64 H must be a multiple of 256 and <= 2048 */
+  int64_t d_head;    /* must be 64 (MCA_ERR_UNSUPPORTED otherwise) */
+  int64_t d_in;      /* 1 .. 2048 */
+  int32_t dtype;     /* mca_dtype of Q, K, X and W_v */
+  int32_t reserved;  /* must be 0 */
+  double alpha;      /* attention error coefficient of Eq. 9; finite and > 0 */
+  uint64_t seed;     /* Philox4x32-10 key (low word, high word) */
+  /* device [B] int32 valid lengths (right padding), clamped to 1..n; NULL = all n */
+  const int32_t* seq_lens;
+  /* device [B*n] int32 or NULL. When set, replaces the count rule: token j of row b
+     uses r_in[b*n+j] clamped to 0..d_in (padded keys still get 0). */
+  const int32_t* r_in;
+  /* Optional device outputs (NULL = not written):
+     colmax_out      [B*n]       float32 m_j = max over heads and valid queries of A[:, j]
+     sample_idx_out  [B*n*d_in]  int32: index s_k of draw k of token (b, j) at
+                                 (b*n+j)*d_in + k, for k < r_j and 0 < r_j < d_in
+     sample_coef_out [B*n*d_in]  float32 x_{s_k} T / (r_j w_{s_k}), same layout
+     encoded_out     [B*n*d_out] float32 H~ (the estimated X W_v rows) */
+  float* colmax_out;
+  int32_t* sample_idx_out;
+  float* sample_coef_out;
+  float* encoded_out;
+  /* mca_profiler handle from mca_profiler_create, or NULL. When set, the call records
+     a pair of HIP events around every stage launch. */
+  void* profiler;
+} mca_forward_desc;
+
+/*
+ * Row norms of the value projection, computed once per weight matrix and cached
+ * (Sec. "Formulation of Sampling Probability": the per-row statistic of W can be
+ * embedded in the model or cached).
+ *   rownorm[i] = float32(sqrt(sum_c W_v[i, c]^2)), squares summed in float64 in
+ *   column order c = 0, 1, ..., d_out-1, one IEEE square root, one rounding to
+ *   float32. Bitwise reproducible.
+ * W_v: device [d_in, d_out] of `dtype`; rownorm: device [d_in] float32 (written).
+ * Errors: MCA_ERR_INVALID_ARGUMENT for null pointers, sizes < 1, d_in > 2048,
+ * d_out > 1 << 20 or a bad dtype; MCA_ERR_HIP if the launch fails.
+ */
+mca_status mca_prepare_weights(const void* W_v, int32_t dtype, int64_t d_in, int64_t d_out,
+                               float* rownorm, void* stream);
+
+/*
+ * Bytes of device workspace mca_attention_forward needs for `desc` (host only, no
+ * device work). Errors: as the argument checks of mca_attention_forward.
+ */
+mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
+
+/*
+ * One MCA forward pass (Eq. 5, with counts from Eq. 9):
+ *   A_h   = softmax(Q_h K_h^T / 8), keys >= seq_lens[b] masked
+ *   m_j   = max over heads h and valid queries i of A_h[i, j]
+ *   r_j   = min(max(ceil(t*t), 1), d_in), t = (len_b * m_j) / alpha in float64; 0 for
+ *           padded keys. r_j = d_in marks a saturated token.
+ *   H~[j] = (1/r_j) sum_k x_{j,s_k} W_v[s_k] / p(s_k)   for 0 < r_j < d_in
+ *           with p(i) = w_i / T the 32-bit fixed-point form of |x_ji| * rownorm[i]
+ *           (Eq. 4 for the product x_j W_v), s_k drawn i.i.d. with replacement
+ *           (Eq. 2) by Philox4x32-10 with key `seed` and counter (k, j, b, 0) and
+ *           an inverse-CDF search; H~[j] = x_j W_v exactly when r_j = d_in; H~[j] = 0
+ *           when r_j = 0 or x_j = 0.
+ *   Y_h   = A_h H~_h (per head column slice)
+ * Inputs Q, K, X, W_v (device, `desc->dtype`), rownorm (device [d_in] from
+ * mca_prepare_weights). Outputs Y (device [B, n, d_out] float32) and r (device [B, n]
+ * int32). Rows of Y for padded queries are computed by the same formula.
+ * `workspace` must hold at least mca_workspace_size bytes; its contents on entry do not
+ * matter and are overwritten.
+ * Errors: MCA_ERR_INVALID_ARGUMENT (null required pointer, size < 1, non-finite or
+ * non-positive alpha, reserved != 0, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
+ * != 64, d_out not a multiple of 256 or > 2048, d_in > 2048), MCA_ERR_WORKSPACE_TOO_SMALL,
+ * MCA_ERR_HIP.
+ */
+mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, const void* K,
+                                 const void* X, const void* W_v, const float* rownorm,
+                                 float* Y, int32_t* r, void* workspace, size_t workspace_bytes,
+                                 void* stream);
+
+/* Static description of a status code. */
+const char* mca_status_string(mca_status status);
+
+/* Reason for the last non-OK status returned on this thread ("" if none). */
+const char* mca_last_error(void);
+
+/* Number of forward stages (MCA_NUM_STAGES) and their names. */
+int mca_num_stages(void);
+const char* mca_stage_name(int stage);
+
+/*
+ * Per-stage kernel timing with HIP events, for benchmarks.
+ * mca_profiler_create: *handle receives a new profiler (host object plus HIP events,
+ *   created on the current device). MCA_ERR_HIP if event creation fails.
+ * mca_profiler_collect: waits for every recorded event, then writes the summed
+ *   milliseconds and the number of timed launches of each stage into stage_ms[0..n)
+ *   and launches[0..n) (host arrays, n <= MCA_NUM_STAGES) and clears the records.
+ * mca_profiler_destroy: releases the handle (NULL is accepted).
+ * A profiler records at most 65536 stage launches between collections; further
+ * launches run untimed.
+ */
+mca_status mca_profiler_create(void** handle);
+mca_status mca_profiler_collect(void* handle, double* stage_ms, int64_t* launches, int n);
+mca_status mca_profiler_destroy(void* handle);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MCA_H_ */

@@ -1,0 +1,246 @@
+"""Thin ctypes binding of libmca (the C ABI in include/mca.h).
+
+Argument marshalling only: torch tensors become device pointers and the
+current HIP stream; every step of the forward pass runs in the library's HIP
+kernels. There is no fallback: if libmca.so is missing or cannot be loaded,
+every call raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libmca.so")
+
+MCA_OK = 0
+MCA_ERR_INVALID_ARGUMENT = 1
+MCA_ERR_UNSUPPORTED = 2
+MCA_ERR_WORKSPACE_TOO_SMALL = 3
+MCA_ERR_HIP = 4
+MCA_F32 = 0
+MCA_BF16 = 1
+NUM_STAGES = 5
+STAGES = ("clear", "scores_colmax", "encode", "dense_encode", "attn_out")
+
+
+class ForwardDesc(ctypes.Structure):
+    _fields_ = [
+        ("batch", ctypes.c_int64),
+        ("seq", ctypes.c_int64),
+        ("heads", ctypes.c_int64),
+        ("d_head", ctypes.c_int64),
+        ("d_in", ctypes.c_int64),
+        ("dtype", ctypes.c_int32),
+        ("reserved", ctypes.c_int32),
+        ("alpha", ctypes.c_double),
+        ("seed", ctypes.c_uint64),
+        ("seq_lens", ctypes.c_void_p),
+        ("r_in", ctypes.c_void_p),
+        ("colmax_out", ctypes.c_void_p),
+        ("sample_idx_out", ctypes.c_void_p),
+        ("sample_coef_out", ctypes.c_void_p),
+        ("encoded_out", ctypes.c_void_p),
+        ("profiler", ctypes.c_void_p),
+    ]
+
+
+class MCAError(RuntimeError):
+    def __init__(self, status: int, where: str, detail: str):
+        self.status = status
+        super().__init__(f"{where}: {status_string(status)}: {detail}")
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
+    """Load libmca.so (raises if it is not built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"{path} is not built; run paper_2201_12854_amd.build_lib.build() first")
+    lib = ctypes.CDLL(path)
+    vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    lib.mca_prepare_weights.argtypes = [vp, i32, i64, i64, vp, vp]
+    lib.mca_prepare_weights.restype = ctypes.c_int
+    lib.mca_workspace_size.argtypes = [ctypes.POINTER(ForwardDesc), ctypes.POINTER(sz)]
+    lib.mca_workspace_size.restype = ctypes.c_int
+    lib.mca_attention_forward.argtypes = [ctypes.POINTER(ForwardDesc), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.mca_attention_forward.restype = ctypes.c_int
+    lib.mca_status_string.argtypes = [ctypes.c_int]
+    lib.mca_status_string.restype = ctypes.c_char_p
+    lib.mca_last_error.argtypes = []
+    lib.mca_last_error.restype = ctypes.c_char_p
+    lib.mca_num_stages.argtypes = []
+    lib.mca_num_stages.restype = ctypes.c_int
+    lib.mca_stage_name.argtypes = [ctypes.c_int]
+    lib.mca_stage_name.restype = ctypes.c_char_p
+    lib.mca_profiler_create.argtypes = [ctypes.POINTER(vp)]
+    lib.mca_profiler_create.restype = ctypes.c_int
+    lib.mca_profiler_collect.argtypes = [vp, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(i64), ctypes.c_int]
+    lib.mca_profiler_collect.restype = ctypes.c_int
+    lib.mca_profiler_destroy.argtypes = [vp]
+    lib.mca_profiler_destroy.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load_library().mca_status_string(status).decode()
+
+
+def _check(status: int, where: str):
+    if status != MCA_OK:
+        raise MCAError(status, where, load_library().mca_last_error().decode())
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _dtype_code(t) -> int:
+    import torch
+
+    if t.dtype == torch.float32:
+        return MCA_F32
+    if t.dtype == torch.bfloat16:
+        return MCA_BF16
+    raise TypeError(f"unsupported dtype {t.dtype}; use float32 or bfloat16")
+
+
+def _stream_handle(device) -> int:
+    import torch
+
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None, r_in=None,
+              colmax_out=None, sample_idx_out=None, sample_coef_out=None, encoded_out=None,
+              profiler=None) -> ForwardDesc:
+    d = ForwardDesc()
+    d.batch, d.seq, d.heads, d.d_head, d.d_in = batch, seq, heads, 64, d_in
+    d.dtype, d.reserved = dtype_code, 0
+    d.alpha, d.seed = float(alpha), int(seed) & 0xFFFFFFFFFFFFFFFF
+    d.seq_lens, d.r_in = _ptr(seq_lens), _ptr(r_in)
+    d.colmax_out, d.sample_idx_out = _ptr(colmax_out), _ptr(sample_idx_out)
+    d.sample_coef_out, d.encoded_out = _ptr(sample_coef_out), _ptr(encoded_out)
+    d.profiler = None if profiler is None else profiler.handle
+    return d
+
+
+def workspace_size(desc: ForwardDesc) -> int:
+    lib = load_library()
+    out = ctypes.c_size_t(0)
+    _check(lib.mca_workspace_size(ctypes.byref(desc), ctypes.byref(out)), "mca_workspace_size")
+    return out.value
+
+
+def prepare_weights(W_v, rownorm=None):
+    """rownorm[i] = ||W_v[i, :]|| (float32) for W_v [d_in, d_out] on a HIP device."""
+    import torch
+
+    lib = load_library()
+    if W_v.dim() != 2 or not W_v.is_cuda or not W_v.is_contiguous():
+        raise ValueError("W_v must be a contiguous 2-D device tensor [d_in, d_out]")
+    if rownorm is None:
+        rownorm = torch.empty(W_v.shape[0], dtype=torch.float32, device=W_v.device)
+    _check(lib.mca_prepare_weights(_ptr(W_v), _dtype_code(W_v), W_v.shape[0], W_v.shape[1], _ptr(rownorm),
+                                   _stream_handle(W_v.device)), "mca_prepare_weights")
+    return rownorm
+
+
+@dataclass
+class ForwardResult:
+    Y: object
+    r: object
+    colmax: object = None
+    sample_idx: object = None
+    sample_coef: object = None
+    encoded: object = None
+
+
+def attention_forward(Q, K, X, W_v, rownorm, alpha: float, seed: int = 0, *, heads: int,
+                      seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
+                      workspace=None, out=None, profiler=None) -> ForwardResult:
+    """One MCA forward pass through libmca on the current HIP stream.
+
+    Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
+    all bfloat16, contiguous, on one device. rownorm from ``prepare_weights``.
+    seq_lens: optional int32 [B]. r_in: optional int32 [B, n] overriding the count
+    rule. ``export`` also returns the column max and H~ (float32); ``export_samples``
+    the per-draw indices and coefficients ([B, n, d_in], first r_j entries valid).
+    ``out`` may pass preallocated (Y, r).
+    """
+    import torch
+
+    lib = load_library()
+    B, n, d_in = X.shape
+    d_out = W_v.shape[1]
+    dt = _dtype_code(X)
+    dev = X.device
+    for name, t in (("Q", Q), ("K", K), ("X", X), ("W_v", W_v)):
+        if not t.is_cuda or not t.is_contiguous() or t.dtype != X.dtype or t.device != dev:
+            raise ValueError(f"{name} must be a contiguous {X.dtype} tensor on {dev}")
+    if Q.shape != (B, n, heads * 64) or K.shape != Q.shape or W_v.shape[0] != d_in or d_out != heads * 64:
+        raise ValueError("shape mismatch: Q, K [B, n, heads*64], X [B, n, d_in], W_v [d_in, heads*64]")
+    if rownorm.dtype != torch.float32 or rownorm.shape != (d_in,) or rownorm.device != dev:
+        raise ValueError("rownorm must be float32 [d_in] on the same device")
+    if seq_lens is not None and (seq_lens.dtype != torch.int32 or seq_lens.shape != (B,)):
+        raise ValueError("seq_lens must be int32 [B]")
+    if r_in is not None and (r_in.dtype != torch.int32 or r_in.numel() != B * n or not r_in.is_contiguous()):
+        raise ValueError("r_in must be a contiguous int32 [B, n]")
+    res = ForwardResult(None, None)
+    if export:
+        res.colmax = torch.empty((B, n), dtype=torch.float32, device=dev)
+        res.encoded = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)
+    if export_samples:
+        res.sample_idx = torch.full((B, n, d_in), -1, dtype=torch.int32, device=dev)
+        res.sample_coef = torch.zeros((B, n, d_in), dtype=torch.float32, device=dev)
+    desc = make_desc(B, n, heads, d_in, dt, alpha, seed, seq_lens=seq_lens, r_in=r_in,
+                     colmax_out=res.colmax, sample_idx_out=res.sample_idx,
+                     sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler)
+    ws_bytes = workspace_size(desc)
+    if workspace is None or workspace.numel() < ws_bytes:
+        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    if out is None:
+        Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)
+        r = torch.empty((B, n), dtype=torch.int32, device=dev)
+    else:
+        Y, r = out
+    _check(lib.mca_attention_forward(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(rownorm),
+                                     _ptr(Y), _ptr(r), _ptr(workspace), workspace.numel(),
+                                     _stream_handle(dev)), "mca_attention_forward")
+    res.Y, res.r = Y, r
+    return res
+
+
+class Profiler:
+    """Per-stage HIP-event timing of mca_attention_forward calls."""
+
+    def __init__(self):
+        lib = load_library()
+        h = ctypes.c_void_p()
+        _check(lib.mca_profiler_create(ctypes.byref(h)), "mca_profiler_create")
+        self.handle = h.value
+
+    def collect(self) -> dict:
+        lib = load_library()
+        ms = (ctypes.c_double * NUM_STAGES)()
+        cnt = (ctypes.c_int64 * NUM_STAGES)()
+        _check(lib.mca_profiler_collect(self.handle, ms, cnt, NUM_STAGES), "mca_profiler_collect")
+        return {STAGES[i]: (ms[i], cnt[i]) for i in range(NUM_STAGES)}
+
+    def close(self):
+        if self.handle:
+            load_library().mca_profiler_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

@@ -1,0 +1,273 @@
+// C ABI of libmca: argument checks, workspace layout, stage launches, profiler.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <new>
+#include <vector>
+
+#include "../../include/mca.h"
+#include "mca_kernels.h"
+
+namespace {
+
+thread_local char g_last_error[512] = "";
+
+mca_status fail(mca_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  std::vsnprintf(g_last_error, sizeof(g_last_error), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+mca_status ok() {
+  g_last_error[0] = '\0';
+  return MCA_OK;
+}
+
+constexpr int64_t kMaxDin = 2048;
+constexpr int64_t kMaxDout = 2048;
+constexpr int64_t kMaxTokens = int64_t(1) << 30;
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
+
+struct Layout {
+  size_t colmax, row_max, row_inv, henc, sat_list, counters, total;
+};
+
+Layout layout_for(const mca_forward_desc& d) {
+  const size_t tokens = size_t(d.batch) * size_t(d.seq);
+  const size_t d_out = size_t(d.heads) * 64;
+  const size_t helem = d.dtype == MCA_BF16 ? 2 : 4;
+  Layout L;
+  size_t off = 0;
+  L.colmax = off;   off = align256(off + 4 * tokens);
+  L.row_max = off;  off = align256(off + 4 * tokens * size_t(d.heads));
+  L.row_inv = off;  off = align256(off + 4 * tokens * size_t(d.heads));
+  L.henc = off;     off = align256(off + helem * tokens * d_out);
+  L.sat_list = off; off = align256(off + 4 * tokens);
+  L.counters = off; off = align256(off + 16);
+  L.total = off;
+  return L;
+}
+
+mca_status check_desc(const mca_forward_desc* d) {
+  if (!d) return fail(MCA_ERR_INVALID_ARGUMENT, "desc is NULL");
+  if (d->batch < 1 || d->seq < 1 || d->heads < 1 || d->d_in < 1 || d->d_head < 1)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "batch, seq, heads, d_head and d_in must be >= 1");
+  if (d->reserved != 0) return fail(MCA_ERR_INVALID_ARGUMENT, "reserved field must be 0");
+  if (d->dtype != MCA_F32 && d->dtype != MCA_BF16)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "dtype %d is not MCA_F32 or MCA_BF16", d->dtype);
+  if (!std::isfinite(d->alpha) || !(d->alpha > 0.0))
+    return fail(MCA_ERR_INVALID_ARGUMENT, "alpha must be finite and > 0 (got %g)", d->alpha);
+  if (d->seq > (int64_t(1) << 24) || d->batch > (int64_t(1) << 24) || d->heads > 1024 ||
+      d->batch * d->seq > kMaxTokens)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "batch * seq too large");
+  if (d->d_head != 64) return fail(MCA_ERR_UNSUPPORTED, "d_head must be 64 (got %lld)", (long long)d->d_head);
+  const int64_t d_out = d->heads * 64;
+  if (d_out % 256 != 0 || d_out > kMaxDout)
+    return fail(MCA_ERR_UNSUPPORTED, "heads * 64 must be a multiple of 256 and <= %lld (got %lld)",
+                (long long)kMaxDout, (long long)d_out);
+  if (d->d_in > kMaxDin)
+    return fail(MCA_ERR_UNSUPPORTED, "d_in must be <= %lld (got %lld)", (long long)kMaxDin, (long long)d->d_in);
+  const void* opt[] = {d->seq_lens, d->r_in, d->colmax_out, d->sample_idx_out, d->sample_coef_out,
+                       d->encoded_out};
+  for (const void* p : opt)
+    if (p && !aligned16(p)) return fail(MCA_ERR_INVALID_ARGUMENT, "optional pointers must be 16-byte aligned");
+  return MCA_OK;
+}
+
+// ------------------------------------------------------------------ profiler
+constexpr int kMaxRecords = 65536;
+
+struct Profiler {
+  std::mutex mu;
+  std::vector<hipEvent_t> start, stop;
+  std::vector<int> stage;
+  int used = 0;
+  ~Profiler() {
+    for (auto e : start) (void)hipEventDestroy(e);
+    for (auto e : stop) (void)hipEventDestroy(e);
+  }
+};
+
+// Grows the event pool in chunks; returns the record slot or -1.
+int prof_slot(Profiler* pr, int stage) {
+  std::lock_guard<std::mutex> lk(pr->mu);
+  if (pr->used >= kMaxRecords) return -1;
+  if (pr->used == (int)pr->start.size()) {
+    for (int i = 0; i < 256; ++i) {
+      hipEvent_t a, b;
+      if (hipEventCreate(&a) != hipSuccess) return -1;
+      if (hipEventCreate(&b) != hipSuccess) {
+        (void)hipEventDestroy(a);
+        return -1;
+      }
+      pr->start.push_back(a);
+      pr->stop.push_back(b);
+      pr->stage.push_back(0);
+    }
+  }
+  pr->stage[pr->used] = stage;
+  return pr->used++;
+}
+
+template <typename F>
+mca_status run_stage(Profiler* pr, int stage, hipStream_t s, F&& launch) {
+  int slot = pr ? prof_slot(pr, stage) : -1;
+  if (slot >= 0 && hipEventRecord(pr->start[slot], s) != hipSuccess)
+    return fail(MCA_ERR_HIP, "hipEventRecord failed");
+  hipError_t e = launch();
+  if (e != hipSuccess)
+    return fail(MCA_ERR_HIP, "stage %s launch failed: %s", mca_stage_name(stage), hipGetErrorString(e));
+  if (slot >= 0 && hipEventRecord(pr->stop[slot], s) != hipSuccess)
+    return fail(MCA_ERR_HIP, "hipEventRecord failed");
+  return MCA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* mca_status_string(mca_status s) {
+  switch (s) {
+    case MCA_OK: return "MCA_OK";
+    case MCA_ERR_INVALID_ARGUMENT: return "MCA_ERR_INVALID_ARGUMENT";
+    case MCA_ERR_UNSUPPORTED: return "MCA_ERR_UNSUPPORTED";
+    case MCA_ERR_WORKSPACE_TOO_SMALL: return "MCA_ERR_WORKSPACE_TOO_SMALL";
+    case MCA_ERR_HIP: return "MCA_ERR_HIP";
+  }
+  return "MCA_ERR_UNKNOWN";
+}
+
+const char* mca_last_error(void) { return g_last_error; }
+
+int mca_num_stages(void) { return MCA_NUM_STAGES; }
+
+const char* mca_stage_name(int stage) {
+  static const char* names[MCA_NUM_STAGES] = {"clear", "scores_colmax", "encode", "dense_encode", "attn_out"};
+  return (stage >= 0 && stage < MCA_NUM_STAGES) ? names[stage] : "unknown";
+}
+
+mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes) {
+  mca_status st = check_desc(desc);
+  if (st != MCA_OK) return st;
+  if (!bytes) return fail(MCA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  *bytes = layout_for(*desc).total;
+  return ok();
+}
+
+mca_status mca_prepare_weights(const void* W_v, int32_t dtype, int64_t d_in, int64_t d_out, float* rownorm,
+                               void* stream) {
+  if (!W_v || !rownorm) return fail(MCA_ERR_INVALID_ARGUMENT, "W_v and rownorm must not be NULL");
+  if (dtype != MCA_F32 && dtype != MCA_BF16) return fail(MCA_ERR_INVALID_ARGUMENT, "bad dtype %d", dtype);
+  if (d_in < 1 || d_out < 1 || d_in > kMaxDin || d_out > (int64_t(1) << 20))
+    return fail(MCA_ERR_INVALID_ARGUMENT, "d_in must be in 1..%lld and d_out in 1..2^20", (long long)kMaxDin);
+  if (!aligned16(W_v) || !aligned16(rownorm)) return fail(MCA_ERR_INVALID_ARGUMENT, "pointers must be 16-byte aligned");
+  hipError_t e = mca::launch_rownorm(W_v, dtype == MCA_BF16, (int)d_in, (int)d_out, rownorm,
+                                     static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(MCA_ERR_HIP, "row-norm launch failed: %s", hipGetErrorString(e));
+  return ok();
+}
+
+mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, const void* K, const void* X,
+                                 const void* W_v, const float* rownorm, float* Y, int32_t* r, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  mca_status st = check_desc(desc);
+  if (st != MCA_OK) return st;
+  if (!Q || !K || !X || !W_v || !rownorm || !Y || !r || !workspace)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "Q, K, X, W_v, rownorm, Y, r and workspace must not be NULL");
+  const void* req[] = {Q, K, X, W_v, rownorm, Y, r, workspace};
+  for (const void* p : req)
+    if (!aligned16(p)) return fail(MCA_ERR_INVALID_ARGUMENT, "device pointers must be 16-byte aligned");
+  const Layout L = layout_for(*desc);
+  if (workspace_bytes < L.total)
+    return fail(MCA_ERR_WORKSPACE_TOO_SMALL, "workspace has %zu bytes, needs %zu", workspace_bytes, L.total);
+
+  mca::FwdParams p{};
+  p.B = (int)desc->batch;
+  p.n = (int)desc->seq;
+  p.H = (int)desc->heads;
+  p.d_in = (int)desc->d_in;
+  p.d_out = (int)(desc->heads * 64);
+  p.bf16 = desc->dtype == MCA_BF16;
+  p.alpha = desc->alpha;
+  p.seed_lo = (uint32_t)(desc->seed & 0xffffffffu);
+  p.seed_hi = (uint32_t)(desc->seed >> 32);
+  p.seq_lens = desc->seq_lens;
+  p.r_in = desc->r_in;
+  p.Q = Q;
+  p.K = K;
+  p.X = X;
+  p.W = W_v;
+  p.rownorm = rownorm;
+  p.Y = Y;
+  p.r = r;
+  char* ws = static_cast<char*>(workspace);
+  p.colmax_bits = reinterpret_cast<uint32_t*>(ws + L.colmax);
+  p.row_max = reinterpret_cast<float*>(ws + L.row_max);
+  p.row_inv_sum = reinterpret_cast<float*>(ws + L.row_inv);
+  p.Henc = ws + L.henc;
+  p.sat_list = reinterpret_cast<int32_t*>(ws + L.sat_list);
+  p.counters = reinterpret_cast<int32_t*>(ws + L.counters);
+  p.colmax_out = desc->colmax_out;
+  p.idx_out = desc->sample_idx_out;
+  p.coef_out = desc->sample_coef_out;
+  p.enc_out = desc->encoded_out;
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  Profiler* pr = static_cast<Profiler*>(desc->profiler);
+  if ((st = run_stage(pr, MCA_STAGE_CLEAR, s, [&] { return mca::launch_clear(p, s); })) != MCA_OK) return st;
+  if ((st = run_stage(pr, MCA_STAGE_SCORES_COLMAX, s, [&] { return mca::launch_scores_colmax(p, s); })) != MCA_OK)
+    return st;
+  if ((st = run_stage(pr, MCA_STAGE_ENCODE, s, [&] { return mca::launch_encode(p, s); })) != MCA_OK) return st;
+  if ((st = run_stage(pr, MCA_STAGE_DENSE_ENCODE, s, [&] { return mca::launch_dense_encode(p, s); })) != MCA_OK)
+    return st;
+  if ((st = run_stage(pr, MCA_STAGE_ATTN_OUT, s, [&] { return mca::launch_attn_out(p, s); })) != MCA_OK) return st;
+  return ok();
+}
+
+mca_status mca_profiler_create(void** handle) {
+  if (!handle) return fail(MCA_ERR_INVALID_ARGUMENT, "handle is NULL");
+  Profiler* pr = new (std::nothrow) Profiler();
+  if (!pr) return fail(MCA_ERR_INVALID_ARGUMENT, "out of host memory");
+  *handle = pr;
+  return ok();
+}
+
+mca_status mca_profiler_collect(void* handle, double* stage_ms, int64_t* launches, int n) {
+  if (!handle || !stage_ms || !launches || n < 0 || n > MCA_NUM_STAGES)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "bad profiler_collect arguments");
+  Profiler* pr = static_cast<Profiler*>(handle);
+  std::lock_guard<std::mutex> lk(pr->mu);
+  for (int i = 0; i < n; ++i) {
+    stage_ms[i] = 0.0;
+    launches[i] = 0;
+  }
+  for (int k = 0; k < pr->used; ++k) {
+    if (hipEventSynchronize(pr->stop[k]) != hipSuccess) return fail(MCA_ERR_HIP, "hipEventSynchronize failed");
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, pr->start[k], pr->stop[k]) != hipSuccess)
+      return fail(MCA_ERR_HIP, "hipEventElapsedTime failed");
+    const int st = pr->stage[k];
+    if (st < n) {
+      stage_ms[st] += ms;
+      launches[st] += 1;
+    }
+  }
+  pr->used = 0;
+  return ok();
+}
+
+mca_status mca_profiler_destroy(void* handle) {
+  delete static_cast<Profiler*>(handle);
+  return ok();
+}
+
+}  // extern "C"
