@@ -1,0 +1,259 @@
+#!/usr/bin/env python3
+"""Benchmark of the MCA attention forward pass on one MI355X.
+
+Workload: a BERT-base-shaped layer in bf16 (batch 32, seq 128, hidden 768, 12 heads of
+64), X ~ N(0, 1) with log-normal(0, 0.5) token scales, W ~ N(0, 0.02^2), Q = X W_q and
+K = X W_k, alpha = 0.4 (default error bound) and seed 0. One step = one
+mca_attention_forward call (scores + softmax statistics + column max, count rule,
+sampler, gather-accumulate, exact encoding of saturated tokens, Y = A H~) over the
+whole batch, inputs resident in HBM. The row norms of W_v are computed once per
+weight matrix and are timed separately (prepare_us).
+
+Prints one JSON line (stdout). Also reported: per-stage kernel times from HIP events
+recorded around each launch on the library's stream, the roofline of the dominant
+kernel, the same layer computed exactly (dense) with torch on the same GPU, the
+realised FLOP reduction, the loose/tight error-bound settings, and the CPU oracle
+timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "MCA attention tokens/s at 1 GPU; % HBM roofline (sampling) / % MFMA peak"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
+MFMA_FP32_PEAK_TFLOPS = 157.3
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def time_loop(fn, steps, warmup):
+    import torch
+
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0 = torch.cuda.Event(enable_timing=True)
+    t1 = torch.cuda.Event(enable_timing=True)
+    w0 = time.perf_counter()
+    t0.record()
+    for _ in range(steps):
+        fn()
+    t1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - w0
+    return t0.elapsed_time(t1) / steps, wall
+
+
+def stage_work(L, r, idx, elem):
+    """Algorithmic bytes and flops of every stage for one forward."""
+    B, n, d_in, d_out, H = L.batch, L.seq, L.d_in, L.d_out, L.heads
+    s_in, s_h = elem, elem  # input element size; H~ stored in the input dtype
+    lens = L.lens.astype(np.int64)
+    sampled = (r > 0) & (r < d_in)
+    sat = r == d_in
+    distinct = 0
+    draws = int(r[sampled].sum())
+    for b, j in zip(*np.nonzero(sampled)):
+        distinct += len(np.unique(idx[b, j, :r[b, j]]))
+    n_sampled, n_sat = int(sampled.sum()), int(sat.sum())
+    n_zero = B * n - n_sampled - n_sat
+    qk_flops = 2.0 * H * 64 * float(np.sum(n * lens))  # per pass over all (query, valid key) pairs
+    w = {}
+    w["clear"] = dict(bytes=4.0 * B * n, flops=0.0)
+    w["scores_colmax"] = dict(bytes=2.0 * B * n * d_out * s_in + 8.0 * B * H * n + 4.0 * B * n,
+                              flops=2 * qk_flops)
+    w["encode"] = dict(bytes=8.0 * B * n + 4.0 * d_in + n_sampled * (d_in * s_in + d_out * s_h)
+                       + distinct * d_out * s_in + n_zero * d_out * s_h,
+                       flops=2.0 * distinct * d_out,
+                       bytes_per_draw=8.0 * B * n + 4.0 * d_in + n_sampled * (d_in * s_in + d_out * s_h)
+                       + draws * d_out * s_in + n_zero * d_out * s_h)
+    w["dense_encode"] = dict(bytes=n_sat * (d_in * s_in + d_out * s_h) + (d_in * d_out * s_in if n_sat else 0),
+                             flops=2.0 * n_sat * d_in * d_out)
+    w["attn_out"] = dict(bytes=2.0 * B * n * d_out * s_in + B * n * d_out * s_h + 4.0 * B * n * d_out
+                         + 8.0 * B * H * n, flops=2 * qk_flops)
+    stats = dict(sampled_tokens=n_sampled, saturated_tokens=n_sat, draws=draws, distinct_rows=distinct)
+    return w, stats
+
+
+def dense_baseline(t, L, steps, warmup):
+    """The exact layer (Eq. 1) with torch on the same GPU: V = X W_v, softmax(Q K^T/8) V."""
+    import torch
+    import torch.nn.functional as F
+
+    B, n, H = L.batch, L.seq, L.heads
+    X2 = t["X"].reshape(B * n, L.d_in)
+    out = {}
+
+    def bmm_path():
+        V = (X2 @ t["Wv"]).view(B, n, H, 64)
+        q = t["Q"].view(B, n, H, 64).permute(0, 2, 1, 3).reshape(B * H, n, 64).contiguous()
+        kT = t["K"].view(B, n, H, 64).permute(0, 2, 3, 1).reshape(B * H, 64, n).contiguous()
+        v = V.permute(0, 2, 1, 3).reshape(B * H, n, 64).contiguous()
+        S = torch.bmm(q, kT).float() * 0.125
+        P = torch.softmax(S, dim=-1).to(q.dtype)
+        return torch.bmm(P, v)
+
+    ms, _ = time_loop(bmm_path, steps, warmup)
+    out["bmm_softmax_ms"] = ms
+    if np.all(L.lens == n):
+        try:
+            from torch.nn.attention import SDPBackend, sdpa_kernel
+
+            q4 = t["Q"].view(B, n, H, 64).transpose(1, 2).contiguous()
+            k4 = t["K"].view(B, n, H, 64).transpose(1, 2).contiguous()
+
+            def sdpa_path():
+                V = (X2 @ t["Wv"]).view(B, n, H, 64).transpose(1, 2).contiguous()
+                with sdpa_kernel([SDPBackend.FLASH_ATTENTION, SDPBackend.EFFICIENT_ATTENTION]):
+                    return F.scaled_dot_product_attention(q4, k4, V)
+
+            ms2, _ = time_loop(sdpa_path, steps, warmup)
+            out["sdpa_ms"] = ms2
+        except Exception as e:  # backend unavailable on this build: keep the bmm path
+            out["sdpa_error"] = str(e)[:200]
+    out["ms"] = min(v for k, v in out.items() if k.endswith("_ms"))
+    out["tokens_per_s"] = float(L.tokens) / (out["ms"] * 1e-3)
+    return out
+
+
+def cpu_baseline(L, alpha, seed, seconds):
+    """The CPU oracle (fp64 numpy), as it stands, on the same layer."""
+    import oracle
+
+    try:
+        from threadpoolctl import threadpool_info
+
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = 1
+    reps, t0 = 0, time.perf_counter()
+    while True:
+        oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed)
+        reps += 1
+        el = time.perf_counter() - t0
+        if el >= seconds or el * (reps + 1) / reps > 3 * seconds:
+            break
+    return {"value": L.tokens * reps / el, "unit": "tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"the whole workload ({L.batch} sequences, {L.tokens} tokens) x {reps} run(s), "
+                      f"{el:.1f} s; python loops plus numpy BLAS with {threads} thread(s)"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--alpha", type=float, default=0.4)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=10.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true", help="skip dense baseline and other alphas")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU layout is a "
+              "design note, not a measured path", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2201_12854_amd as mca
+    from paper_2201_12854_amd import workloads as wl
+
+    if not torch.cuda.is_available():
+        raise SystemExit("bench.py needs a HIP device")
+    dev = torch.device("cuda:0")
+    L = wl.bert_base_bf16()
+    elem = 2
+    t = {k: torch.from_numpy(getattr(L, k)).to(dev).to(torch.bfloat16).contiguous() for k in ("Q", "K", "X", "Wv")}
+    lens = torch.from_numpy(L.lens.astype(np.int32)).to(dev)
+    log(f"workload {L.name}: B={L.batch} n={L.seq} d={L.d_in} H={L.heads} tokens={L.tokens} alpha={args.alpha}")
+
+    rho = mca.prepare_weights(t["Wv"])
+    prep_ms, _ = time_loop(lambda: mca.prepare_weights(t["Wv"], rho), 20, 3)
+
+    plan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], rho, args.alpha, args.seed, heads=L.heads, seq_lens=lens)
+    ms, wall = time_loop(plan.run, args.steps, args.warmup)
+    value = L.tokens / (ms * 1e-3)
+    log(f"mca forward: {ms * 1e3:.1f} us/step, {value:.4g} tokens/s (wall {wall:.2f} s)")
+
+    # per-stage kernel times: HIP events around every launch on the library's stream
+    prof = mca.Profiler()
+    pplan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], rho, args.alpha, args.seed, heads=L.heads,
+                            seq_lens=lens, profiler=prof)
+    for _ in range(args.warmup):
+        pplan.run()
+    torch.cuda.synchronize()
+    prof.collect()
+    for _ in range(args.steps):
+        pplan.run()
+    torch.cuda.synchronize()
+    st = prof.collect()
+    stage_us = {k: (v[0] / max(v[1], 1)) * 1e3 for k, v in st.items()}
+    log("stage us: " + ", ".join(f"{k}={v:.1f}" for k, v in stage_us.items()))
+
+    ex = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], rho, args.alpha, args.seed, heads=L.heads,
+                               seq_lens=lens, export_samples=True)
+    torch.cuda.synchronize()
+    r = ex.r.cpu().numpy()
+    idx = ex.sample_idx.cpu().numpy()
+    work, wstats = stage_work(L, r, idx, elem)
+    dom = max((k for k in stage_us if k != "clear"), key=lambda k: stage_us[k])
+    dur = stage_us[dom] * 1e-6
+    if dom == "encode":
+        ach = work[dom]["bytes"] / dur / 1e9
+        roof = {"kernel": "k_encode", "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": ach / HBM_PEAK_GBS, "traffic": None,
+                "achieved_counting_every_draw": work[dom]["bytes_per_draw"] / dur / 1e9}
+    else:
+        ach = work[dom]["flops"] / dur / 1e12
+        roof = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": ach / MFMA_BF16_PEAK_TFLOPS, "traffic": None}
+    roof["avg_launch_us"] = stage_us[dom]
+    stages = {k: {"us": stage_us[k], "GB/s": work[k]["bytes"] / (stage_us[k] * 1e-6) / 1e9 if stage_us[k] else None,
+                  "TFLOP/s": work[k]["flops"] / (stage_us[k] * 1e-6) / 1e12 if stage_us[k] else None}
+              for k in stage_us}
+    d_in = L.d_in
+    red = {"vs_dense_xw": float(L.tokens * d_in) / float(np.sum(r)),
+           "mean_r": float(r[r > 0].mean()), "saturated_frac": float((r == d_in).mean()), **wstats}
+
+    record = {"metric": METRIC, "value": value, "unit": "tokens/s", "n_gpus": 1, "steps": args.steps,
+              "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+              "vs_baseline": None, "dtype": "bf16",
+              "data": "synthetic: seeded BERT-base-shaped layer, random N(0, 0.02^2) weights",
+              "config": {"workload": L.name, "batch": L.batch, "seq_len": L.seq, "hidden": L.d_in,
+                         "heads": L.heads, "d_head": 64, "alpha": args.alpha, "seed": args.seed,
+                         "token_scale": "lognormal(0, 0.5)"},
+              "roofline": roof, "stages": stages, "prepare_us": prep_ms * 1e3, "flop_reduction": red}
+
+    if not args.no_extras:
+        dense = dense_baseline(t, L, args.steps, args.warmup)
+        record["dense_exact"] = dense
+        record["speedup_vs_dense"] = dense["ms"] / ms
+        log(f"dense exact layer: {dense['ms'] * 1e3:.1f} us/step")
+        other = {}
+        for a in (1.0, 0.2):
+            p2 = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], rho, a, args.seed, heads=L.heads, seq_lens=lens)
+            ms_a, _ = time_loop(p2.run, args.steps, args.warmup)
+            other[str(a)] = {"ms_per_step": ms_a, "tokens_per_s": L.tokens / (ms_a * 1e-3)}
+        record["other_alphas"] = other
+    if not args.no_cpu_baseline:
+        record["cpu_baseline"] = cpu_baseline(L, args.alpha, args.seed, args.cpu_seconds)
+        log(f"cpu oracle: {record['cpu_baseline']['value']:.4g} tokens/s")
+    print(json.dumps(record), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -244,3 +244,33 @@ class Profiler:
             self.close()
         except Exception:
             pass
+
+
+class ForwardPlan:
+    """A forward call with every argument bound once (tensors, workspace, outputs,
+    stream), so that ``run()`` is a single C call: for timing loops and serving."""
+
+    def __init__(self, Q, K, X, W_v, rownorm, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
+                 r_in=None, profiler=None):
+        import torch
+
+        lib = load_library()
+        B, n, d_in = X.shape
+        d_out = W_v.shape[1]
+        dev = X.device
+        self._keep = (Q, K, X, W_v, rownorm, seq_lens, r_in)
+        self.desc = make_desc(B, n, heads, d_in, _dtype_code(X), alpha, seed, seq_lens=seq_lens, r_in=r_in,
+                              profiler=profiler)
+        ws = workspace_size(self.desc)
+        self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
+        self.Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)
+        self.r = torch.empty((B, n), dtype=torch.int32, device=dev)
+        self._fn = lib.mca_attention_forward
+        self._args = (ctypes.byref(self.desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(rownorm), _ptr(self.Y),
+                      _ptr(self.r), _ptr(self.workspace), self.workspace.numel())
+        self._stream = _stream_handle(dev)
+
+    def run(self):
+        st = self._fn(*self._args, self._stream)
+        if st != MCA_OK:
+            _check(st, "mca_attention_forward")
