@@ -181,17 +181,17 @@ def main():
     lens = torch.from_numpy(L.lens.astype(np.int32)).to(dev)
     log(f"workload {L.name}: B={L.batch} n={L.seq} d={L.d_in} H={L.heads} tokens={L.tokens} alpha={args.alpha}")
 
-    rho = mca.prepare_weights(t["Wv"])
-    prep_ms, _ = time_loop(lambda: mca.prepare_weights(t["Wv"], rho), 20, 3)
+    prep = mca.prepare_weights(t["Wv"])
+    prep_ms, _ = time_loop(lambda: mca.prepare_weights(t["Wv"], prep), 20, 3)
 
-    plan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], rho, args.alpha, args.seed, heads=L.heads, seq_lens=lens)
+    plan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads, seq_lens=lens)
     ms, wall = time_loop(plan.run, args.steps, args.warmup)
     value = L.tokens / (ms * 1e-3)
     log(f"mca forward: {ms * 1e3:.1f} us/step, {value:.4g} tokens/s (wall {wall:.2f} s)")
 
     # per-stage kernel times: HIP events around every launch on the library's stream
     prof = mca.Profiler()
-    pplan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], rho, args.alpha, args.seed, heads=L.heads,
+    pplan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
                             seq_lens=lens, profiler=prof)
     for _ in range(args.warmup):
         pplan.run()
@@ -204,7 +204,7 @@ def main():
     stage_us = {k: (v[0] / max(v[1], 1)) * 1e3 for k, v in st.items()}
     log("stage us: " + ", ".join(f"{k}={v:.1f}" for k, v in stage_us.items()))
 
-    ex = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], rho, args.alpha, args.seed, heads=L.heads,
+    ex = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
                                seq_lens=lens, export_samples=True)
     torch.cuda.synchronize()
     r = ex.r.cpu().numpy()
@@ -245,7 +245,7 @@ def main():
         log(f"dense exact layer: {dense['ms'] * 1e3:.1f} us/step")
         other = {}
         for a in (1.0, 0.2):
-            p2 = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], rho, a, args.seed, heads=L.heads, seq_lens=lens)
+            p2 = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, a, args.seed, heads=L.heads, seq_lens=lens)
             ms_a, _ = time_loop(p2.run, args.steps, args.warmup)
             other[str(a)] = {"ms_per_step": ms_a, "tokens_per_s": L.tokens / (ms_a * 1e-3)}
         record["other_alphas"] = other

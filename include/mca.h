@@ -51,12 +51,11 @@ typedef enum mca_dtype {
 
 /* Stages of the forward pass, in launch order (profiler slots). */
 typedef enum mca_stage {
-  MCA_STAGE_CLEAR = 0,          /* zero the column-max and saturated-token counters */
-  MCA_STAGE_SCORES_COLMAX = 1,  /* softmax(Q K^T / 8) row statistics and column max */
-  MCA_STAGE_ENCODE = 2,         /* count rule, sampler and gather-accumulate */
-  MCA_STAGE_DENSE_ENCODE = 3,   /* exact x_j W_v for saturated tokens (MFMA) */
-  MCA_STAGE_ATTN_OUT = 4,       /* Y = A H~ (MFMA) */
-  MCA_NUM_STAGES = 5
+  MCA_STAGE_SCORES_COLMAX = 0,  /* softmax(Q K^T / 8) row statistics and column-max partials */
+  MCA_STAGE_ENCODE = 1,         /* count rule, sampler and gather-accumulate */
+  MCA_STAGE_DENSE_ENCODE = 2,   /* exact x_j W_v for saturated tokens (MFMA) */
+  MCA_STAGE_ATTN_OUT = 3,       /* Y = A H~ (MFMA) */
+  MCA_NUM_STAGES = 4
 } mca_stage;
 
 /*
@@ -102,18 +101,25 @@ typedef struct mca_forward_desc {
 } mca_forward_desc;
 
 /*
- * Row norms of the value projection, computed once per weight matrix and cached
- * (Sec. "Formulation of Sampling Probability": the per-row statistic of W can be
- * embedded in the model or cached).
- *   rownorm[i] = float32(sqrt(sum_c W_v[i, c]^2)), squares summed in float64 in
- *   column order c = 0, 1, ..., d_out-1, one IEEE square root, one rounding to
- *   float32. Bitwise reproducible.
- * W_v: device [d_in, d_out] of `dtype`; rownorm: device [d_in] float32 (written).
+ * Prepared weights: the per-row statistic of the value projection, computed once per
+ * weight matrix and cached (Sec. "Formulation of Sampling Probability": it can be
+ * embedded in the model or cached), plus a copy of W_v laid out for the exact MFMA path.
+ * Layout of the `prepared` buffer (device, caller-owned):
+ *   offset 0:                        rownorm float32 [d_in]
+ *                                    rownorm[i] = float32(sqrt(sum_c W_v[i, c]^2)), squares
+ *                                    summed in float64 in column order c = 0 .. d_out-1, one
+ *                                    IEEE square root, one rounding to float32 (bitwise
+ *                                    reproducible)
+ *   offset round_up(4 d_in, 256):    W_v^T [d_out][round_up(d_in, 32)] in `dtype`, zero padded
+ * mca_prepared_size gives the buffer size (host only). mca_prepare_weights fills it from
+ * W_v (device [d_in, d_out] of `dtype`).
  * Errors: MCA_ERR_INVALID_ARGUMENT for null pointers, sizes < 1, d_in > 2048,
- * d_out > 1 << 20 or a bad dtype; MCA_ERR_HIP if the launch fails.
+ * d_out > 1 << 20, a bad dtype, misalignment or prepared_bytes smaller than
+ * mca_prepared_size; MCA_ERR_HIP if a launch fails.
  */
+mca_status mca_prepared_size(int32_t dtype, int64_t d_in, int64_t d_out, size_t* bytes);
 mca_status mca_prepare_weights(const void* W_v, int32_t dtype, int64_t d_in, int64_t d_out,
-                               float* rownorm, void* stream);
+                               void* prepared, size_t prepared_bytes, void* stream);
 
 /*
  * Bytes of device workspace mca_attention_forward needs for `desc` (host only, no
@@ -134,8 +140,8 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  *           an inverse-CDF search; H~[j] = x_j W_v exactly when r_j = d_in; H~[j] = 0
  *           when r_j = 0 or x_j = 0.
  *   Y_h   = A_h H~_h (per head column slice)
- * Inputs Q, K, X, W_v (device, `desc->dtype`), rownorm (device [d_in] from
- * mca_prepare_weights). Outputs Y (device [B, n, d_out] float32) and r (device [B, n]
+ * Inputs Q, K, X, W_v (device, `desc->dtype`) and `prepared` (filled by
+ * mca_prepare_weights from this W_v with the same dtype and sizes). Outputs Y (device [B, n, d_out] float32) and r (device [B, n]
  * int32). Rows of Y for padded queries are computed by the same formula.
  * `workspace` must hold at least mca_workspace_size bytes; its contents on entry do not
  * matter and are overwritten.
@@ -145,7 +151,7 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  * MCA_ERR_HIP.
  */
 mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, const void* K,
-                                 const void* X, const void* W_v, const float* rownorm,
+                                 const void* X, const void* W_v, const void* prepared,
                                  float* Y, int32_t* r, void* workspace, size_t workspace_bytes,
                                  void* stream);
 

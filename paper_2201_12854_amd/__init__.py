@@ -6,4 +6,4 @@ package only marshals arguments to it (``binding``) and builds it
 """
 from .binding import (ForwardPlan, ForwardResult, MCAError, Profiler, attention_forward,  # noqa: F401
                       load_library,
-                      prepare_weights, status_string, workspace_size, make_desc)
+                      prepare_weights, prepared_size, rownorm, status_string, workspace_size, make_desc)

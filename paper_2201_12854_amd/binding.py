@@ -22,8 +22,8 @@ MCA_ERR_WORKSPACE_TOO_SMALL = 3
 MCA_ERR_HIP = 4
 MCA_F32 = 0
 MCA_BF16 = 1
-NUM_STAGES = 5
-STAGES = ("clear", "scores_colmax", "encode", "dense_encode", "attn_out")
+NUM_STAGES = 4
+STAGES = ("scores_colmax", "encode", "dense_encode", "attn_out")
 
 
 class ForwardDesc(ctypes.Structure):
@@ -65,7 +65,9 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         raise RuntimeError(f"{path} is not built; run paper_2201_12854_amd.build_lib.build() first")
     lib = ctypes.CDLL(path)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
-    lib.mca_prepare_weights.argtypes = [vp, i32, i64, i64, vp, vp]
+    lib.mca_prepared_size.argtypes = [i32, i64, i64, ctypes.POINTER(sz)]
+    lib.mca_prepared_size.restype = ctypes.c_int
+    lib.mca_prepare_weights.argtypes = [vp, i32, i64, i64, vp, sz, vp]
     lib.mca_prepare_weights.restype = ctypes.c_int
     lib.mca_workspace_size.argtypes = [ctypes.POINTER(ForwardDesc), ctypes.POINTER(sz)]
     lib.mca_workspace_size.restype = ctypes.c_int
@@ -139,18 +141,31 @@ def workspace_size(desc: ForwardDesc) -> int:
     return out.value
 
 
-def prepare_weights(W_v, rownorm=None):
-    """rownorm[i] = ||W_v[i, :]|| (float32) for W_v [d_in, d_out] on a HIP device."""
+def prepared_size(dtype_code: int, d_in: int, d_out: int) -> int:
+    out = ctypes.c_size_t(0)
+    _check(load_library().mca_prepared_size(dtype_code, d_in, d_out, ctypes.byref(out)), "mca_prepared_size")
+    return out.value
+
+
+def prepare_weights(W_v, prepared=None):
+    """Prepared weights of W_v [d_in, d_out] (a uint8 device buffer): the row norms
+    float32 [d_in] at offset 0 (see ``rownorm``) and a transposed copy for the MFMA path."""
     import torch
 
     lib = load_library()
     if W_v.dim() != 2 or not W_v.is_cuda or not W_v.is_contiguous():
         raise ValueError("W_v must be a contiguous 2-D device tensor [d_in, d_out]")
-    if rownorm is None:
-        rownorm = torch.empty(W_v.shape[0], dtype=torch.float32, device=W_v.device)
-    _check(lib.mca_prepare_weights(_ptr(W_v), _dtype_code(W_v), W_v.shape[0], W_v.shape[1], _ptr(rownorm),
-                                   _stream_handle(W_v.device)), "mca_prepare_weights")
-    return rownorm
+    nbytes = prepared_size(_dtype_code(W_v), W_v.shape[0], W_v.shape[1])
+    if prepared is None:
+        prepared = torch.empty(nbytes, dtype=torch.uint8, device=W_v.device)
+    _check(lib.mca_prepare_weights(_ptr(W_v), _dtype_code(W_v), W_v.shape[0], W_v.shape[1], _ptr(prepared),
+                                   prepared.numel(), _stream_handle(W_v.device)), "mca_prepare_weights")
+    return prepared
+
+
+def rownorm(prepared, d_in: int):
+    """The float32 row norms held at the start of a prepared-weights buffer."""
+    return prepared[: 4 * d_in].view(dtype=__import__("torch").float32)
 
 
 @dataclass
@@ -163,13 +178,13 @@ class ForwardResult:
     encoded: object = None
 
 
-def attention_forward(Q, K, X, W_v, rownorm, alpha: float, seed: int = 0, *, heads: int,
+def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int,
                       seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
                       workspace=None, out=None, profiler=None) -> ForwardResult:
     """One MCA forward pass through libmca on the current HIP stream.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
-    all bfloat16, contiguous, on one device. rownorm from ``prepare_weights``.
+    all bfloat16, contiguous, on one device. ``prepared`` from ``prepare_weights(W_v)``.
     seq_lens: optional int32 [B]. r_in: optional int32 [B, n] overriding the count
     rule. ``export`` also returns the column max and H~ (float32); ``export_samples``
     the per-draw indices and coefficients ([B, n, d_in], first r_j entries valid).
@@ -187,8 +202,9 @@ def attention_forward(Q, K, X, W_v, rownorm, alpha: float, seed: int = 0, *, hea
             raise ValueError(f"{name} must be a contiguous {X.dtype} tensor on {dev}")
     if Q.shape != (B, n, heads * 64) or K.shape != Q.shape or W_v.shape[0] != d_in or d_out != heads * 64:
         raise ValueError("shape mismatch: Q, K [B, n, heads*64], X [B, n, d_in], W_v [d_in, heads*64]")
-    if rownorm.dtype != torch.float32 or rownorm.shape != (d_in,) or rownorm.device != dev:
-        raise ValueError("rownorm must be float32 [d_in] on the same device")
+    if prepared.dtype != torch.uint8 or prepared.device != dev or \
+            prepared.numel() < prepared_size(dt, d_in, d_out):
+        raise ValueError("prepared must be the uint8 buffer prepare_weights(W_v) returns")
     if seq_lens is not None and (seq_lens.dtype != torch.int32 or seq_lens.shape != (B,)):
         raise ValueError("seq_lens must be int32 [B]")
     if r_in is not None and (r_in.dtype != torch.int32 or r_in.numel() != B * n or not r_in.is_contiguous()):
@@ -211,7 +227,7 @@ def attention_forward(Q, K, X, W_v, rownorm, alpha: float, seed: int = 0, *, hea
         r = torch.empty((B, n), dtype=torch.int32, device=dev)
     else:
         Y, r = out
-    _check(lib.mca_attention_forward(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(rownorm),
+    _check(lib.mca_attention_forward(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(prepared),
                                      _ptr(Y), _ptr(r), _ptr(workspace), workspace.numel(),
                                      _stream_handle(dev)), "mca_attention_forward")
     res.Y, res.r = Y, r
@@ -250,7 +266,7 @@ class ForwardPlan:
     """A forward call with every argument bound once (tensors, workspace, outputs,
     stream), so that ``run()`` is a single C call: for timing loops and serving."""
 
-    def __init__(self, Q, K, X, W_v, rownorm, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
+    def __init__(self, Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
                  r_in=None, profiler=None):
         import torch
 
@@ -258,7 +274,7 @@ class ForwardPlan:
         B, n, d_in = X.shape
         d_out = W_v.shape[1]
         dev = X.device
-        self._keep = (Q, K, X, W_v, rownorm, seq_lens, r_in)
+        self._keep = (Q, K, X, W_v, prepared, seq_lens, r_in)
         self.desc = make_desc(B, n, heads, d_in, _dtype_code(X), alpha, seed, seq_lens=seq_lens, r_in=r_in,
                               profiler=profiler)
         ws = workspace_size(self.desc)
@@ -266,7 +282,7 @@ class ForwardPlan:
         self.Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)
         self.r = torch.empty((B, n), dtype=torch.int32, device=dev)
         self._fn = lib.mca_attention_forward
-        self._args = (ctypes.byref(self.desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(rownorm), _ptr(self.Y),
+        self._args = (ctypes.byref(self.desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(prepared), _ptr(self.Y),
                       _ptr(self.r), _ptr(self.workspace), self.workspace.numel())
         self._stream = _stream_handle(dev)
 

@@ -1,6 +1,6 @@
 // Attention stages of the MCA forward pass on gfx950:
-//   scores + row softmax statistics + column max   (softmax(a Q K^T), a = 1/8, and
-//                                                    max A[:, j] of Eq. 8/9)
+//   scores + row softmax statistics + column max   (softmax(a Q K^T), a = 1/8, and the
+//                                                    per-block part of max A[:, j], Eq. 8/9)
 //   Y = A H~                                        ("Y = AH", Sec. "Self-Attention
 //                                                    Mechanisms"; Eq. 5 outer sum)
 // Both kernels rebuild the score tiles from Q and K with one shared routine, so the
@@ -159,9 +159,9 @@ __global__ __launch_bounds__(kThreads) void k_scores_colmax(FwdParams p) {
   // Sweep 1: online row max and row sum of exp over the valid keys.
   float M = -INFINITY, L = 0.f;
   for (int kt = 0; kt < ntiles; ++kt) {
-    __syncthreads();
+    lds_barrier();
     stage_rows(Ks, Kb, d_out, kt * kTile, n, tid);
-    __syncthreads();
+    lds_barrier();
     f32x4_t acc[4];
     score_tile(acc, Ks, qf, r16, g);
     float mx = -INFINITY;
@@ -196,13 +196,15 @@ __global__ __launch_bounds__(kThreads) void k_scores_colmax(FwdParams p) {
     p.row_inv_sum[o] = inv;
   }
 
-  // Sweep 2: probabilities of valid queries, max over this block's queries per key,
-  // then one atomic max per key (A >= 0, so the float bit pattern orders like the value).
+  // Sweep 2: probabilities of valid queries and their max over this block's queries per
+  // key, stored in this block's slot of the token's column-max partials (every slot is
+  // written, so nothing needs clearing and no atomics are involved).
   const bool qvalid = q < len;
+  float* part = p.colmax_part + (int64_t)b * n * p.nparts + h * p.qtiles + qt;
   for (int kt = 0; kt < ntiles; ++kt) {
-    __syncthreads();
+    lds_barrier();
     stage_rows(Ks, Kb, d_out, kt * kTile, n, tid);
-    __syncthreads();
+    lds_barrier();
     f32x4_t acc[4];
     score_tile(acc, Ks, qf, r16, g);
 #pragma unroll
@@ -217,11 +219,11 @@ __global__ __launch_bounds__(kThreads) void k_scores_colmax(FwdParams p) {
         a = fmaxf(a, __shfl_xor(a, 8, kWave));
         if (r16 == 0) cm[wave][16 * s + 4 * g + i] = a;
       }
-    __syncthreads();
+    lds_barrier();
     if (tid < kTile) {
       const float v = fmaxf(fmaxf(cm[0][tid], cm[1][tid]), fmaxf(cm[2][tid], cm[3][tid]));
       const int key = kt * kTile + tid;
-      if (key < len && v > 0.f) atomicMax(p.colmax_bits + (int64_t)b * n + key, __float_as_uint(v));
+      if (key < n) part[(int64_t)key * p.nparts] = v;
     }
   }
 }
@@ -256,11 +258,11 @@ __global__ __launch_bounds__(kThreads) void k_attn_out(FwdParams p) {
   for (int c = 0; c < 4; ++c) y[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 
   for (int kt = 0; kt < ntiles; ++kt) {
-    __syncthreads();
+    lds_barrier();
     stage_rows(Ks, Kb, d_out, kt * kTile, n, tid);
     if constexpr (BF) stage_rows_transposed(Vs, Vb, d_out, kt * kTile, n, tid);
     else stage_rows(Vs, Vb, d_out, kt * kTile, n, tid);
-    __syncthreads();
+    lds_barrier();
     f32x4_t acc[4];
     score_tile(acc, Ks, qf, r16, g);
 #pragma unroll
@@ -312,20 +314,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_out(FwdParams p) {
   }
 }
 
-__global__ void k_clear(uint32_t* colmax_bits, int64_t count, int32_t* counters) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < count) colmax_bits[i] = 0u;
-  if (i < 4) counters[i] = 0;
-}
-
 }  // namespace
-
-hipError_t launch_clear(const FwdParams& p, hipStream_t s) {
-  const int64_t count = (int64_t)p.B * p.n;
-  const int64_t blocks = (count + 255) / 256;
-  hipLaunchKernelGGL(k_clear, dim3((unsigned)blocks), dim3(256), 0, s, p.colmax_bits, count, p.counters);
-  return hipGetLastError();
-}
 
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
   const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B);

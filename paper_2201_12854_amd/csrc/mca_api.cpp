@@ -9,7 +9,7 @@
 #include <new>
 #include <vector>
 
-#include "../../include/mca.h"
+#include "mca.h"
 #include "mca_kernels.h"
 
 namespace {
@@ -38,7 +38,8 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t colmax, row_max, row_inv, henc, sat_list, counters, total;
+  size_t colmax_part, row_max, row_inv, henc, total;
+  int qtiles, nparts;
 };
 
 Layout layout_for(const mca_forward_desc& d) {
@@ -46,13 +47,13 @@ Layout layout_for(const mca_forward_desc& d) {
   const size_t d_out = size_t(d.heads) * 64;
   const size_t helem = d.dtype == MCA_BF16 ? 2 : 4;
   Layout L;
+  L.qtiles = (int)((d.seq + mca::kQueryTile - 1) / mca::kQueryTile);
+  L.nparts = (int)(d.heads * L.qtiles);
   size_t off = 0;
-  L.colmax = off;   off = align256(off + 4 * tokens);
-  L.row_max = off;  off = align256(off + 4 * tokens * size_t(d.heads));
-  L.row_inv = off;  off = align256(off + 4 * tokens * size_t(d.heads));
-  L.henc = off;     off = align256(off + helem * tokens * d_out);
-  L.sat_list = off; off = align256(off + 4 * tokens);
-  L.counters = off; off = align256(off + 16);
+  L.colmax_part = off; off = align256(off + 4 * tokens * size_t(L.nparts));
+  L.row_max = off;     off = align256(off + 4 * tokens * size_t(d.heads));
+  L.row_inv = off;     off = align256(off + 4 * tokens * size_t(d.heads));
+  L.henc = off;        off = align256(off + helem * tokens * d_out);
   L.total = off;
   return L;
 }
@@ -151,7 +152,7 @@ const char* mca_last_error(void) { return g_last_error; }
 int mca_num_stages(void) { return MCA_NUM_STAGES; }
 
 const char* mca_stage_name(int stage) {
-  static const char* names[MCA_NUM_STAGES] = {"clear", "scores_colmax", "encode", "dense_encode", "attn_out"};
+  static const char* names[MCA_NUM_STAGES] = {"scores_colmax", "encode", "dense_encode", "attn_out"};
   return (stage >= 0 && stage < MCA_NUM_STAGES) ? names[stage] : "unknown";
 }
 
@@ -163,27 +164,44 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes) {
   return ok();
 }
 
-mca_status mca_prepare_weights(const void* W_v, int32_t dtype, int64_t d_in, int64_t d_out, float* rownorm,
-                               void* stream) {
-  if (!W_v || !rownorm) return fail(MCA_ERR_INVALID_ARGUMENT, "W_v and rownorm must not be NULL");
+static mca_status check_weights(int32_t dtype, int64_t d_in, int64_t d_out) {
   if (dtype != MCA_F32 && dtype != MCA_BF16) return fail(MCA_ERR_INVALID_ARGUMENT, "bad dtype %d", dtype);
   if (d_in < 1 || d_out < 1 || d_in > kMaxDin || d_out > (int64_t(1) << 20))
     return fail(MCA_ERR_INVALID_ARGUMENT, "d_in must be in 1..%lld and d_out in 1..2^20", (long long)kMaxDin);
-  if (!aligned16(W_v) || !aligned16(rownorm)) return fail(MCA_ERR_INVALID_ARGUMENT, "pointers must be 16-byte aligned");
-  hipError_t e = mca::launch_rownorm(W_v, dtype == MCA_BF16, (int)d_in, (int)d_out, rownorm,
+  return MCA_OK;
+}
+
+mca_status mca_prepared_size(int32_t dtype, int64_t d_in, int64_t d_out, size_t* bytes) {
+  mca_status st = check_weights(dtype, d_in, d_out);
+  if (st != MCA_OK) return st;
+  if (!bytes) return fail(MCA_ERR_INVALID_ARGUMENT, "bytes is NULL");
+  *bytes = mca::prepared_bytes(dtype == MCA_BF16, d_in, d_out);
+  return ok();
+}
+
+mca_status mca_prepare_weights(const void* W_v, int32_t dtype, int64_t d_in, int64_t d_out, void* prepared,
+                               size_t prepared_bytes, void* stream) {
+  if (!W_v || !prepared) return fail(MCA_ERR_INVALID_ARGUMENT, "W_v and prepared must not be NULL");
+  mca_status st = check_weights(dtype, d_in, d_out);
+  if (st != MCA_OK) return st;
+  if (!aligned16(W_v) || !aligned16(prepared)) return fail(MCA_ERR_INVALID_ARGUMENT, "pointers must be 16-byte aligned");
+  const size_t need = mca::prepared_bytes(dtype == MCA_BF16, d_in, d_out);
+  if (prepared_bytes < need)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "prepared buffer has %zu bytes, needs %zu", prepared_bytes, need);
+  hipError_t e = mca::launch_prepare(W_v, dtype == MCA_BF16, (int)d_in, (int)d_out, prepared,
                                      static_cast<hipStream_t>(stream));
-  if (e != hipSuccess) return fail(MCA_ERR_HIP, "row-norm launch failed: %s", hipGetErrorString(e));
+  if (e != hipSuccess) return fail(MCA_ERR_HIP, "weight preparation launch failed: %s", hipGetErrorString(e));
   return ok();
 }
 
 mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, const void* K, const void* X,
-                                 const void* W_v, const float* rownorm, float* Y, int32_t* r, void* workspace,
+                                 const void* W_v, const void* prepared, float* Y, int32_t* r, void* workspace,
                                  size_t workspace_bytes, void* stream) {
   mca_status st = check_desc(desc);
   if (st != MCA_OK) return st;
-  if (!Q || !K || !X || !W_v || !rownorm || !Y || !r || !workspace)
-    return fail(MCA_ERR_INVALID_ARGUMENT, "Q, K, X, W_v, rownorm, Y, r and workspace must not be NULL");
-  const void* req[] = {Q, K, X, W_v, rownorm, Y, r, workspace};
+  if (!Q || !K || !X || !W_v || !prepared || !Y || !r || !workspace)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "Q, K, X, W_v, prepared, Y, r and workspace must not be NULL");
+  const void* req[] = {Q, K, X, W_v, prepared, Y, r, workspace};
   for (const void* p : req)
     if (!aligned16(p)) return fail(MCA_ERR_INVALID_ARGUMENT, "device pointers must be 16-byte aligned");
   const Layout L = layout_for(*desc);
@@ -197,6 +215,9 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.d_in = (int)desc->d_in;
   p.d_out = (int)(desc->heads * 64);
   p.bf16 = desc->dtype == MCA_BF16;
+  p.qtiles = L.qtiles;
+  p.nparts = L.nparts;
+  p.din_pad = (int)mca::prepared_din_pad(desc->d_in);
   p.alpha = desc->alpha;
   p.seed_lo = (uint32_t)(desc->seed & 0xffffffffu);
   p.seed_hi = (uint32_t)(desc->seed >> 32);
@@ -206,16 +227,15 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.K = K;
   p.X = X;
   p.W = W_v;
-  p.rownorm = rownorm;
+  p.rownorm = static_cast<const float*>(prepared);
+  p.Wt = static_cast<const char*>(prepared) + mca::prepared_wt_offset(desc->d_in);
   p.Y = Y;
   p.r = r;
   char* ws = static_cast<char*>(workspace);
-  p.colmax_bits = reinterpret_cast<uint32_t*>(ws + L.colmax);
+  p.colmax_part = reinterpret_cast<float*>(ws + L.colmax_part);
   p.row_max = reinterpret_cast<float*>(ws + L.row_max);
   p.row_inv_sum = reinterpret_cast<float*>(ws + L.row_inv);
   p.Henc = ws + L.henc;
-  p.sat_list = reinterpret_cast<int32_t*>(ws + L.sat_list);
-  p.counters = reinterpret_cast<int32_t*>(ws + L.counters);
   p.colmax_out = desc->colmax_out;
   p.idx_out = desc->sample_idx_out;
   p.coef_out = desc->sample_coef_out;
@@ -223,7 +243,6 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   Profiler* pr = static_cast<Profiler*>(desc->profiler);
-  if ((st = run_stage(pr, MCA_STAGE_CLEAR, s, [&] { return mca::launch_clear(p, s); })) != MCA_OK) return st;
   if ((st = run_stage(pr, MCA_STAGE_SCORES_COLMAX, s, [&] { return mca::launch_scores_colmax(p, s); })) != MCA_OK)
     return st;
   if ((st = run_stage(pr, MCA_STAGE_ENCODE, s, [&] { return mca::launch_encode(p, s); })) != MCA_OK) return st;

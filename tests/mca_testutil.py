@@ -32,19 +32,19 @@ def to_device(L, dev):
     return t
 
 
-def run_gpu(L, dev, alpha, seed, *, r_in=None, export=True, export_samples=False, tensors=None, rho=None):
+def run_gpu(L, dev, alpha, seed, *, r_in=None, export=True, export_samples=False, tensors=None, prep=None):
     import torch
 
     import paper_2201_12854_amd as mca
 
     t = tensors or to_device(L, dev)
-    if rho is None:
-        rho = mca.prepare_weights(t["Wv"])
+    if prep is None:
+        prep = mca.prepare_weights(t["Wv"])
     rin = None if r_in is None else torch.from_numpy(np.ascontiguousarray(r_in, dtype=np.int32)).to(dev)
-    out = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], rho, alpha, seed, heads=L.heads,
+    out = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], prep, alpha, seed, heads=L.heads,
                                 seq_lens=t["lens"], r_in=rin, export=export, export_samples=export_samples)
     torch.cuda.synchronize()
-    res = {"Y": out.Y.cpu().numpy(), "r": out.r.cpu().numpy(), "rho": rho.cpu().numpy()}
+    res = {"Y": out.Y.cpu().numpy(), "r": out.r.cpu().numpy(), "rho": mca.rownorm(prep, L.d_in).cpu().numpy()}
     if export:
         res["m"] = out.colmax.cpu().numpy()
         res["H"] = out.encoded.cpu().numpy()

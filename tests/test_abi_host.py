@@ -32,7 +32,7 @@ def test_header_enums_match_binding():
     text = open(HEADER).read()
     for name, val in [("MCA_OK", 0), ("MCA_ERR_INVALID_ARGUMENT", 1), ("MCA_ERR_UNSUPPORTED", 2),
                       ("MCA_ERR_WORKSPACE_TOO_SMALL", 3), ("MCA_ERR_HIP", 4), ("MCA_F32", 0), ("MCA_BF16", 1),
-                      ("MCA_NUM_STAGES", 5)]:
+                      ("MCA_NUM_STAGES", 4)]:
         assert re.search(rf"\b{name}\s*=\s*{val}\b", text), name
     # struct layout: the binding's ctypes mirror has the header's field order
     body = re.search(r"typedef struct mca_forward_desc \{(.*?)\} mca_forward_desc;", text, re.S).group(1)
@@ -46,8 +46,8 @@ def test_status_strings_and_stages():
     for code, name in [(0, "MCA_OK"), (1, "MCA_ERR_INVALID_ARGUMENT"), (2, "MCA_ERR_UNSUPPORTED"),
                        (3, "MCA_ERR_WORKSPACE_TOO_SMALL"), (4, "MCA_ERR_HIP")]:
         assert mca.status_string(code) == name
-    assert lib.mca_num_stages() == 5
-    assert [lib.mca_stage_name(i).decode() for i in range(5)] == list(binding.STAGES)
+    assert lib.mca_num_stages() == 4
+    assert [lib.mca_stage_name(i).decode() for i in range(4)] == list(binding.STAGES)
     assert lib.mca_stage_name(99).decode() == "unknown"
 
 
@@ -62,13 +62,21 @@ def test_workspace_size_formula():
     B, n, H, d = 2, 128, 12, 768
     got = mca.workspace_size(_desc())
     tokens = B * n
+    parts = H * ((n + 63) // 64)
 
     def a(v):
         return (v + 255) // 256 * 256
 
-    expect = a(4 * tokens) + 2 * a(4 * tokens * H) + a(2 * tokens * H * 64) + a(4 * tokens) + a(16)
+    expect = a(4 * tokens * parts) + 2 * a(4 * tokens * H) + a(2 * tokens * H * 64)
     assert got == expect
     assert mca.workspace_size(_desc(dtype_code=0)) > got  # float32 H~
+
+
+def test_prepared_size_formula():
+    for dt, esz in ((0, 4), (1, 2)):
+        for d_in, d_out in ((768, 768), (45, 256), (1, 64)):
+            off = (4 * d_in + 255) // 256 * 256
+            assert mca.prepared_size(dt, d_in, d_out) == off + d_out * ((d_in + 31) // 32 * 32) * esz
 
 
 @pytest.mark.parametrize("field,value,status", [
@@ -117,11 +125,17 @@ def test_forward_rejects_null_and_small_workspace_without_device_work():
 def test_prepare_weights_rejects_bad_arguments():
     lib = mca.load_library()
     fake = ctypes.c_void_p(0x10000)
-    assert lib.mca_prepare_weights(None, 0, 8, 8, fake, None) == binding.MCA_ERR_INVALID_ARGUMENT
-    assert lib.mca_prepare_weights(fake, 3, 8, 8, fake, None) == binding.MCA_ERR_INVALID_ARGUMENT
-    assert lib.mca_prepare_weights(fake, 0, 0, 8, fake, None) == binding.MCA_ERR_INVALID_ARGUMENT
-    assert lib.mca_prepare_weights(fake, 0, 4097, 8, fake, None) == binding.MCA_ERR_INVALID_ARGUMENT
-    assert lib.mca_prepare_weights(fake, 0, 8, 8, ctypes.c_void_p(0x10002), None) == binding.MCA_ERR_INVALID_ARGUMENT
+    big = 1 << 30
+    assert lib.mca_prepare_weights(None, 0, 8, 8, fake, big, None) == binding.MCA_ERR_INVALID_ARGUMENT
+    assert lib.mca_prepare_weights(fake, 3, 8, 8, fake, big, None) == binding.MCA_ERR_INVALID_ARGUMENT
+    assert lib.mca_prepare_weights(fake, 0, 0, 8, fake, big, None) == binding.MCA_ERR_INVALID_ARGUMENT
+    assert lib.mca_prepare_weights(fake, 0, 4097, 8, fake, big, None) == binding.MCA_ERR_INVALID_ARGUMENT
+    assert lib.mca_prepare_weights(fake, 0, 8, 8, ctypes.c_void_p(0x10002), big, None) == \
+        binding.MCA_ERR_INVALID_ARGUMENT
+    need = mca.prepared_size(0, 8, 8)
+    assert lib.mca_prepare_weights(fake, 0, 8, 8, fake, need - 1, None) == binding.MCA_ERR_INVALID_ARGUMENT
+    with pytest.raises(binding.MCAError):
+        mca.prepared_size(5, 8, 8)
 
 
 def test_profiler_lifecycle_without_device_work():

@@ -60,21 +60,28 @@ def _full_check(L, dev, alpha, seed, *, check_e2e_y=True):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-def test_rownorm_bitexact(dev, dtype):
+def test_prepared_weights_bitexact(dev, dtype):
     import torch
 
     import paper_2201_12854_amd as mca
 
     for (d_in, d_out, scale) in [(96, 256, 0.02), (768, 768, 0.02), (1024, 1024, 1.0), (7, 1000, 1e-20),
-                                 (2048, 2048, 3.0)]:
-        print(f"[case] rownorm {dtype} {d_in}x{d_out}", flush=True)
+                                 (2048, 2048, 3.0), (45, 512, 1.0)]:
+        print(f"[case] prepare {dtype} {d_in}x{d_out}", flush=True)
         W = (scale * np.random.default_rng(d_in).standard_normal((d_in, d_out))).astype(np.float32)
         if dtype == "bf16":
             W = wl.round_to_bf16(W)
         tdt = torch.float32 if dtype == "f32" else torch.bfloat16
-        rho = mca.prepare_weights(torch.from_numpy(W).to(dev).to(tdt))
+        Wd = torch.from_numpy(W).to(dev).to(tdt)
+        prep = mca.prepare_weights(Wd)
         torch.cuda.synchronize()
-        assert np.array_equal(rho.cpu().numpy(), oracle.row_norms(W))
+        assert np.array_equal(mca.rownorm(prep, d_in).cpu().numpy(), oracle.row_norms(W))
+        # the transposed, zero-padded copy used by the exact MFMA path
+        off = (4 * d_in + 255) // 256 * 256
+        pad = (d_in + 31) // 32 * 32
+        esz = 4 if dtype == "f32" else 2
+        raw = prep[off: off + d_out * pad * esz].view(tdt).view(d_out, pad).float().cpu().numpy()
+        assert np.array_equal(raw[:, :d_in], W.T) and np.all(raw[:, d_in:] == 0)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
