@@ -3,16 +3,28 @@
 //                                                    per-block part of max A[:, j], Eq. 8/9)
 //   Y = A H~                                        ("Y = AH", Sec. "Self-Attention
 //                                                    Mechanisms"; Eq. 5 outer sum)
-// Both kernels rebuild the score tiles from Q and K with one shared routine, so the
-// attention probabilities that set the sample counts are bitwise the ones multiplied
-// into H~. A is never written to memory.
+// Both kernels rebuild the score tiles from Q and K with one shared routine and the same
+// row statistics, so the attention probabilities that set the sample counts are bitwise
+// the ones multiplied into H~. A is never written to memory.
 //
 // Tiling: one block = 4 waves = 64 queries of one (batch row, head); a wave owns 16
-// queries. Keys are processed in tiles of 64 staged in LDS. Scores are computed
-// transposed, S^T = K Q^T, with 16x16 MFMA tiles (bf16 16x16x32 or fp32 16x16x4), so
-// after the score MFMA lane l holds the scores of query (l % 16) for keys
-// 16 s + 4 (l / 16) + i (s, i = 0..3): exactly the A-operand layout of the P V MFMA,
-// with no data movement between the two products.
+// queries. Keys come in tiles of 64 staged in LDS. Scores are computed transposed,
+// S^T = K Q^T, with 16x16 MFMA tiles (bf16 16x16x32 or fp32 16x16x4), so after the score
+// MFMA lane l holds the scores of query (l % 16) for keys 16 s + 4 (l / 16) + i
+// (s, i = 0..3): exactly the A-operand layout of the P V MFMA, with no data movement
+// between the two products.
+//
+// Two variants of each kernel:
+//   resident (padded length <= 64 NT keys): every K (and H~) tile of the sequence is
+//     loaded at once behind one barrier and all scores stay in registers, so the
+//     statistics and the column max come from a single pass;
+//   streaming (longer sequences): tiles are double buffered in LDS with the next tile
+//     prefetched into registers; the score pass sweeps twice (online statistics, then
+//     probabilities).
+// Rows past the padded length are read from the last row instead of being zero-filled:
+// their scores are masked and their probabilities are exactly 0. Tile loads are
+// unconditional (a tile index past the last valid tile is clamped to it), which keeps the
+// tiles in registers and the load stream free of divergent branches.
 #include "mca_device.h"
 #include "mca_kernels.h"
 
@@ -26,6 +38,7 @@ constexpr int kStrideF = kDHead + 4;     // LDS row stride of fp32 tiles (elemen
 
 template <int BF> struct Elem { using T = float; };
 template <> struct Elem<1> { using T = uint16_t; };
+template <int BF> constexpr int stride_of() { return BF ? kStrideBf : kStrideF; }
 
 // ------------------------------------------------------------------ Q fragments
 // The wave's 16 queries as the B operand of S^T = K Q^T.
@@ -33,20 +46,16 @@ template <int BF> struct QFrag;
 template <> struct QFrag<1> { bf16x8_t v[2]; };   // d = 32 ks + 8 g + (0..7)
 template <> struct QFrag<0> { float v[16]; };      // d = 16 g + t
 
-__device__ __forceinline__ void load_qfrag(QFrag<1>& f, const uint16_t* qrow, bool valid, int g) {
+__device__ __forceinline__ void load_qfrag(QFrag<1>& f, const uint16_t* qrow, int g) {
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (valid) u = *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g);
-    f.v[ks] = __builtin_bit_cast(bf16x8_t, u);
-  }
+  for (int ks = 0; ks < 2; ++ks)
+    f.v[ks] = __builtin_bit_cast(bf16x8_t, *reinterpret_cast<const uint4*>(qrow + 32 * ks + 8 * g));
 }
 
-__device__ __forceinline__ void load_qfrag(QFrag<0>& f, const float* qrow, bool valid, int g) {
+__device__ __forceinline__ void load_qfrag(QFrag<0>& f, const float* qrow, int g) {
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
-    float4 u = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (valid) u = *reinterpret_cast<const float4*>(qrow + 16 * g + 4 * c);
+    const float4 u = *reinterpret_cast<const float4*>(qrow + 16 * g + 4 * c);
     f.v[4 * c + 0] = u.x;
     f.v[4 * c + 1] = u.y;
     f.v[4 * c + 2] = u.z;
@@ -54,46 +63,77 @@ __device__ __forceinline__ void load_qfrag(QFrag<0>& f, const float* qrow, bool 
   }
 }
 
-// ------------------------------------------------------------------ LDS staging
-// Rows key0 .. key0+63 of a [*, d_out] matrix (head column slice at `base`), rows >= n
-// zero-filled, into a row-major LDS tile.
-__device__ __forceinline__ void stage_rows(uint16_t* lds, const uint16_t* base, int64_t ld,
-                                           int key0, int n, int tid) {
-#pragma unroll
-  for (int v = tid; v < kTile * 8; v += kThreads) {
-    const int key = v >> 3, ch = v & 7;
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (key0 + key < n) u = *reinterpret_cast<const uint4*>(base + (int64_t)(key0 + key) * ld + 8 * ch);
-    *reinterpret_cast<uint4*>(lds + key * kStrideBf + 8 * ch) = u;
-  }
+// ------------------------------------------------------------------ tiles in flight
+// A 64-row x 64-column tile of a [*, d_out] matrix (the head's column slice) held in
+// registers between its global load and its LDS store: 16-byte vectors v0, v1 (bf16) or
+// v0..v3 (fp32) per thread; vector v of the tile is row v / R, chunk v % R (R vectors per
+// row). Row indices past the padded length are clamped to the last row. (Plain members,
+// no arrays: the tiles are carried across loop iterations and must stay in registers.)
+struct TileRegs {
+  uint4 v0, v1, v2, v3;
+};
+
+template <int BF>
+__device__ __forceinline__ uint4 tile_vec_load(const void* base, int64_t ld, int key0, int n, int v) {
+  using T = typename Elem<BF>::T;
+  constexpr int R = BF ? 8 : 16;
+  const int key = min(key0 + v / R, n - 1);
+  return *reinterpret_cast<const uint4*>(static_cast<const T*>(base) + (int64_t)key * ld + (v % R) * (16 / (int)sizeof(T)));
 }
 
-__device__ __forceinline__ void stage_rows(float* lds, const float* base, int64_t ld, int key0,
-                                           int n, int tid) {
-#pragma unroll
-  for (int v = tid; v < kTile * 16; v += kThreads) {
-    const int key = v >> 4, ch = v & 15;
-    float4 u = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (key0 + key < n) u = *reinterpret_cast<const float4*>(base + (int64_t)(key0 + key) * ld + 4 * ch);
-    *reinterpret_cast<float4*>(lds + key * kStrideF + 4 * ch) = u;
+template <int BF>
+__device__ __forceinline__ TileRegs tile_load(const void* base, int64_t ld, int key0, int n, int tid) {
+  TileRegs t;
+  t.v0 = tile_vec_load<BF>(base, ld, key0, n, tid);
+  t.v1 = tile_vec_load<BF>(base, ld, key0, n, tid + kThreads);
+  if constexpr (!BF) {
+    t.v2 = tile_vec_load<BF>(base, ld, key0, n, tid + 2 * kThreads);
+    t.v3 = tile_vec_load<BF>(base, ld, key0, n, tid + 3 * kThreads);
+  } else {
+    t.v2 = t.v3 = make_uint4(0, 0, 0, 0);
+  }
+  return t;
+}
+
+// row-major LDS tile [key][d]
+template <int BF>
+__device__ __forceinline__ void tile_vec_store(uint4 u, typename Elem<BF>::T* lds, int v) {
+  constexpr int R = BF ? 8 : 16;
+  *reinterpret_cast<uint4*>(lds + (v / R) * stride_of<BF>() + (v % R) * (BF ? 8 : 4)) = u;
+}
+
+template <int BF>
+__device__ __forceinline__ void tile_store(const TileRegs& t, typename Elem<BF>::T* lds, int tid) {
+  tile_vec_store<BF>(t.v0, lds, tid);
+  tile_vec_store<BF>(t.v1, lds, tid + kThreads);
+  if constexpr (!BF) {
+    tile_vec_store<BF>(t.v2, lds, tid + 2 * kThreads);
+    tile_vec_store<BF>(t.v3, lds, tid + 3 * kThreads);
   }
 }
 
 // bf16 H~ tile stored transposed ([column][key]) so that the B operand of the P V MFMA
 // (8 keys of one column per lane) is two 8-byte LDS reads.
-__device__ __forceinline__ void stage_rows_transposed(uint16_t* lds, const uint16_t* base, int64_t ld,
-                                                      int key0, int n, int tid) {
-#pragma unroll
-  for (int v = tid; v < kTile * 8; v += kThreads) {
-    const int key = v >> 3, ch = v & 7;
-    uint4 u = make_uint4(0, 0, 0, 0);
-    if (key0 + key < n) u = *reinterpret_cast<const uint4*>(base + (int64_t)(key0 + key) * ld + 8 * ch);
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      lds[(8 * ch + 2 * e) * kStrideBf + key] = (uint16_t)(w[e] & 0xffffu);
-      lds[(8 * ch + 2 * e + 1) * kStrideBf + key] = (uint16_t)(w[e] >> 16);
-    }
+__device__ __forceinline__ void vec_store_transposed(uint4 u, uint16_t* lds, int v) {
+  const int key = v >> 3, ch = v & 7;
+  uint16_t* col = lds + (8 * ch) * kStrideBf + key;
+  col[0 * kStrideBf] = (uint16_t)(u.x & 0xffffu);
+  col[1 * kStrideBf] = (uint16_t)(u.x >> 16);
+  col[2 * kStrideBf] = (uint16_t)(u.y & 0xffffu);
+  col[3 * kStrideBf] = (uint16_t)(u.y >> 16);
+  col[4 * kStrideBf] = (uint16_t)(u.z & 0xffffu);
+  col[5 * kStrideBf] = (uint16_t)(u.z >> 16);
+  col[6 * kStrideBf] = (uint16_t)(u.w & 0xffffu);
+  col[7 * kStrideBf] = (uint16_t)(u.w >> 16);
+}
+
+template <int BF>
+__device__ __forceinline__ void tile_store_v(const TileRegs& t, typename Elem<BF>::T* lds, int tid) {
+  if constexpr (BF) {
+    vec_store_transposed(t.v0, lds, tid);
+    vec_store_transposed(t.v1, lds, tid + kThreads);
+  } else {
+    tile_store<0>(t, lds, tid);
   }
 }
 
@@ -137,196 +177,381 @@ __device__ __forceinline__ int valid_len(const FwdParams& p, int b) {
   return min(max(len, 1), p.n);
 }
 
-// ------------------------------------------------------------------ kernels
-template <int BF>
-__global__ __launch_bounds__(kThreads) void k_scores_colmax(FwdParams p) {
+// P V for one 64-key tile: acc holds the probabilities (S^T layout), Vs the H~ tile.
+__device__ __forceinline__ void pv_tile(f32x4_t y[4], const f32x4_t acc[4], const uint16_t* Vs, int r16, int g) {
+  // 32 keys per MFMA: k-slots 0..3 = keys 32 pp + 4 g + (0..3), 4..7 = keys 32 pp + 16 + 4 g + (0..3)
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    const uint4 pa = make_uint4(pack_bf16x2(acc[2 * pp][0], acc[2 * pp][1]), pack_bf16x2(acc[2 * pp][2], acc[2 * pp][3]),
+                                pack_bf16x2(acc[2 * pp + 1][0], acc[2 * pp + 1][1]),
+                                pack_bf16x2(acc[2 * pp + 1][2], acc[2 * pp + 1][3]));
+    const bf16x8_t a = __builtin_bit_cast(bf16x8_t, pa);
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const uint16_t* vrow = Vs + (16 * c + r16) * kStrideBf + 32 * pp + 4 * g;
+      const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
+      const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+      const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
+      y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bv, y[c], 0, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void pv_tile(f32x4_t y[4], const f32x4_t acc[4], const float* Vs, int r16, int g) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const float* vrow = Vs + (16 * s + 4 * g + i) * kStrideF + r16;
+#pragma unroll
+      for (int c = 0; c < 4; ++c) y[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[s][i], vrow[16 * c], y[c], 0, 0, 0);
+    }
+}
+
+struct BlockCtx {
+  int qt, h, b, tid, wave, lane, r16, g, n, d_out, len, q, ntl;
+};
+
+__device__ __forceinline__ BlockCtx block_ctx(const FwdParams& p) {
+  BlockCtx c;
+  c.qt = blockIdx.x;
+  c.h = blockIdx.y;
+  c.b = blockIdx.z;
+  c.tid = threadIdx.x;
+  c.wave = c.tid >> 6;
+  c.lane = c.tid & 63;
+  c.r16 = c.lane & 15;
+  c.g = c.lane >> 4;
+  c.n = p.n;
+  c.d_out = p.d_out;
+  c.len = valid_len(p, c.b);
+  c.q = c.qt * kTile + c.wave * 16 + c.r16;
+  c.ntl = (c.len + kTile - 1) / kTile;  // tiles past the valid length are all masked
+  return c;
+}
+
+// Max over the wave's 16 queries (the 16 lanes of a row, same l / 16) of a probability.
+__device__ __forceinline__ float max_over_queries(float a) { return row16_max(a); }
+
+// Writes Y rows of the wave's queries: y[cc][i] = Y[query 4 g + i][column 16 cc + l % 16].
+__device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, const f32x4_t y[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int row = c.qt * kTile + c.wave * 16 + 4 * c.g + i;
+    if (row < c.n) {
+      float* yrow = p.Y + ((int64_t)c.b * c.n + row) * c.d_out + c.h * kDHead + c.r16;
+#pragma unroll
+      for (int cc = 0; cc < 4; ++cc) yrow[16 * cc] = y[cc][i];
+    }
+  }
+}
+
+// ------------------------------------------------------------------ score pass
+// Resident variant: all ntl <= NT tiles in LDS and all scores in registers.
+template <int BF, int NT>
+__global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
   using T = typename Elem<BF>::T;
-  constexpr int kStride = BF ? kStrideBf : kStrideF;
-  __shared__ __align__(16) T Ks[kTile * kStride];
-  __shared__ float cm[4][kTile];
+  constexpr int S = stride_of<BF>();
+  __shared__ __align__(16) T Ks[NT][kTile * S];
+  __shared__ float cm[NT][4][kTile];
+  const BlockCtx c = block_ctx(p);
+  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
 
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
-  const int n = p.n, d_out = p.d_out, len = valid_len(p, b);
-  const int q = qt * kTile + wave * 16 + r16;
-  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)b * n * d_out + h * kDHead;
-  const T* Kb = static_cast<const T*>(p.K) + (int64_t)b * n * d_out + h * kDHead;
-
+  TileRegs kr[NT];
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt) kr[kt] = tile_load<BF>(Kb, c.d_out, min(kt, c.ntl - 1) * kTile, c.n, c.tid);
   QFrag<BF> qf;
-  load_qfrag(qf, Qb + (int64_t)q * d_out, q < n, g);
-  const int ntiles = (len + kTile - 1) / kTile;  // tiles past the valid length are all masked
+  load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt)
+    if (kt < c.ntl) tile_store<BF>(kr[kt], Ks[kt], c.tid);
+  lds_barrier();
+
+  // row statistics: exact max over the valid keys, then the sum of exp
+  f32x4_t acc[NT][4];
+  float M = -INFINITY;
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt) {
+    if (kt < c.ntl) {
+      score_tile(acc[kt], Ks[kt], qf, c.r16, c.g);
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt * kTile + 16 * s + 4 * c.g + i;
+          if (key < c.len) M = fmaxf(M, logit(acc[kt][s][i]));
+        }
+    }
+  }
+  M = fmaxf(M, __shfl_xor(M, 16, kWave));
+  M = fmaxf(M, __shfl_xor(M, 32, kWave));
+  // e = exp(logit - M), kept in acc for the column max (masked keys: 0)
+  float L = 0.f;
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt) {
+    if (kt < c.ntl) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt * kTile + 16 * s + 4 * c.g + i;
+          const float e = key < c.len ? expf(__fsub_rn(logit(acc[kt][s][i]), M)) : 0.f;
+          acc[kt][s][i] = e;
+          L += e;
+        }
+    }
+  }
+  L += __shfl_xor(L, 16, kWave);
+  L += __shfl_xor(L, 32, kWave);
+  const float inv = 1.0f / L;
+  if (c.g == 0 && c.q < c.n) {
+    const int64_t o = ((int64_t)c.b * p.H + c.h) * c.n + c.q;
+    p.row_max[o] = M;
+    p.row_inv_sum[o] = inv;
+  }
+
+  // column max of the valid queries, every tile in its own LDS slot (one barrier)
+  const bool qvalid = c.q < c.len;
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt) {
+    if (kt < c.ntl) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int key = kt * kTile + 16 * s + 4 * c.g + i;
+          // probability = e * (1/L), bitwise the value prob() gives in the output pass
+          const float a = max_over_queries((qvalid && key < c.len) ? __fmul_rn(acc[kt][s][i], inv) : 0.f);
+          if (c.r16 == 0) cm[kt][c.wave][16 * s + 4 * c.g + i] = a;
+        }
+    }
+  }
+  lds_barrier();
+  float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
+  for (int e = c.tid; e < c.ntl * kTile; e += kThreads) {
+    const int kt = e / kTile, k = e % kTile;
+    const float v = fmaxf(fmaxf(cm[kt][0][k], cm[kt][1][k]), fmaxf(cm[kt][2][k], cm[kt][3][k]));
+    if (e < c.n) part[(int64_t)e * p.nparts] = v;
+  }
+}
+
+// Streaming variant: tiles double buffered, next tile prefetched; two sweeps.
+template <int BF>
+__global__ __launch_bounds__(kThreads) void k_scores_stream(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  constexpr int S = stride_of<BF>();
+  __shared__ __align__(16) T Ks[2][kTile * S];
+  __shared__ float cm[2][4][kTile];
+  const BlockCtx c = block_ctx(p);
+  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  QFrag<BF> qf;
+  load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
 
   // Sweep 1: online row max and row sum of exp over the valid keys.
   float M = -INFINITY, L = 0.f;
-  for (int kt = 0; kt < ntiles; ++kt) {
+  TileRegs kr;
+  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  for (int kt = 0; kt < c.ntl; ++kt) {
+    T* buf = Ks[kt & 1];
+    tile_store<BF>(kr, buf, c.tid);
     lds_barrier();
-    stage_rows(Ks, Kb, d_out, kt * kTile, n, tid);
-    lds_barrier();
+    kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
     f32x4_t acc[4];
-    score_tile(acc, Ks, qf, r16, g);
+    score_tile(acc, buf, qf, c.r16, c.g);
     float mx = -INFINITY;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kt * kTile + 16 * s + 4 * g + i;
-        const float lg = key < len ? logit(acc[s][i]) : -INFINITY;
+        const int key = kt * kTile + 16 * s + 4 * c.g + i;
+        const float lg = key < c.len ? logit(acc[s][i]) : -INFINITY;
         acc[s][i] = lg;
         mx = fmaxf(mx, lg);
       }
     mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float Mn = fmaxf(M, mx);
+    const float Mn = fmaxf(M, mx);  // finite: key 0 of tile 0 is valid
     float sum = 0.f;
-    if (Mn != -INFINITY) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
+    for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) sum += expf(__fsub_rn(acc[s][i], Mn));
-    }
+      for (int i = 0; i < 4; ++i) sum += expf(__fsub_rn(acc[s][i], Mn));  // masked: exp(-inf) = 0
     sum += __shfl_xor(sum, 16, kWave);
     sum += __shfl_xor(sum, 32, kWave);
     L = (M == -INFINITY ? 0.f : __fmul_rn(L, expf(__fsub_rn(M, Mn)))) + sum;
     M = Mn;
   }
   const float inv = 1.0f / L;
-  if (g == 0 && q < n) {
-    const int64_t o = ((int64_t)b * p.H + h) * n + q;
+  if (c.g == 0 && c.q < c.n) {
+    const int64_t o = ((int64_t)c.b * p.H + c.h) * c.n + c.q;
     p.row_max[o] = M;
     p.row_inv_sum[o] = inv;
   }
 
-  // Sweep 2: probabilities of valid queries and their max over this block's queries per
-  // key, stored in this block's slot of the token's column-max partials (every slot is
-  // written, so nothing needs clearing and no atomics are involved).
-  const bool qvalid = q < len;
-  float* part = p.colmax_part + (int64_t)b * n * p.nparts + h * p.qtiles + qt;
-  for (int kt = 0; kt < ntiles; ++kt) {
+  // Sweep 2: probabilities and the per-key column max of this block's valid queries.
+  // Tile kt uses K buffer kt & 1 and column-max slot kt & 1; the barrier after its LDS
+  // store also orders the reads of tile kt - 2's slot before this tile's writes.
+  lds_barrier();  // sweep 1 is done with both K buffers
+  float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
+  const bool qvalid = c.q < c.len;
+  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  for (int kt = 0; kt < c.ntl; ++kt) {
+    T* buf = Ks[kt & 1];
+    float (*cmk)[kTile] = cm[kt & 1];
+    tile_store<BF>(kr, buf, c.tid);
     lds_barrier();
-    stage_rows(Ks, Kb, d_out, kt * kTile, n, tid);
-    lds_barrier();
+    kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
     f32x4_t acc[4];
-    score_tile(acc, Ks, qf, r16, g);
+    score_tile(acc, buf, qf, c.r16, c.g);
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kt * kTile + 16 * s + 4 * g + i;
-        float a = (qvalid && key < len) ? prob(logit(acc[s][i]), M, inv) : 0.f;
-        a = fmaxf(a, __shfl_xor(a, 1, kWave));
-        a = fmaxf(a, __shfl_xor(a, 2, kWave));
-        a = fmaxf(a, __shfl_xor(a, 4, kWave));
-        a = fmaxf(a, __shfl_xor(a, 8, kWave));
-        if (r16 == 0) cm[wave][16 * s + 4 * g + i] = a;
+        const int key = kt * kTile + 16 * s + 4 * c.g + i;
+        const float a = max_over_queries((qvalid && key < c.len) ? prob(logit(acc[s][i]), M, inv) : 0.f);
+        if (c.r16 == 0) cmk[c.wave][16 * s + 4 * c.g + i] = a;
       }
     lds_barrier();
-    if (tid < kTile) {
-      const float v = fmaxf(fmaxf(cm[0][tid], cm[1][tid]), fmaxf(cm[2][tid], cm[3][tid]));
-      const int key = kt * kTile + tid;
-      if (key < n) part[(int64_t)key * p.nparts] = v;
+    if (c.tid < kTile) {
+      const float v = fmaxf(fmaxf(cmk[0][c.tid], cmk[1][c.tid]), fmaxf(cmk[2][c.tid], cmk[3][c.tid]));
+      const int key = kt * kTile + c.tid;
+      if (key < c.n) part[(int64_t)key * p.nparts] = v;
     }
   }
 }
 
-template <int BF>
-__global__ __launch_bounds__(kThreads) void k_attn_out(FwdParams p) {
+// ------------------------------------------------------------------ Y = A H~
+template <int BF, int NT>
+__global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
   using T = typename Elem<BF>::T;
-  constexpr int kStride = BF ? kStrideBf : kStrideF;
-  __shared__ __align__(16) T Ks[kTile * kStride];
-  __shared__ __align__(16) T Vs[kTile * kStride];  // bf16: [column][key]; fp32: [key][column]
+  constexpr int S = stride_of<BF>();
+  __shared__ __align__(16) T Ks[NT][kTile * S];
+  __shared__ __align__(16) T Vs[NT][kTile * S];  // bf16: [column][key]; fp32: [key][column]
+  const BlockCtx c = block_ctx(p);
+  const int64_t off = (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const T* Qb = static_cast<const T*>(p.Q) + off;
+  const T* Kb = static_cast<const T*>(p.K) + off;
+  const T* Vb = static_cast<const T*>(p.Henc) + off;
 
-  const int qt = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63, r16 = lane & 15, g = lane >> 4;
-  const int n = p.n, d_out = p.d_out, len = valid_len(p, b);
-  const int q = qt * kTile + wave * 16 + r16;
-  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)b * n * d_out + h * kDHead;
-  const T* Kb = static_cast<const T*>(p.K) + (int64_t)b * n * d_out + h * kDHead;
-  const T* Vb = static_cast<const T*>(p.Henc) + (int64_t)b * n * d_out + h * kDHead;
-
-  QFrag<BF> qf;
-  load_qfrag(qf, Qb + (int64_t)q * d_out, q < n, g);
-  float M = 0.f, inv = 0.f;
-  if (q < n) {
-    const int64_t o = ((int64_t)b * p.H + h) * n + q;
-    M = p.row_max[o];
-    inv = p.row_inv_sum[o];
+  TileRegs kr[NT], vr[NT];
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt) {
+    kr[kt] = tile_load<BF>(Kb, c.d_out, min(kt, c.ntl - 1) * kTile, c.n, c.tid);
+    vr[kt] = tile_load<BF>(Vb, c.d_out, min(kt, c.ntl - 1) * kTile, c.n, c.tid);
   }
-  const int ntiles = (len + kTile - 1) / kTile;
+  QFrag<BF> qf;
+  load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
+  const int64_t so = ((int64_t)c.b * p.H + c.h) * c.n + min(c.q, c.n - 1);
+  const float M = p.row_max[so], inv = p.row_inv_sum[so];
+#pragma unroll
+  for (int kt = 0; kt < NT; ++kt) {
+    if (kt < c.ntl) {
+      tile_store<BF>(kr[kt], Ks[kt], c.tid);
+      tile_store_v<BF>(vr[kt], Vs[kt], c.tid);
+    }
+  }
+  lds_barrier();
 
   f32x4_t y[4];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) y[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-
-  for (int kt = 0; kt < ntiles; ++kt) {
-    lds_barrier();
-    stage_rows(Ks, Kb, d_out, kt * kTile, n, tid);
-    if constexpr (BF) stage_rows_transposed(Vs, Vb, d_out, kt * kTile, n, tid);
-    else stage_rows(Vs, Vb, d_out, kt * kTile, n, tid);
-    lds_barrier();
-    f32x4_t acc[4];
-    score_tile(acc, Ks, qf, r16, g);
+  for (int cc = 0; cc < 4; ++cc) y[cc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = kt * kTile + 16 * s + 4 * g + i;
-        acc[s][i] = key < len ? prob(logit(acc[s][i]), M, inv) : 0.f;
-      }
-    if constexpr (BF) {
-      // 32 keys per MFMA: k-slots 0..3 = keys 32 pp + 4 g + (0..3), 4..7 = keys 32 pp + 16 + 4 g + (0..3)
-#pragma unroll
-      for (int pp = 0; pp < 2; ++pp) {
-        const uint4 pa = make_uint4(pack_bf16x2(acc[2 * pp][0], acc[2 * pp][1]),
-                                    pack_bf16x2(acc[2 * pp][2], acc[2 * pp][3]),
-                                    pack_bf16x2(acc[2 * pp + 1][0], acc[2 * pp + 1][1]),
-                                    pack_bf16x2(acc[2 * pp + 1][2], acc[2 * pp + 1][3]));
-        const bf16x8_t a = __builtin_bit_cast(bf16x8_t, pa);
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          const uint16_t* vrow = Vs + (16 * c + r16) * kStrideBf + 32 * pp + 4 * g;
-          const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-          const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
-          const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
-          y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bv, y[c], 0, 0, 0);
-        }
-      }
-    } else {
+  for (int kt = 0; kt < NT; ++kt) {
+    if (kt < c.ntl) {
+      f32x4_t acc[4];
+      score_tile(acc, Ks[kt], qf, c.r16, c.g);
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float* vrow = reinterpret_cast<const float*>(Vs) + (16 * s + 4 * g + i) * kStrideF + r16;
-#pragma unroll
-          for (int c = 0; c < 4; ++c)
-            y[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[s][i], vrow[16 * c], y[c], 0, 0, 0);
+          const int key = kt * kTile + 16 * s + 4 * c.g + i;
+          acc[s][i] = key < c.len ? prob(logit(acc[s][i]), M, inv) : 0.f;
         }
+      pv_tile(y, acc, Vs[kt], c.r16, c.g);
     }
   }
-  // y[c][i] = Y[query 4 g + i of the wave][column 16 c + l % 16]
+  store_y(p, c, y);
+}
+
+template <int BF>
+__global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  constexpr int S = stride_of<BF>();
+  __shared__ __align__(16) T Ks[2][kTile * S];
+  __shared__ __align__(16) T Vs[2][kTile * S];
+  const BlockCtx c = block_ctx(p);
+  const int64_t off = (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const T* Qb = static_cast<const T*>(p.Q) + off;
+  const T* Kb = static_cast<const T*>(p.K) + off;
+  const T* Vb = static_cast<const T*>(p.Henc) + off;
+
+  TileRegs kr, vr;
+  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  vr = tile_load<BF>(Vb, c.d_out, 0, c.n, c.tid);
+  QFrag<BF> qf;
+  load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
+  const int64_t so = ((int64_t)c.b * p.H + c.h) * c.n + min(c.q, c.n - 1);
+  const float M = p.row_max[so], inv = p.row_inv_sum[so];
+
+  f32x4_t y[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int row = qt * kTile + wave * 16 + 4 * g + i;
-    if (row < n) {
-      float* yrow = p.Y + ((int64_t)b * n + row) * d_out + h * kDHead + r16;
+  for (int cc = 0; cc < 4; ++cc) y[cc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  for (int kt = 0; kt < c.ntl; ++kt) {
+    T* kb = Ks[kt & 1];
+    T* vb = Vs[kt & 1];
+    tile_store<BF>(kr, kb, c.tid);
+    tile_store_v<BF>(vr, vb, c.tid);
+    lds_barrier();
+    kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
+    vr = tile_load<BF>(Vb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
+    f32x4_t acc[4];
+    score_tile(acc, kb, qf, c.r16, c.g);
 #pragma unroll
-      for (int c = 0; c < 4; ++c) yrow[16 * c] = y[c][i];
-    }
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int key = kt * kTile + 16 * s + 4 * c.g + i;
+        acc[s][i] = key < c.len ? prob(logit(acc[s][i]), M, inv) : 0.f;
+      }
+    pv_tile(y, acc, vb, c.r16, c.g);
   }
+  store_y(p, c, y);
 }
 
 }  // namespace
 
+// Resident variants for padded lengths up to 256 keys (bf16) or 128 keys (fp32).
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
-  const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B);
-  if (p.bf16) hipLaunchKernelGGL(k_scores_colmax<1>, grid, dim3(kThreads), 0, s, p);
-  else hipLaunchKernelGGL(k_scores_colmax<0>, grid, dim3(kThreads), 0, s, p);
+  const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B), blk(kThreads);
+  const int nt = (p.n + kTile - 1) / kTile;
+  if (p.bf16) {
+    if (nt <= 1) hipLaunchKernelGGL((k_scores_res<1, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) hipLaunchKernelGGL((k_scores_res<1, 2>), grid, blk, 0, s, p);
+    else if (nt <= 4) hipLaunchKernelGGL((k_scores_res<1, 4>), grid, blk, 0, s, p);
+    else hipLaunchKernelGGL(k_scores_stream<1>, grid, blk, 0, s, p);
+  } else {
+    if (nt <= 1) hipLaunchKernelGGL((k_scores_res<0, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) hipLaunchKernelGGL((k_scores_res<0, 2>), grid, blk, 0, s, p);
+    else hipLaunchKernelGGL(k_scores_stream<0>, grid, blk, 0, s, p);
+  }
   return hipGetLastError();
 }
 
 hipError_t launch_attn_out(const FwdParams& p, hipStream_t s) {
-  const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B);
-  if (p.bf16) hipLaunchKernelGGL(k_attn_out<1>, grid, dim3(kThreads), 0, s, p);
-  else hipLaunchKernelGGL(k_attn_out<0>, grid, dim3(kThreads), 0, s, p);
+  const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B), blk(kThreads);
+  const int nt = (p.n + kTile - 1) / kTile;
+  if (p.bf16) {
+    if (nt <= 1) hipLaunchKernelGGL((k_attn_res<1, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) hipLaunchKernelGGL((k_attn_res<1, 2>), grid, blk, 0, s, p);
+    else if (nt <= 4) hipLaunchKernelGGL((k_attn_res<1, 4>), grid, blk, 0, s, p);
+    else hipLaunchKernelGGL(k_attn_stream<1>, grid, blk, 0, s, p);
+  } else {
+    if (nt <= 1) hipLaunchKernelGGL((k_attn_res<0, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) hipLaunchKernelGGL((k_attn_res<0, 2>), grid, blk, 0, s, p);
+    else hipLaunchKernelGGL(k_attn_stream<0>, grid, blk, 0, s, p);
+  }
   return hipGetLastError();
 }
 
