@@ -112,29 +112,23 @@ __device__ __forceinline__ void tile_store(const TileRegs& t, typename Elem<BF>:
   }
 }
 
-// bf16 H~ tile stored transposed ([column][key]) so that the B operand of the P V MFMA
-// (8 keys of one column per lane) is two 8-byte LDS reads.
-__device__ __forceinline__ void vec_store_transposed(uint4 u, uint16_t* lds, int v) {
-  const int key = v >> 3, ch = v & 7;
-  uint16_t* col = lds + (8 * ch) * kStrideBf + key;
-  col[0 * kStrideBf] = (uint16_t)(u.x & 0xffffu);
-  col[1 * kStrideBf] = (uint16_t)(u.x >> 16);
-  col[2 * kStrideBf] = (uint16_t)(u.y & 0xffffu);
-  col[3 * kStrideBf] = (uint16_t)(u.y >> 16);
-  col[4 * kStrideBf] = (uint16_t)(u.z & 0xffffu);
-  col[5 * kStrideBf] = (uint16_t)(u.z >> 16);
-  col[6 * kStrideBf] = (uint16_t)(u.w & 0xffffu);
-  col[7 * kStrideBf] = (uint16_t)(u.w >> 16);
-}
-
+// H~ tiles are stored like K tiles, row-major [key][column]; the P V MFMA reads its B
+// operand (8 keys of one column per lane) with the transposing LDS read below.
 template <int BF>
 __device__ __forceinline__ void tile_store_v(const TileRegs& t, typename Elem<BF>::T* lds, int tid) {
-  if constexpr (BF) {
-    vec_store_transposed(t.v0, lds, tid);
-    vec_store_transposed(t.v1, lds, tid + kThreads);
-  } else {
-    tile_store<0>(t, lds, tid);
-  }
+  tile_store<BF>(t, lds, tid);
+}
+
+// ds_read_b64_tr_b16 (gfx950). Within each row of 16 lanes, every lane supplies the address
+// of 4 consecutive 16-bit elements; lane i receives, as its element k (k = 0..3), element
+// i % 4 of the 4 addressed by lane 4 k + i / 4 of its row. Lane s addressing
+// V[kb + s / 4][d0 + 4 (s % 4)] of a row-major tile therefore gives lane i the column
+// V[kb .. kb + 3][d0 + i].
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t lds_v4i16_t;
+
+__device__ __forceinline__ uint2 lds_read_tr16(const uint16_t* p) {
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_t*)p));
 }
 
 // ------------------------------------------------------------------ score tile
@@ -188,9 +182,10 @@ __device__ __forceinline__ void pv_tile(f32x4_t y[4], const f32x4_t acc[4], cons
     const bf16x8_t a = __builtin_bit_cast(bf16x8_t, pa);
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      const uint16_t* vrow = Vs + (16 * c + r16) * kStrideBf + 32 * pp + 4 * g;
-      const uint2 lo = *reinterpret_cast<const uint2*>(vrow);
-      const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 16);
+      // lane (g, r16) addresses key 32 pp + 4 g + r16 / 4, columns 16 c + 4 (r16 % 4) .. + 3
+      const uint16_t* vrow = Vs + (32 * pp + 4 * g + (r16 >> 2)) * kStrideBf + 16 * c + 4 * (r16 & 3);
+      const uint2 lo = lds_read_tr16(vrow);
+      const uint2 hi = lds_read_tr16(vrow + 16 * kStrideBf);
       const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
       y[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, bv, y[c], 0, 0, 0);
     }
@@ -428,7 +423,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[NT][kTile * S];
-  __shared__ __align__(16) T Vs[NT][kTile * S];  // bf16: [column][key]; fp32: [key][column]
+  __shared__ __align__(16) T Vs[NT][kTile * S];  // [key][column]
   const BlockCtx c = block_ctx(p);
   const int64_t off = (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Qb = static_cast<const T*>(p.Q) + off;
