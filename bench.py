@@ -33,6 +33,7 @@ METRIC = "MCA attention tokens/s at 1 GPU; % HBM roofline (sampling) / % MFMA pe
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # dense bf16
 MFMA_FP32_PEAK_TFLOPS = 157.3
+FP32_VECTOR_PEAK_TFLOPS = 157.3  # published vector fp32 (counts packed FMA)
 
 
 def log(*a):
@@ -62,6 +63,7 @@ def stage_work(L, r, idx, elem):
     B, n, d_in, d_out, H = L.batch, L.seq, L.d_in, L.d_out, L.heads
     s_in, s_h = elem, elem  # input element size; H~ stored in the input dtype
     lens = L.lens.astype(np.int64)
+    nparts = H * ((n + 63) // 64)
     sampled = (r > 0) & (r < d_in)
     sat = r == d_in
     distinct = 0
@@ -69,19 +71,22 @@ def stage_work(L, r, idx, elem):
     for b, j in zip(*np.nonzero(sampled)):
         distinct += len(np.unique(idx[b, j, :r[b, j]]))
     n_sampled, n_sat = int(sampled.sum()), int(sat.sum())
+    n_valid = int(lens.sum())
     n_zero = B * n - n_sampled - n_sat
     qk_flops = 2.0 * H * 64 * float(np.sum(n * lens))  # per pass over all (query, valid key) pairs
     w = {}
-    w["clear"] = dict(bytes=4.0 * B * n, flops=0.0)
-    w["scores_colmax"] = dict(bytes=2.0 * B * n * d_out * s_in + 8.0 * B * H * n + 4.0 * B * n,
+    w["scores_colmax"] = dict(bytes=2.0 * B * n * d_out * s_in + 8.0 * B * H * n + 4.0 * B * n * nparts,
                               flops=2 * qk_flops)
-    w["encode"] = dict(bytes=8.0 * B * n + 4.0 * d_in + n_sampled * (d_in * s_in + d_out * s_h)
-                       + distinct * d_out * s_in + n_zero * d_out * s_h,
-                       flops=2.0 * distinct * d_out,
-                       bytes_per_draw=8.0 * B * n + 4.0 * d_in + n_sampled * (d_in * s_in + d_out * s_h)
-                       + draws * d_out * s_in + n_zero * d_out * s_h)
-    w["dense_encode"] = dict(bytes=n_sat * (d_in * s_in + d_out * s_h) + (d_in * d_out * s_in if n_sat else 0),
-                             flops=2.0 * n_sat * d_in * d_out)
+    # partials, x rows of valid tokens, rho, r, the lists (8 bytes per distinct row), zero rows
+    w["sample"] = dict(bytes=4.0 * B * n * nparts + n_valid * d_in * s_in + 4.0 * d_in + 4.0 * B * n
+                       + 8.0 * distinct + n_zero * d_out * s_h, flops=0.0)
+    # sampled: lists + one W_v row per distinct sampled row + H~ rows; saturated: x rows, W_v once, H~ rows
+    gather_bytes = 8.0 * distinct + distinct * d_out * s_in + n_sampled * d_out * s_h
+    sat_bytes = n_sat * (d_in * s_in + d_out * s_h) + (d_in * d_out * s_in if n_sat else 0)
+    w["gather"] = dict(bytes=gather_bytes + sat_bytes, flops=2.0 * distinct * d_out + 2.0 * n_sat * d_in * d_out,
+                       sampled_bytes=gather_bytes, sampled_flops=2.0 * distinct * d_out,
+                       sampled_bytes_every_draw=8.0 * distinct + draws * d_out * s_in + n_sampled * d_out * s_h,
+                       mfma_flops=2.0 * n_sat * d_in * d_out)
     w["attn_out"] = dict(bytes=2.0 * B * n * d_out * s_in + B * n * d_out * s_h + 4.0 * B * n * d_out
                          + 8.0 * B * H * n, flops=2 * qk_flops)
     stats = dict(sampled_tokens=n_sampled, saturated_tokens=n_sat, draws=draws, distinct_rows=distinct)
@@ -210,13 +215,18 @@ def main():
     r = ex.r.cpu().numpy()
     idx = ex.sample_idx.cpu().numpy()
     work, wstats = stage_work(L, r, idx, elem)
-    dom = max((k for k in stage_us if k != "clear"), key=lambda k: stage_us[k])
+    dom = max(stage_us, key=lambda k: stage_us[k])
     dur = stage_us[dom] * 1e-6
-    if dom == "encode":
-        ach = work[dom]["bytes"] / dur / 1e9
-        roof = {"kernel": "k_encode", "bound": "hbm", "achieved": ach, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": ach / HBM_PEAK_GBS, "traffic": None,
-                "achieved_counting_every_draw": work[dom]["bytes_per_draw"] / dur / 1e9}
+    if dom == "gather":
+        # the sampled rows are gathered from a W_v slice held in LDS: the kernel is bound by
+        # LDS reads and float32 FMAs, not HBM; achieved = gather FMAs only (the MFMA work on
+        # saturated tokens in the same launch is not counted)
+        ach = work[dom]["sampled_flops"] / dur / 1e12
+        roof = {"kernel": "k_gather", "bound": "alu", "achieved": ach, "peak": FP32_VECTOR_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": ach / FP32_VECTOR_PEAK_TFLOPS, "traffic": None,
+                "hbm_view": {"algorithmic_GBps": work[dom]["bytes"] / dur / 1e9, "peak": HBM_PEAK_GBS,
+                             "frac": work[dom]["bytes"] / dur / 1e9 / HBM_PEAK_GBS,
+                             "counting_every_draw_GBps": work[dom]["sampled_bytes_every_draw"] / dur / 1e9}}
     else:
         ach = work[dom]["flops"] / dur / 1e12
         roof = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",

@@ -52,8 +52,8 @@ typedef enum mca_dtype {
 /* Stages of the forward pass, in launch order (profiler slots). */
 typedef enum mca_stage {
   MCA_STAGE_SCORES_COLMAX = 0,  /* softmax(Q K^T / 8) row statistics and column-max partials */
-  MCA_STAGE_ENCODE = 1,         /* count rule, sampler and gather-accumulate */
-  MCA_STAGE_DENSE_ENCODE = 2,   /* exact x_j W_v for saturated tokens (MFMA) */
+  MCA_STAGE_SAMPLE = 1,         /* count rule (Eq. 9), sampling weights (Eq. 4), draws, merge */
+  MCA_STAGE_GATHER = 2,         /* H~: sampled rows gather-accumulate, saturated tokens on MFMA */
   MCA_STAGE_ATTN_OUT = 3,       /* Y = A H~ (MFMA) */
   MCA_NUM_STAGES = 4
 } mca_stage;
@@ -110,7 +110,12 @@ typedef struct mca_forward_desc {
  *                                    summed in float64 in column order c = 0 .. d_out-1, one
  *                                    IEEE square root, one rounding to float32 (bitwise
  *                                    reproducible)
- *   offset round_up(4 d_in, 256):    W_v^T [d_out][round_up(d_in, 32)] in `dtype`, zero padded
+ *   offset round_up(4 d_in, 256):    W_v^T in `dtype`, in MFMA fragment order: for column
+ *                                    tile t (16 columns) and k step s (32 bf16 / 16 float32
+ *                                    values of k), 64 x 16 bytes; the 16 bytes at index
+ *                                    16 g + r hold W_v[s*KS + g*E + e][16 t + r], e < E
+ *                                    (E = 8 bf16 / 4 float32); k zero padded to a multiple
+ *                                    of 128, columns to a multiple of 16
  * mca_prepared_size gives the buffer size (host only). mca_prepare_weights fills it from
  * W_v (device [d_in, d_out] of `dtype`).
  * Errors: MCA_ERR_INVALID_ARGUMENT for null pointers, sizes < 1, d_in > 2048,

@@ -23,7 +23,7 @@ MCA_ERR_HIP = 4
 MCA_F32 = 0
 MCA_BF16 = 1
 NUM_STAGES = 4
-STAGES = ("scores_colmax", "encode", "dense_encode", "attn_out")
+STAGES = ("scores_colmax", "sample", "gather", "attn_out")
 
 
 class ForwardDesc(ctypes.Structure):

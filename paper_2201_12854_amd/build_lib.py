@@ -20,7 +20,7 @@ BUILD = os.path.join(ROOT, "_build", "libmca")
 LIB = os.path.join(PKG, "libmca.so")
 ARCH = "gfx950"
 
-SOURCES = ["k_attention.hip", "k_encode.hip", "k_dense.hip", "mca_api.cpp"]
+SOURCES = ["k_attention.hip", "k_sample.hip", "k_gather.hip", "k_prepare.hip", "mca_api.cpp"]
 
 CXXFLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -1,0 +1,79 @@
+// One-time weight preparation (Sec. "Formulation of Sampling Probability": the per-row
+// statistic of W is computed once per weight matrix and cached, not per forward pass):
+//   rho_i = ||W_v[i, :]||, the row norms that scale the sampling weights of Eq. 4;
+//   W_v^T in MFMA fragment order, the B operand of the MFMA products that encode saturated
+//   tokens exactly (one coalesced 1 KB load per 16x16 tile and k step).
+#include "mca_device.h"
+#include "mca_kernels.h"
+
+namespace mca {
+namespace {
+
+template <int BF> struct Elem { using T = float; };
+template <> struct Elem<1> { using T = uint16_t; };
+
+// rho_i = float32(sqrt(sum_c W[i, c]^2)), float64 running sum in column order. One wave
+// per 64 rows; 64x64 tiles go through LDS so global reads are coalesced.
+template <int BF>
+__global__ __launch_bounds__(64) void k_rownorm(const void* Wp, int d_in, int d_out, float* rownorm) {
+  using T = typename Elem<BF>::T;
+  __shared__ double tile[64][65];
+  const T* W = static_cast<const T*>(Wp);
+  const int r0 = blockIdx.x * 64, lane = threadIdx.x;
+  double s = 0.0;
+  for (int c0 = 0; c0 < d_out; c0 += 64) {
+    for (int rr = 0; rr < 64; ++rr) {
+      const int row = r0 + rr, c = c0 + lane;
+      tile[rr][lane] = (row < d_in && c < d_out) ? (double)load_f32(W, (int64_t)row * d_out + c) : 0.0;
+    }
+    lds_barrier();
+    const int cend = min(64, d_out - c0);
+    for (int cc = 0; cc < cend; ++cc) {
+      const double v = tile[lane][cc];
+      s = __dadd_rn(s, __dmul_rn(v, v));  // v*v is exact in float64
+    }
+    lds_barrier();
+  }
+  if (r0 + lane < d_in) rownorm[r0 + lane] = (float)sqrt(s);
+}
+
+// W_v^T in MFMA fragment order (layout in mca_kernels.h): one thread per 16-byte chunk;
+// elements past d_in or d_out are zero. One-time preparation, so the strided reads of W
+// are not tuned.
+template <int BF>
+__global__ __launch_bounds__(256) void k_fragment_wt(const void* Wp, int d_in, int d_out, int nks, int64_t nchunks,
+                                                     void* Wtp) {
+  using T = typename Elem<BF>::T;
+  constexpr int E = BF ? 8 : 4, KS = 4 * E;
+  const int64_t q = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (q >= nchunks) return;
+  const int l = (int)(q % 64);
+  const int64_t tk = q / 64;  // t * nks + ks
+  const int ks = (int)(tk % nks), t = (int)(tk / nks);
+  const int c = 16 * t + (l % 16), k0 = ks * KS + (l / 16) * E;
+  const T* W = static_cast<const T*>(Wp);
+  T* dst = static_cast<T*>(Wtp) + q * E;
+#pragma unroll
+  for (int e = 0; e < E; ++e) dst[e] = (c < d_out && k0 + e < d_in) ? W[(int64_t)(k0 + e) * d_out + c] : T(0);
+}
+
+}  // namespace
+
+hipError_t launch_prepare(const void* W, int bf16, int d_in, int d_out, void* prepared, hipStream_t s) {
+  float* rownorm = static_cast<float*>(prepared);
+  void* Wt = static_cast<char*>(prepared) + prepared_wt_offset(d_in);
+  const int nks = (int)(prepared_din_pad(d_in) / (bf16 ? 32 : 16));
+  const int64_t nchunks = prepared_dout_pad(d_out) / 16 * nks * 64;
+  const dim3 g1((d_in + 63) / 64);
+  const dim3 g2((unsigned)((nchunks + 255) / 256));
+  if (bf16) {
+    hipLaunchKernelGGL(k_rownorm<1>, g1, dim3(64), 0, s, W, d_in, d_out, rownorm);
+    hipLaunchKernelGGL(k_fragment_wt<1>, g2, dim3(256), 0, s, W, d_in, d_out, nks, nchunks, Wt);
+  } else {
+    hipLaunchKernelGGL(k_rownorm<0>, g1, dim3(64), 0, s, W, d_in, d_out, rownorm);
+    hipLaunchKernelGGL(k_fragment_wt<0>, g2, dim3(256), 0, s, W, d_in, d_out, nks, nchunks, Wt);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace mca

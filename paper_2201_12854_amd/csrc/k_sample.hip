@@ -1,0 +1,249 @@
+// Sampler of the MCA forward pass on gfx950: one wavefront per token j of batch row b.
+//
+//   1. column max m_j = max over the per-(head, query tile) partials written by the score
+//      pass, and the sample count of Eq. 9 (Sec. "Determining Sample Size from
+//      Attention") in float64: t = (len_b * m_j) / alpha, r_j = ceil(t * t) clamped to
+//      [1, d_in]; padded keys get 0. r_j = d_in marks a saturated token, encoded exactly
+//      by the gather kernel's MFMA path (cost of d_in samples, no error).
+//   2. sampling weights of Eq. 4 for the product x_j W_v: v_i = |x_ji| * rho_i in one
+//      float32 multiply, quantised to 32-bit fixed point aligned to the largest v_i,
+//      w_i = floor(v_i 2^(32-e)); inclusive prefix sums C (uint64) by a wavefront scan
+//      (each lane owns a contiguous run of rows), stored in the wave's part of the LDS.
+//   3. r_j i.i.d. draws with replacement (Eq. 2): Philox4x32-10 with counter (k, j, b, 0),
+//      u = o0 | o1 << 32, t = floor(u T / 2^64), s_k = min{i : C_i > t} by binary search
+//      in LDS; draws are counted per row with LDS integer atomics (exact, order-free).
+//   4. duplicates merged: coefficient of row i = count_i x_ji T / (r_j w_i) (float64,
+//      rounded once); the distinct rows, ascending, with their coefficients form the
+//      token's list (rows as byte offsets into the gather kernel's LDS slice), and its
+//      length U goes to ucount (0 for tokens without a list).
+// A wave works on its own token and its own LDS region only: the kernel has no block
+// barriers and no global atomics (on a multi-die GPU, device-scope atomics on a few hot
+// counters serialise). Everything it writes is deterministic.
+#include "mca_device.h"
+#include "mca_kernels.h"
+
+namespace mca {
+namespace {
+
+template <int BF> struct Elem { using T = float; };
+template <> struct Elem<1> { using T = uint16_t; };
+
+constexpr int kWaves = 4;  // tokens per block
+
+// LDS of one wave: C uint64 [d_in], then cnt uint32 [d_in].
+__host__ __device__ inline int sample_lds_per_wave(int d_in) { return (12 * d_in + 15) / 16 * 16; }
+
+// Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
+// LDS instructions in issue order, so only compiler reordering has to be prevented.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+template <typename U>
+__device__ __forceinline__ U wave_inclusive_scan(U v, int lane) {
+#pragma unroll
+  for (int off = 1; off < kWave; off <<= 1) {
+    const U y = __shfl_up(v, off, kWave);
+    if (lane >= off) v += y;
+  }
+  return v;
+}
+
+template <int BF>
+__device__ __forceinline__ void write_zero4(const FwdParams& p, int64_t off) {
+  if constexpr (BF) *reinterpret_cast<uint2*>(static_cast<uint16_t*>(p.Henc) + off) = make_uint2(0u, 0u);
+  else *reinterpret_cast<float4*>(static_cast<float*>(p.Henc) + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+  if (p.enc_out) *reinterpret_cast<float4*>(p.enc_out + off) = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+// PER: upper bound of the rows one lane owns, ceil(d_in / 64) <= PER.
+template <int BF, int PER>
+__global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  extern __shared__ __align__(16) unsigned char smem[];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t ntok = (int64_t)p.B * p.n;
+  const int64_t tok = (int64_t)blockIdx.x * kWaves + wave;
+  if (tok >= ntok) return;  // whole waves only; no block barrier follows
+  const int d_in = p.d_in, n = p.n;
+  const int b = (int)(tok / n), j = (int)(tok - (int64_t)b * n);
+  unsigned char* wl = smem + wave * sample_lds_per_wave(d_in);
+  uint64_t* C = reinterpret_cast<uint64_t*>(wl);
+  uint32_t* cnt = reinterpret_cast<uint32_t*>(wl + 8 * d_in);
+
+  // ---- independent loads first: length, column-max partials, x and rho of this lane's
+  // contiguous run of rows [i0, i0 + cnt_rows)
+  int len = p.seq_lens ? p.seq_lens[b] : n;
+  len = min(max(len, 1), n);
+  const int rin = p.r_in ? p.r_in[tok] : 0;
+  const float* part = p.colmax_part + tok * p.nparts;
+  float m = 0.f;
+  for (int t = lane; t < p.nparts; t += kWave) m = fmaxf(m, part[t]);
+  const int per = (d_in + kWave - 1) / kWave;
+  const int i0 = min(lane * per, d_in);
+  const int nrows = min(per, d_in - i0);
+  const T* xrow = static_cast<const T*>(p.X) + tok * d_in;
+  float xv[PER], vv[PER];
+  float lmax = 0.f;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    xv[k] = 0.f;
+    vv[k] = 0.f;
+    if (k < nrows) {
+      xv[k] = load_f32(xrow, i0 + k);
+      vv[k] = __fmul_rn(fabsf(xv[k]), p.rownorm[i0 + k]);
+      lmax = fmaxf(lmax, vv[k]);
+    }
+  }
+  m = wave_max(m);
+  const float vmax = wave_max(lmax);
+
+  // ---- 1. sample count (Eq. 9)
+  int r;
+  if (j >= len) {
+    r = 0;
+    m = 0.f;
+  } else if (p.r_in) {
+    r = min(max(rin, 0), d_in);
+  } else {
+    const double t = ((double)len * (double)m) / p.alpha;
+    const double tt = t * t;
+    r = (tt >= (double)d_in) ? d_in : max((int)ceil(tt), 1);
+  }
+  if (lane == 0) {
+    p.r[tok] = r;
+    if (p.colmax_out) p.colmax_out[tok] = m;
+  }
+  if (r >= d_in) {  // saturated: exact encoding on the MFMA path of the gather kernel
+    if (lane == 0) p.ucount[tok] = 0;
+    return;
+  }
+  if (r == 0 || !(vmax > 0.f) || !(vmax <= 3.40282347e38f)) {  // padded, x_j = 0 or non-finite
+    if (lane == 0) p.ucount[tok] = 0;
+    for (int c = 4 * lane; c < p.d_out; c += 4 * kWave) write_zero4<BF>(p, tok * p.d_out + c);
+    return;
+  }
+
+  // ---- 2. fixed-point weights and their prefix sums
+  int e;
+  (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
+  const int shift = 32 - e;
+  uint32_t wv[PER];
+  uint64_t lsum = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    wv[k] = (k < nrows) ? (uint32_t)ldexpf(vv[k], shift) : 0u;
+    lsum += wv[k];
+  }
+  const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum, lane);
+  const uint64_t Tw = __shfl(incl, kWave - 1, kWave);  // = C[d_in - 1]
+  uint64_t run = incl - lsum;
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (k < nrows) {
+      run += wv[k];
+      C[i0 + k] = run;
+      cnt[i0 + k] = 0u;
+    }
+  }
+  wave_lds_sync();
+
+  // ---- 3. draws, 4 per lane at a time so that their searches overlap. The search runs a
+  // fixed number of halvings (ceil(log2 d_in)) without branches; once lo == hi it stays put,
+  // since C[lo] > t there.
+  const int nsteps = 32 - __clz(max(d_in - 1, 1));
+  for (int k0 = lane; k0 < r; k0 += 4 * kWave) {
+    uint64_t t[4];
+    int lo[4], hi[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = k0 + u * kWave;
+      const u32x4 o = philox4x32_10(u32x4{(uint32_t)k, (uint32_t)j, (uint32_t)b, 0u}, p.seed_lo, p.seed_hi);
+      t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), Tw);  // in [0, T)
+      lo[u] = 0;
+      hi[u] = d_in - 1;  // C[d_in-1] = T > t, so the answer is in range
+    }
+    for (int st = 0; st < nsteps; ++st) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int mid = (lo[u] + hi[u]) >> 1;
+        const bool right = C[mid] <= t[u];
+        lo[u] = right ? mid + 1 : lo[u];
+        hi[u] = right ? hi[u] : mid;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int k = k0 + u * kWave;
+      if (k < r) {
+        atomicAdd(cnt + lo[u], 1u);
+        const int64_t o2 = tok * d_in + k;
+        if (p.idx_out) p.idx_out[o2] = lo[u];
+        if (p.coef_out) {
+          const uint64_t ws = C[lo[u]] - (lo[u] > 0 ? C[lo[u] - 1] : 0ull);
+          p.coef_out[o2] = (float)(((double)load_f32(xrow, lo[u]) * (double)Tw) / ((double)r * (double)ws));
+        }
+      }
+    }
+  }
+  wave_lds_sync();
+
+  // ---- 4. merge duplicates into the token's list, ascending row order
+  int nloc = 0;
+#pragma unroll
+  for (int k = 0; k < PER; ++k)
+    if (k < nrows) nloc += cnt[i0 + k] != 0u;
+  const int incl_u = wave_inclusive_scan<int>(nloc, lane);
+  const int U = __shfl(incl_u, kWave - 1, kWave);
+  int pos = incl_u - nloc;
+  uint2* lst = p.list + tok * d_in;
+  const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
+#pragma unroll
+  for (int k = 0; k < PER; ++k) {
+    if (k < nrows) {
+      const uint32_t c = cnt[i0 + k];
+      if (c) {
+        const float coef = (float)(((double)c * (double)xv[k] * (double)Tw) / ((double)r * (double)wv[k]));
+        lst[pos] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
+        ++pos;
+      }
+    }
+  }
+  if (lane == 0) p.ucount[tok] = U;
+}
+
+template <int BF, int PER>
+hipError_t launch_per(const FwdParams& p, hipStream_t s) {
+  const int64_t ntok = (int64_t)p.B * p.n;
+  const dim3 grid((unsigned)((ntok + kWaves - 1) / kWaves));
+  const size_t lds = (size_t)kWaves * sample_lds_per_wave(p.d_in);
+  if (lds > 65536) {
+    const hipError_t e = hipFuncSetAttribute((const void*)k_sample<BF, PER>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+  }
+  hipLaunchKernelGGL((k_sample<BF, PER>), grid, dim3(64 * kWaves), lds, s, p);
+  return hipGetLastError();
+}
+
+template <int BF>
+hipError_t launch_bf(const FwdParams& p, hipStream_t s) {
+  const int per = (p.d_in + kWave - 1) / kWave;
+  if (per <= 4) return launch_per<BF, 4>(p, s);
+  if (per <= 8) return launch_per<BF, 8>(p, s);
+  if (per <= 12) return launch_per<BF, 12>(p, s);
+  if (per <= 16) return launch_per<BF, 16>(p, s);
+  if (per <= 24) return launch_per<BF, 24>(p, s);
+  if (per <= 32) return launch_per<BF, 32>(p, s);
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+hipError_t launch_sample(const FwdParams& p, hipStream_t s) {
+  return p.bf16 ? launch_bf<1>(p, s) : launch_bf<0>(p, s);
+}
+
+}  // namespace mca

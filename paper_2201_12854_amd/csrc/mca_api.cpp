@@ -38,7 +38,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t colmax_part, row_max, row_inv, henc, total;
+  size_t colmax_part, row_max, row_inv, henc, list, ucount, total;
   int qtiles, nparts;
 };
 
@@ -54,6 +54,8 @@ Layout layout_for(const mca_forward_desc& d) {
   L.row_max = off;     off = align256(off + 4 * tokens * size_t(d.heads));
   L.row_inv = off;     off = align256(off + 4 * tokens * size_t(d.heads));
   L.henc = off;        off = align256(off + helem * tokens * d_out);
+  L.list = off;        off = align256(off + 8 * tokens * size_t(d.d_in));
+  L.ucount = off;      off = align256(off + 4 * tokens);
   L.total = off;
   return L;
 }
@@ -152,7 +154,7 @@ const char* mca_last_error(void) { return g_last_error; }
 int mca_num_stages(void) { return MCA_NUM_STAGES; }
 
 const char* mca_stage_name(int stage) {
-  static const char* names[MCA_NUM_STAGES] = {"scores_colmax", "encode", "dense_encode", "attn_out"};
+  static const char* names[MCA_NUM_STAGES] = {"scores_colmax", "sample", "gather", "attn_out"};
   return (stage >= 0 && stage < MCA_NUM_STAGES) ? names[stage] : "unknown";
 }
 
@@ -236,6 +238,10 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.row_max = reinterpret_cast<float*>(ws + L.row_max);
   p.row_inv_sum = reinterpret_cast<float*>(ws + L.row_inv);
   p.Henc = ws + L.henc;
+  p.list = reinterpret_cast<uint2*>(ws + L.list);
+  p.ucount = reinterpret_cast<int32_t*>(ws + L.ucount);
+  p.wc = mca::gather_slice_cols(p.d_in);
+  p.gather_bps = mca::gather_blocks_per_slice(p.d_in, p.d_out);
   p.colmax_out = desc->colmax_out;
   p.idx_out = desc->sample_idx_out;
   p.coef_out = desc->sample_coef_out;
@@ -245,9 +251,8 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   Profiler* pr = static_cast<Profiler*>(desc->profiler);
   if ((st = run_stage(pr, MCA_STAGE_SCORES_COLMAX, s, [&] { return mca::launch_scores_colmax(p, s); })) != MCA_OK)
     return st;
-  if ((st = run_stage(pr, MCA_STAGE_ENCODE, s, [&] { return mca::launch_encode(p, s); })) != MCA_OK) return st;
-  if ((st = run_stage(pr, MCA_STAGE_DENSE_ENCODE, s, [&] { return mca::launch_dense_encode(p, s); })) != MCA_OK)
-    return st;
+  if ((st = run_stage(pr, MCA_STAGE_SAMPLE, s, [&] { return mca::launch_sample(p, s); })) != MCA_OK) return st;
+  if ((st = run_stage(pr, MCA_STAGE_GATHER, s, [&] { return mca::launch_gather(p, s); })) != MCA_OK) return st;
   if ((st = run_stage(pr, MCA_STAGE_ATTN_OUT, s, [&] { return mca::launch_attn_out(p, s); })) != MCA_OK) return st;
   return ok();
 }

@@ -9,12 +9,19 @@ namespace mca {
 
 constexpr int kQueryTile = 64;  // queries per attention block
 
-// Prepared weights: rownorm float32 [d_in] at offset 0, then W_v^T [d_out][d_in_pad] in the
-// input dtype (zero padded), at offset prepared_wt_offset(d_in).
-inline int64_t prepared_din_pad(int64_t d_in) { return (d_in + 31) / 32 * 32; }
+
+// Prepared weights: rownorm float32 [d_in] at offset 0, then, at prepared_wt_offset(d_in),
+// W_v^T in the input dtype in MFMA fragment order: for every 16-column tile t and k step
+// ks (KS = 32 bf16 or 16 float32 values of k), 64 lanes x 16 bytes, lane l = 16 g + r
+// holding W_v[ks KS + g E + e][16 t + r], e < E (E = 8 bf16 or 4 float32 per 16 bytes).
+// One wave-wide 16-byte load then fetches the B operand of a 16x16 MFMA tile as one
+// contiguous 1 KB block. k is zero padded to a multiple of 128 (whole rounds of 4 steps),
+// columns to a multiple of 16.
+inline int64_t prepared_din_pad(int64_t d_in) { return (d_in + 127) / 128 * 128; }
+inline int64_t prepared_dout_pad(int64_t d_out) { return (d_out + 15) / 16 * 16; }
 inline size_t prepared_wt_offset(int64_t d_in) { return (size_t)((4 * d_in + 255) / 256 * 256); }
 inline size_t prepared_bytes(int bf16, int64_t d_in, int64_t d_out) {
-  return prepared_wt_offset(d_in) + (size_t)d_out * (size_t)prepared_din_pad(d_in) * (bf16 ? 2 : 4);
+  return prepared_wt_offset(d_in) + (size_t)prepared_dout_pad(d_out) * (size_t)prepared_din_pad(d_in) * (bf16 ? 2 : 4);
 }
 
 // Everything one forward pass needs, with the workspace already carved up.
@@ -41,6 +48,11 @@ struct FwdParams {
   float* row_max;      // [B*H*n]
   float* row_inv_sum;  // [B*H*n]
   void* Henc;          // [B*n*d_out] H~ in the input dtype
+  uint2* list;         // [B*n][d_in] distinct sampled rows of a token:
+                       // (row * gather_row_bytes(d_in), float32 bits of coef)
+  int32_t* ucount;     // [B*n] number of distinct rows U of a sampled token, else 0
+  int wc;              // W_v columns per gather slice (32 or 16)
+  int gather_bps;      // gather blocks per slice
   // optional outputs
   float* colmax_out;
   int32_t* idx_out;
@@ -49,8 +61,15 @@ struct FwdParams {
 };
 
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s);
-hipError_t launch_encode(const FwdParams& p, hipStream_t s);
-hipError_t launch_dense_encode(const FwdParams& p, hipStream_t s);
+hipError_t launch_sample(const FwdParams& p, hipStream_t s);
+hipError_t launch_gather(const FwdParams& p, hipStream_t s);
+// Columns per gather slice for d_in (the slice, float32, must fit the LDS with the staging area).
+__host__ __device__ inline int gather_slice_cols(int d_in) { return d_in <= 1024 ? 32 : 16; }
+// Bytes of one slice row in LDS (float32); list entries hold row * gather_row_bytes.
+__host__ __device__ inline int gather_row_bytes(int d_in) { return 4 * gather_slice_cols(d_in); }
+// Gather blocks per column slice: at most one block per CU over all slices (a block holds
+// most of a CU's LDS, so a second round of blocks would double the time).
+int gather_blocks_per_slice(int d_in, int d_out);
 hipError_t launch_attn_out(const FwdParams& p, hipStream_t s);
 hipError_t launch_prepare(const void* W, int bf16, int d_in, int d_out, void* prepared, hipStream_t s);
 

@@ -67,7 +67,10 @@ def test_workspace_size_formula():
     def a(v):
         return (v + 255) // 256 * 256
 
-    expect = a(4 * tokens * parts) + 2 * a(4 * tokens * H) + a(2 * tokens * H * 64)
+    # colmax partials, row max, row 1/sum, H~ (bf16), sample lists (8 bytes per row slot),
+    # list lengths
+    expect = (a(4 * tokens * parts) + 2 * a(4 * tokens * H) + a(2 * tokens * H * 64) + a(8 * tokens * d)
+              + a(4 * tokens))
     assert got == expect
     assert mca.workspace_size(_desc(dtype_code=0)) > got  # float32 H~
 
@@ -76,7 +79,7 @@ def test_prepared_size_formula():
     for dt, esz in ((0, 4), (1, 2)):
         for d_in, d_out in ((768, 768), (45, 256), (1, 64)):
             off = (4 * d_in + 255) // 256 * 256
-            assert mca.prepared_size(dt, d_in, d_out) == off + d_out * ((d_in + 31) // 32 * 32) * esz
+            assert mca.prepared_size(dt, d_in, d_out) == off + ((d_out + 15) // 16 * 16) * ((d_in + 127) // 128 * 128) * esz
 
 
 @pytest.mark.parametrize("field,value,status", [

@@ -76,12 +76,18 @@ def test_prepared_weights_bitexact(dev, dtype):
         prep = mca.prepare_weights(Wd)
         torch.cuda.synchronize()
         assert np.array_equal(mca.rownorm(prep, d_in).cpu().numpy(), oracle.row_norms(W))
-        # the transposed, zero-padded copy used by the exact MFMA path
+        # W_v^T in MFMA fragment order, zero padded: [tile][k step][g][r][e] holds
+        # W_v[step * KS + g * E + e][16 * tile + r]
         off = (4 * d_in + 255) // 256 * 256
-        pad = (d_in + 31) // 32 * 32
-        esz = 4 if dtype == "f32" else 2
-        raw = prep[off: off + d_out * pad * esz].view(tdt).view(d_out, pad).float().cpu().numpy()
-        assert np.array_equal(raw[:, :d_in], W.T) and np.all(raw[:, d_in:] == 0)
+        pad = (d_in + 127) // 128 * 128
+        cpad = (d_out + 15) // 16 * 16
+        esz, E = (4, 4) if dtype == "f32" else (2, 8)
+        nks = pad // (4 * E)
+        raw = prep[off: off + cpad * pad * esz].view(tdt).float().cpu().numpy()
+        wt = raw.reshape(cpad // 16, nks, 4, 16, E).transpose(0, 3, 1, 2, 4).reshape(cpad, pad)
+        ref = np.zeros((cpad, pad), np.float32)
+        ref[:d_out, :d_in] = W.T
+        assert np.array_equal(wt, ref)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
