@@ -58,6 +58,48 @@ __device__ __forceinline__ void write_zero4(const FwdParams& p, int64_t off) {
   if (p.enc_out) *reinterpret_cast<float4*>(p.enc_out + off) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
+// W draws of one lane, k = k0 + 64 u (u < W), searched together so that their LDS reads
+// overlap. The search runs a fixed number of halvings (ceil(log2 d_in)) without branches;
+// once lo == hi it stays put, since C[lo] > t there.
+template <int W>
+__device__ __forceinline__ void draw_batch(const FwdParams& p, const uint64_t* C, uint32_t* cnt, const void* xrow,
+                                           int k0, int r, int j, int b, int64_t tok, uint64_t Tw, int nsteps) {
+  uint64_t t[W];
+  int lo[W], hi[W];
+#pragma unroll
+  for (int u = 0; u < W; ++u) {
+    const int k = k0 + u * kWave;
+    const u32x4 o = philox4x32_10(u32x4{(uint32_t)k, (uint32_t)j, (uint32_t)b, 0u}, p.seed_lo, p.seed_hi);
+    t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), Tw);  // in [0, T)
+    lo[u] = 0;
+    hi[u] = p.d_in - 1;  // C[d_in-1] = T > t, so the answer is in range
+  }
+  for (int st = 0; st < nsteps; ++st) {
+#pragma unroll
+    for (int u = 0; u < W; ++u) {
+      const int mid = (lo[u] + hi[u]) >> 1;
+      const bool right = C[mid] <= t[u];
+      lo[u] = right ? mid + 1 : lo[u];
+      hi[u] = right ? hi[u] : mid;
+    }
+  }
+#pragma unroll
+  for (int u = 0; u < W; ++u) {
+    const int k = k0 + u * kWave;
+    if (k < r) {
+      atomicAdd(cnt + lo[u], 1u);
+      const int64_t o2 = tok * p.d_in + k;
+      if (p.idx_out) p.idx_out[o2] = lo[u];
+      if (p.coef_out) {
+        const uint64_t ws = C[lo[u]] - (lo[u] > 0 ? C[lo[u] - 1] : 0ull);
+        const double xs = p.bf16 ? (double)load_f32(static_cast<const uint16_t*>(xrow), lo[u])
+                                 : (double)load_f32(static_cast<const float*>(xrow), lo[u]);
+        p.coef_out[o2] = (float)((xs * (double)Tw) / ((double)r * (double)ws));
+      }
+    }
+  }
+}
+
 // PER: upper bound of the rows one lane owns, ceil(d_in / 64) <= PER.
 template <int BF, int PER>
 __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
@@ -85,16 +127,34 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const int i0 = min(lane * per, d_in);
   const int nrows = min(per, d_in - i0);
   const T* xrow = static_cast<const T*>(p.X) + tok * d_in;
+  // full: d_in = 64 PER, every lane owns exactly PER rows and its runs of x, rho, C and
+  // cnt are 16-byte aligned (i0 = PER lane), so they move as 16-byte vectors
+  const bool full = d_in == kWave * PER;
   float xv[PER], vv[PER];
   float lmax = 0.f;
+  if (full) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    xv[k] = 0.f;
-    vv[k] = 0.f;
-    if (k < nrows) {
-      xv[k] = load_f32(xrow, i0 + k);
-      vv[k] = __fmul_rn(fabsf(xv[k]), p.rownorm[i0 + k]);
-      lmax = fmaxf(lmax, vv[k]);
+    for (int k = 0; k < PER; k += 4) {
+      const float4 xs = load4_f32(xrow + i0 + k);
+      const float4 rs = *reinterpret_cast<const float4*>(p.rownorm + i0 + k);
+      xv[k] = xs.x; xv[k + 1] = xs.y; xv[k + 2] = xs.z; xv[k + 3] = xs.w;
+      vv[k] = __fmul_rn(fabsf(xs.x), rs.x);
+      vv[k + 1] = __fmul_rn(fabsf(xs.y), rs.y);
+      vv[k + 2] = __fmul_rn(fabsf(xs.z), rs.z);
+      vv[k + 3] = __fmul_rn(fabsf(xs.w), rs.w);
+    }
+#pragma unroll
+    for (int k = 0; k < PER; ++k) lmax = fmaxf(lmax, vv[k]);
+  } else {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      xv[k] = 0.f;
+      vv[k] = 0.f;
+      if (k < nrows) {
+        xv[k] = load_f32(xrow, i0 + k);
+        vv[k] = __fmul_rn(fabsf(xv[k]), p.rownorm[i0 + k]);
+        lmax = fmaxf(lmax, vv[k]);
+      }
     }
   }
   m = wave_max(m);
@@ -140,61 +200,55 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum, lane);
   const uint64_t Tw = __shfl(incl, kWave - 1, kWave);  // = C[d_in - 1]
   uint64_t run = incl - lsum;
+  if (full) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    if (k < nrows) {
-      run += wv[k];
-      C[i0 + k] = run;
-      cnt[i0 + k] = 0u;
+    for (int k = 0; k < PER; k += 2) {
+      const uint64_t c0 = run + wv[k], c1 = c0 + wv[k + 1];
+      run = c1;
+      *reinterpret_cast<uint4*>(C + i0 + k) = make_uint4((uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32));
+    }
+#pragma unroll
+    for (int k = 0; k < PER; k += 4) *reinterpret_cast<uint4*>(cnt + i0 + k) = make_uint4(0u, 0u, 0u, 0u);
+  } else {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      if (k < nrows) {
+        run += wv[k];
+        C[i0 + k] = run;
+        cnt[i0 + k] = 0u;
+      }
     }
   }
   wave_lds_sync();
 
-  // ---- 3. draws, 4 per lane at a time so that their searches overlap. The search runs a
-  // fixed number of halvings (ceil(log2 d_in)) without branches; once lo == hi it stays put,
-  // since C[lo] > t there.
+  // ---- 3. draws: ceil(r / 64) per lane, in batches of up to 4 searched together
   const int nsteps = 32 - __clz(max(d_in - 1, 1));
-  for (int k0 = lane; k0 < r; k0 += 4 * kWave) {
-    uint64_t t[4];
-    int lo[4], hi[4];
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int k = k0 + u * kWave;
-      const u32x4 o = philox4x32_10(u32x4{(uint32_t)k, (uint32_t)j, (uint32_t)b, 0u}, p.seed_lo, p.seed_hi);
-      t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), Tw);  // in [0, T)
-      lo[u] = 0;
-      hi[u] = d_in - 1;  // C[d_in-1] = T > t, so the answer is in range
-    }
-    for (int st = 0; st < nsteps; ++st) {
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int mid = (lo[u] + hi[u]) >> 1;
-        const bool right = C[mid] <= t[u];
-        lo[u] = right ? mid + 1 : lo[u];
-        hi[u] = right ? hi[u] : mid;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int k = k0 + u * kWave;
-      if (k < r) {
-        atomicAdd(cnt + lo[u], 1u);
-        const int64_t o2 = tok * d_in + k;
-        if (p.idx_out) p.idx_out[o2] = lo[u];
-        if (p.coef_out) {
-          const uint64_t ws = C[lo[u]] - (lo[u] > 0 ? C[lo[u] - 1] : 0ull);
-          p.coef_out[o2] = (float)(((double)load_f32(xrow, lo[u]) * (double)Tw) / ((double)r * (double)ws));
-        }
-      }
-    }
+  const int nper = (r + kWave - 1) / kWave;
+  for (int u0 = 0; u0 < nper; u0 += 4) {
+    const int k0 = lane + u0 * kWave;
+    const int w = min(4, nper - u0);
+    if (w == 4) draw_batch<4>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
+    else if (w == 3) draw_batch<3>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
+    else if (w == 2) draw_batch<2>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
+    else draw_batch<1>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
   }
   wave_lds_sync();
 
   // ---- 4. merge duplicates into the token's list, ascending row order
+  uint32_t cv[PER];
+  if (full) {
+#pragma unroll
+    for (int k = 0; k < PER; k += 4) {
+      const uint4 c4 = *reinterpret_cast<const uint4*>(cnt + i0 + k);
+      cv[k] = c4.x; cv[k + 1] = c4.y; cv[k + 2] = c4.z; cv[k + 3] = c4.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < PER; ++k) cv[k] = k < nrows ? cnt[i0 + k] : 0u;
+  }
   int nloc = 0;
 #pragma unroll
-  for (int k = 0; k < PER; ++k)
-    if (k < nrows) nloc += cnt[i0 + k] != 0u;
+  for (int k = 0; k < PER; ++k) nloc += cv[k] != 0u;
   const int incl_u = wave_inclusive_scan<int>(nloc, lane);
   const int U = __shfl(incl_u, kWave - 1, kWave);
   int pos = incl_u - nloc;
@@ -202,8 +256,8 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
-    if (k < nrows) {
-      const uint32_t c = cnt[i0 + k];
+    {
+      const uint32_t c = cv[k];
       if (c) {
         const float coef = (float)(((double)c * (double)xv[k] * (double)Tw) / ((double)r * (double)wv[k]));
         lst[pos] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
