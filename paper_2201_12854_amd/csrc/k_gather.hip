@@ -11,8 +11,9 @@
 // gather reads LDS instead of L2. A row of the slice is WC / 4 lanes x 16 bytes; a wave
 // works on 64 / (WC / 4) sampled tokens at once, one per lane group, so each 16-byte LDS
 // read instruction fetches one sampled row for each of them and no cross-lane reduction
-// is needed. The list entries (LDS byte offset of the row, coefficient) stream in through
-// a register ring kRing entries ahead of use.
+// is needed. The list entries (LDS byte offset of the row, coefficient) are loaded one
+// round ahead with coalesced 16-byte loads and shared within each lane group through a
+// small LDS staging area.
 //
 // Work distribution: the blocks of a slice split the tokens into contiguous ranges. A block
 // reads r and U of its range, puts the saturated tokens on one LDS list and sorts the
@@ -159,7 +160,6 @@ __device__ __forceinline__ int wave_max_int(int v) {
   return max(max(__builtin_amdgcn_readlane(v, 0), __builtin_amdgcn_readlane(v, 16)),
              max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
 }
-__device__ __forceinline__ int wave_min_int(int v) { return -wave_max_int(-v); }
 
 // acc += coef * W_lds[row] (4 columns) for one list entry (LDS byte offset of the row, coef).
 __device__ __forceinline__ void fma_row(float4& acc, const unsigned char* wl, uint2 e) {
@@ -174,7 +174,6 @@ __device__ __forceinline__ void fma_row(float4& acc, const unsigned char* wl, ui
 constexpr int kChunk = kThreads;  // tokens classified per block pass (one per thread)
 constexpr int kNumKeys = 48;      // sort keys floor(4 log2 U) for 1 <= U < 4096
 constexpr int kUBits = 12;        // order entry: (local token << 12) | U
-constexpr int kRing = 16;         // list entries in flight per lane
 
 // floor(4 log2 U) for 1 <= U < 4096: the octave and the next two bits of U.
 __device__ __forceinline__ int sort_key(int U) {
@@ -183,66 +182,82 @@ __device__ __forceinline__ int sort_key(int U) {
   return 4 * e + f;
 }
 
+constexpr int kWavesPerBlock = kThreads / 64;
+
 __host__ __device__ inline size_t gather_lds_bytes(int d_in, int wc) {
-  return (size_t)(d_in + 1) * wc * 4  // W_v slice, float32, and a zero row
-         + (size_t)kChunk * 4 * 2     // sampled order, saturated list
-         + 64 * 4;                    // counters
+  return (size_t)(d_in + 1) * wc * 4         // W_v slice, float32, and a zero row
+         + (size_t)kWavesPerBlock * 1024      // list staging, 1 KB per wave
+         + (size_t)kChunk * 4 * 2            // sampled order, saturated list
+         + 64 * 4;                           // counters
 }
 
-// Entry q of a list of length U, or the zero row with coefficient 0 past its end. The load
-// address is clamped into the list and the selection done with masks (no branch).
-__device__ __forceinline__ uint2 masked_entry(const uint2* L, int q, int U, uint32_t zero_row) {
-  const uint2 v = L[min(q, U - 1)];
-  const uint32_t keep = q < U ? 0xffffffffu : 0u;
-  return make_uint2((v.x & keep) | (zero_row & ~keep), v.y & keep);
+// Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
+// LDS instructions in issue order, so only compiler reordering has to be prevented.
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+}
+
+// This lane's two list entries q, q + 1 (q even, 16 bytes) of a list of length U; entries
+// past the end become the zero row with coefficient 0. The load address is clamped into
+// the token's list slot (stride entries, even) and the selection done with masks, so the
+// load needs no branch.
+__device__ __forceinline__ uint4 entry_pair(const uint2* L, int q, int U, int stride, uint32_t zero_row) {
+  const uint4 v = *reinterpret_cast<const uint4*>(L + min(q, stride - 2));
+  const uint32_t k0 = q < U ? 0xffffffffu : 0u, k1 = q + 1 < U ? 0xffffffffu : 0u;
+  return make_uint4((v.x & k0) | (zero_row & ~k0), v.y & k0, (v.z & k1) | (zero_row & ~k1), v.w & k1);
 }
 
 // G = 64 / (RB / 16) sampled tokens s0 .. s0 + G - 1 of the sorted order, one per lane group:
 // group g accumulates its token's rows for the 4 columns 4 cl .. 4 cl + 3 of every lane.
-// The entries stream through a ring of kRing registers, one block of kRing ahead; blocks
-// inside every list of the item load plainly, later ones with masks (past its own list a
-// group reads the zero row with coefficient 0).
+// A round covers RB / 8 list entries of every group: the wave loads them with one
+// coalesced 16-byte load per lane (lane cl of group g: entries 2 cl, 2 cl + 1 of its
+// token), one round ahead, writes them to its LDS staging area and every group reads its
+// own entries back as broadcast reads. A wave's LDS instructions execute in issue order,
+// so one staging buffer per wave suffices.
 template <int BF, int RB>
-__device__ void sampled_item(const FwdParams& p, const float* Ws, const uint32_t* order, int s0, int nsampled,
-                             int64_t t0, int c0, int lane) {
-  constexpr int LPR = RB / 16;
+__device__ void sampled_item(const FwdParams& p, const float* Ws, uint4* stage, const uint32_t* order, int s0,
+                             int nsampled, int64_t t0, int c0, int lane) {
+  constexpr int LPR = RB / 16;    // lanes per row and per group
+  constexpr int NE = 2 * LPR;     // entries per group per round
   const int g = lane / LPR, cl = lane % LPR;
   const bool valid = s0 + g < nsampled;  // groups past the end repeat the item's first token
   const uint32_t e = order[valid ? s0 + g : s0];
   const int64_t tk = t0 + (e >> kUBits);
   const int U = (int)(e & ((1u << kUBits) - 1u));  // >= 1
-  const uint2* L = p.list + tk * p.d_in;
-  const int minU = wave_min_int(U), maxU = wave_max_int(U);
+  const int stride = list_stride(p.d_in);
+  const uint2* L = p.list + tk * stride;
+  const int maxU = wave_max_int(U);
   const uint32_t zero_row = (uint32_t)p.d_in * RB;
   const unsigned char* wl = reinterpret_cast<const unsigned char*>(Ws) + cl * 16;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  uint2 ring[kRing];
-  if (kRing <= minU) {
+  uint4 nxt = entry_pair(L, 2 * cl, U, stride, zero_row);
+  for (int q0 = 0; q0 < maxU; q0 += NE) {
+    uint4* st = stage;
+    wave_lds_sync();  // the previous round's reads stay ahead of this write
+    st[lane] = nxt;
+    wave_lds_sync();
+    nxt = entry_pair(L, q0 + NE + 2 * cl, U, stride, zero_row);  // next round (unused after the last)
+    const uint4* mine = st + g * LPR;                      // this group's NE entries
+    // all entry reads, then all row reads (distinct registers, so they are in flight
+    // together), then the FMAs
+    uint4 two[LPR];
 #pragma unroll
-    for (int u = 0; u < kRing; ++u) ring[u] = L[u];
-  } else {
+    for (int k = 0; k < LPR; ++k) two[k] = mine[k];
+    float4 w[2 * LPR];
 #pragma unroll
-    for (int u = 0; u < kRing; ++u) ring[u] = masked_entry(L, u, U, zero_row);
-  }
-  for (int q0 = 0; q0 < maxU; q0 += kRing) {
-    const int qn = q0 + kRing;  // the block loaded during this round
-    if (qn + kRing <= minU) {
+    for (int k = 0; k < LPR; ++k) {
+      w[2 * k] = *reinterpret_cast<const float4*>(wl + two[k].x);
+      w[2 * k + 1] = *reinterpret_cast<const float4*>(wl + two[k].z);
+    }
 #pragma unroll
-      for (int u = 0; u < kRing; ++u) {
-        const uint2 cur = ring[u];
-        ring[u] = L[qn + u];
-        fma_row(acc, wl, cur);
-      }
-    } else if (qn < maxU) {
-#pragma unroll
-      for (int u = 0; u < kRing; ++u) {
-        const uint2 cur = ring[u];
-        ring[u] = masked_entry(L, qn + u, U, zero_row);
-        fma_row(acc, wl, cur);
-      }
-    } else {
-#pragma unroll
-      for (int u = 0; u < kRing; ++u) fma_row(acc, wl, ring[u]);
+    for (int k = 0; k < 2 * LPR; ++k) {
+      const float c = __uint_as_float((k & 1) ? two[k >> 1].w : two[k >> 1].y);
+      acc.x = fmaf(c, w[k].x, acc.x);
+      acc.y = fmaf(c, w[k].y, acc.y);
+      acc.z = fmaf(c, w[k].z, acc.z);
+      acc.w = fmaf(c, w[k].w, acc.w);
     }
   }
   if (valid) store_h4<BF>(p, tk * p.d_out + c0 + 4 * cl, acc);
@@ -260,35 +275,57 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t ntok = (int64_t)p.B * p.n;
   float* Ws = reinterpret_cast<float*>(smem);  // [d_in + 1][WC], the last row zero
-  uint32_t* order = reinterpret_cast<uint32_t*>(smem + (size_t)(d_in + 1) * WC * 4);  // [kChunk]
+  uint4* stage = reinterpret_cast<uint4*>(smem + (size_t)(d_in + 1) * WC * 4) + (tid >> 6) * 64;  // 64 per wave
+  uint32_t* order = reinterpret_cast<uint32_t*>(smem + (size_t)(d_in + 1) * WC * 4 + kWavesPerBlock * 1024);
   int* satl = reinterpret_cast<int*>(order + kChunk);                                // [kChunk]
   int* ctr = satl + kChunk;  // [0] saturated, [1 + key] sort-key counts, [60] work queue
 
-  // ---- the slice of W_v, as float32, into LDS (16-byte global loads), then a zero row
+  const int64_t per_block = (ntok + p.gather_bps - 1) / p.gather_bps;
+  const int64_t t_begin = (int64_t)bis * per_block, t_end = min(t_begin + per_block, ntok);
+  // the first pass's r and U, loaded together with the slice
+  int r_first = 0, u_first = 0;
+  if (t_begin + tid < t_end) {
+    r_first = p.r[t_begin + tid];
+    u_first = p.ucount[t_begin + tid];
+  }
+
+  // ---- the slice of W_v, as float32, into LDS, then a zero row: 16-byte global loads,
+  // four per thread in flight before the conversions and LDS stores
   if (tid < WC) Ws[d_in * WC + tid] = 0.f;
   {
     using T = typename Elem<BF>::T;
     constexpr int CE = BF ? 8 : 4;  // elements per 16-byte chunk
     constexpr int CPR = WC / CE;    // chunks per slice row
     const T* W = static_cast<const T*>(p.W);
-    for (int v = tid; v < d_in * CPR; v += kThreads) {
-      const int row = v / CPR, ch = v % CPR;
-      const uint4 u = *reinterpret_cast<const uint4*>(W + (int64_t)row * d_out + c0 + ch * CE);
-      float* dst = Ws + row * WC + ch * CE;
-      if constexpr (BF) {
-        reinterpret_cast<float4*>(dst)[0] = make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
-                                                        __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
-        reinterpret_cast<float4*>(dst)[1] = make_float4(__uint_as_float(u.z << 16), __uint_as_float(u.z & 0xffff0000u),
-                                                        __uint_as_float(u.w << 16), __uint_as_float(u.w & 0xffff0000u));
-      } else {
-        *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(u.x), __uint_as_float(u.y),
-                                                      __uint_as_float(u.z), __uint_as_float(u.w));
+    const int nchunk = d_in * CPR;
+    for (int v0 = tid; v0 < nchunk; v0 += 4 * kThreads) {
+      uint4 u[4];
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const int v = min(v0 + h * kThreads, nchunk - 1);  // clamped: in range, stored only if v < nchunk
+        u[h] = *reinterpret_cast<const uint4*>(W + (int64_t)(v / CPR) * d_out + c0 + (v % CPR) * CE);
+      }
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        const int v = v0 + h * kThreads;
+        if (v < nchunk) {
+          float* dst = Ws + (v / CPR) * WC + (v % CPR) * CE;
+          if constexpr (BF) {
+            reinterpret_cast<float4*>(dst)[0] =
+                make_float4(__uint_as_float(u[h].x << 16), __uint_as_float(u[h].x & 0xffff0000u),
+                            __uint_as_float(u[h].y << 16), __uint_as_float(u[h].y & 0xffff0000u));
+            reinterpret_cast<float4*>(dst)[1] =
+                make_float4(__uint_as_float(u[h].z << 16), __uint_as_float(u[h].z & 0xffff0000u),
+                            __uint_as_float(u[h].w << 16), __uint_as_float(u[h].w & 0xffff0000u));
+          } else {
+            *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(u[h].x), __uint_as_float(u[h].y),
+                                                          __uint_as_float(u[h].z), __uint_as_float(u[h].w));
+          }
+        }
       }
     }
   }
 
-  const int64_t per_block = (ntok + p.gather_bps - 1) / p.gather_bps;
-  const int64_t t_begin = (int64_t)bis * per_block, t_end = min(t_begin + per_block, ntok);
   for (int64_t t0 = t_begin; t0 < t_end; t0 += kChunk) {
     const int m = (int)min((int64_t)kChunk, t_end - t0);
     if (tid < 64) ctr[tid] = 0;
@@ -296,8 +333,8 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
     // ---- classify this pass's tokens (one per thread) and sort the sampled ones by key
     int key = -1, rank = 0, U = 0;
     if (tid < m) {
-      const int r = p.r[t0 + tid];
-      U = min(max(p.ucount[t0 + tid], 0), d_in);
+      const int r = t0 == t_begin ? r_first : p.r[t0 + tid];
+      U = min(max(t0 == t_begin ? u_first : p.ucount[t0 + tid], 0), d_in);
       if (r >= d_in) {
         satl[atomicAdd(ctr, 1)] = tid;
       } else if (r > 0 && U > 0) {
@@ -325,7 +362,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
       it = __builtin_amdgcn_readfirstlane(it);
       if (it >= nitems) break;
       if (it < ngroups) saturated_group<BF, WC, VEC>(p, satl, t0, it, nsat, c0, lane);
-      else sampled_item<BF, RB>(p, Ws, order, (it - ngroups) * G, nsampled, t0, c0, lane);
+      else sampled_item<BF, RB>(p, Ws, stage, order, (it - ngroups) * G, nsampled, t0, c0, lane);
     }
     __syncthreads();  // the lists of this pass are rewritten next
   }
@@ -346,6 +383,7 @@ int device_cus() {
 template <int BF, int WC, bool VEC>
 hipError_t launch_wc(const FwdParams& p, hipStream_t s) {
   const size_t lds = gather_lds_bytes(p.d_in, WC);
+  if (lds > 160 * 1024) return hipErrorInvalidValue;  // gfx950: 160 KB of LDS per workgroup
   // the largest slice (2048 x 16 or 1024 x 32 floats) plus the lists; allowed once per device
   static int allowed[64] = {0};
   int dev = 0;

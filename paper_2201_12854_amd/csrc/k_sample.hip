@@ -252,7 +252,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const int incl_u = wave_inclusive_scan<int>(nloc, lane);
   const int U = __shfl(incl_u, kWave - 1, kWave);
   int pos = incl_u - nloc;
-  uint2* lst = p.list + tok * d_in;
+  uint2* lst = p.list + tok * list_stride(d_in);
   const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
 #pragma unroll
   for (int k = 0; k < PER; ++k) {

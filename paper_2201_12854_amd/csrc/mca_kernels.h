@@ -48,7 +48,7 @@ struct FwdParams {
   float* row_max;      // [B*H*n]
   float* row_inv_sum;  // [B*H*n]
   void* Henc;          // [B*n*d_out] H~ in the input dtype
-  uint2* list;         // [B*n][d_in] distinct sampled rows of a token:
+  uint2* list;         // [B*n][list_stride(d_in)] distinct sampled rows of a token:
                        // (row * gather_row_bytes(d_in), float32 bits of coef)
   int32_t* ucount;     // [B*n] number of distinct rows U of a sampled token, else 0
   int wc;              // W_v columns per gather slice (32 or 16)
@@ -65,6 +65,9 @@ hipError_t launch_sample(const FwdParams& p, hipStream_t s);
 hipError_t launch_gather(const FwdParams& p, hipStream_t s);
 // Columns per gather slice for d_in (the slice, float32, must fit the LDS with the staging area).
 __host__ __device__ inline int gather_slice_cols(int d_in) { return d_in <= 1024 ? 32 : 16; }
+// Entries reserved per token in the sample list: d_in rounded up to even, so that every
+// list starts 16-byte aligned and entries can be read in pairs.
+__host__ __device__ inline int list_stride(int d_in) { return (d_in + 1) & ~1; }
 // Bytes of one slice row in LDS (float32); list entries hold row * gather_row_bytes.
 __host__ __device__ inline int gather_row_bytes(int d_in) { return 4 * gather_slice_cols(d_in); }
 // Gather blocks per column slice: at most one block per CU over all slices (a block holds
