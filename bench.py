@@ -86,11 +86,58 @@ def stage_work(L, r, idx, elem):
     w["gather"] = dict(bytes=gather_bytes + sat_bytes, flops=2.0 * distinct * d_out + 2.0 * n_sat * d_in * d_out,
                        sampled_bytes=gather_bytes, sampled_flops=2.0 * distinct * d_out,
                        sampled_bytes_every_draw=8.0 * distinct + draws * d_out * s_in + n_sampled * d_out * s_h,
+                       sampled_flops_every_draw=2.0 * draws * d_out,
+                       bytes_every_draw=8.0 * distinct + draws * d_out * s_in + n_sampled * d_out * s_h + sat_bytes,
                        mfma_flops=2.0 * n_sat * d_in * d_out)
     w["attn_out"] = dict(bytes=2.0 * B * n * d_out * s_in + B * n * d_out * s_h + 4.0 * B * n * d_out
                          + 8.0 * B * H * n, flops=2 * qk_flops)
     stats = dict(sampled_tokens=n_sampled, saturated_tokens=n_sat, draws=draws, distinct_rows=distinct)
     return w, stats
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "k_gather_bert_base_bf16_b32_s128_traffic.md")
+GATHER_SOURCE = os.path.join(ROOT, "paper_2201_12854_amd", "csrc", "k_gather.hip")
+
+
+def source_sha256(path):
+    import hashlib
+
+    return hashlib.sha256(open(path, "rb").read()).hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per k_gather launch from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary (scaled by the copy-kernel calibration recorded there); None if the summary is
+    missing or was taken on a different k_gather source."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    for line in open(TRAFFIC_FILE):
+        if ":" in line and line.strip().startswith("- "):
+            k, v = line.strip()[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    try:
+        if vals.get("k_gather.hip sha256") != source_sha256(GATHER_SOURCE):
+            return None
+        return {"fetch_bytes": float(vals["fetch bytes per launch"]), "write_bytes": float(vals["write bytes per launch"]),
+                "bytes": float(vals["fetch bytes per launch"]) + float(vals["write bytes per launch"]),
+                "source": os.path.relpath(TRAFFIC_FILE, ROOT)}
+    except (KeyError, ValueError):
+        return None
+
+
+def copy_calibration(mib):
+    """A plain elementwise copy of known size (read mib MiB, write mib MiB): the reference
+    for scaling the FETCH_SIZE / WRITE_SIZE counters of a profiled run."""
+    import torch
+
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.mul(src, 1.0, out=dst)
+    torch.cuda.synchronize()
+    log(f"copy calibration: 3 x elementwise copy of {mib} MiB (read {mib} MiB + write {mib} MiB each)")
 
 
 def dense_baseline(t, L, steps, warmup):
@@ -166,6 +213,8 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip dense baseline and other alphas")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="also run a plain copy of MIB MiB (for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the multi-GPU layout is a "
@@ -207,6 +256,8 @@ def main():
     torch.cuda.synchronize()
     st = prof.collect()
     stage_us = {k: (v[0] / max(v[1], 1)) * 1e3 for k, v in st.items()}
+    ms_prof, _ = time_loop(pplan.run, args.steps, 0)
+    prof.collect()
     log("stage us: " + ", ".join(f"{k}={v:.1f}" for k, v in stage_us.items()))
 
     ex = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
@@ -218,15 +269,23 @@ def main():
     dom = max(stage_us, key=lambda k: stage_us[k])
     dur = stage_us[dom] * 1e-6
     if dom == "gather":
-        # the sampled rows are gathered from a W_v slice held in LDS: the kernel is bound by
-        # LDS reads and float32 FMAs, not HBM; achieved = gather FMAs only (the MFMA work on
-        # saturated tokens in the same launch is not counted)
-        ach = work[dom]["sampled_flops"] / dur / 1e12
+        # Sampled rows are gathered from a W_v slice held in LDS, so the kernel is bound by
+        # LDS reads and float32 FMA issue, not HBM. achieved = the algorithmic FLOPs of the
+        # sampled tokens (2 r_j d_out per token, every draw counted) per launch over the
+        # measured launch duration; the MFMA work on saturated tokens in the same launch is
+        # not counted. Executed FLOPs (duplicates merged) are reported beside it.
+        ach = work[dom]["sampled_flops_every_draw"] / dur / 1e12
         roof = {"kernel": "k_gather", "bound": "alu", "achieved": ach, "peak": FP32_VECTOR_PEAK_TFLOPS,
                 "unit": "TFLOP/s", "frac": ach / FP32_VECTOR_PEAK_TFLOPS, "traffic": None,
-                "hbm_view": {"algorithmic_GBps": work[dom]["bytes"] / dur / 1e9, "peak": HBM_PEAK_GBS,
-                             "frac": work[dom]["bytes"] / dur / 1e9 / HBM_PEAK_GBS,
-                             "counting_every_draw_GBps": work[dom]["sampled_bytes_every_draw"] / dur / 1e9}}
+                "executed_TFLOPs": work[dom]["sampled_flops"] / dur / 1e12,
+                "hbm_view": {"algorithmic_GBps": work[dom]["bytes_every_draw"] / dur / 1e9, "peak": HBM_PEAK_GBS,
+                             "frac": work[dom]["bytes_every_draw"] / dur / 1e9 / HBM_PEAK_GBS,
+                             "note": "algorithmic bytes (one W_v row per draw) per launch / duration; W_v is "
+                                     "on chip (LDS slices), so this exceeds the HBM roofline"}}
+        tr = measured_traffic()
+        if tr is not None:
+            roof["traffic"] = tr["bytes"]
+            roof["traffic_detail"] = tr
     else:
         ach = work[dom]["flops"] / dur / 1e12
         roof = {"kernel": dom, "bound": "mfma", "achieved": ach, "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -246,7 +305,8 @@ def main():
               "config": {"workload": L.name, "batch": L.batch, "seq_len": L.seq, "hidden": L.d_in,
                          "heads": L.heads, "d_head": 64, "alpha": args.alpha, "seed": args.seed,
                          "token_scale": "lognormal(0, 0.5)"},
-              "roofline": roof, "stages": stages, "prepare_us": prep_ms * 1e3, "flop_reduction": red}
+              "roofline": roof, "stages": stages, "ms_per_step_with_stage_events": ms_prof,
+              "prepare_us": prep_ms * 1e3, "flop_reduction": red}
 
     if not args.no_extras:
         dense = dense_baseline(t, L, args.steps, args.warmup)
@@ -259,6 +319,8 @@ def main():
             ms_a, _ = time_loop(p2.run, args.steps, args.warmup)
             other[str(a)] = {"ms_per_step": ms_a, "tokens_per_s": L.tokens / (ms_a * 1e-3)}
         record["other_alphas"] = other
+    if args.calibrate_copy:
+        copy_calibration(args.calibrate_copy)
     if not args.no_cpu_baseline:
         record["cpu_baseline"] = cpu_baseline(L, args.alpha, args.seed, args.cpu_seconds)
         log(f"cpu oracle: {record['cpu_baseline']['value']:.4g} tokens/s")
