@@ -59,7 +59,9 @@ def time_loop(fn, steps, warmup):
 
 
 def stage_work(L, r, idx, elem):
-    """Algorithmic bytes and flops of every stage for one forward."""
+    """Algorithmic bytes and flops of every stage for one forward pass: per sampled token
+    s_x d_in + r_j d_out s_W bytes and 2 r_j d_out flops (every draw counted; merged
+    duplicates are also reported), per saturated token 2 d_in d_out MFMA flops."""
     B, n, d_in, d_out, H = L.batch, L.seq, L.d_in, L.d_out, L.heads
     s_in, s_h = elem, elem  # input element size; H~ stored in the input dtype
     lens = L.lens.astype(np.int64)
