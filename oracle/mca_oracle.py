@@ -16,6 +16,9 @@ Mechanism" (AAAI-22), step by step, in the paper's notation:
   O4  sqrt(r_j) = n * m_j / alpha                              (Eq. 9)
   O5  p_ji proportional to |x_ji| * ||W[i]||                   (Eq. 4, the DKM-optimal
                                                                  probability, per token)
+      or, in the paper's own input-independent mode,
+      p_i proportional to ||W[i]||^2                           (Eq. 6, one distribution
+                                                                 per weight matrix)
   O6  i.i.d. draws with replacement, Pr[s_k = i] = p(i)        (Eq. 2 and the text after it)
   O7  H~[j] = (1/r_j) sum_k x_{j,s_k} W[s_k] / p(s_k)          (Eq. 2 applied to X[j] W,
                                                                  i.e. Eq. 5's inner sum)
@@ -44,6 +47,11 @@ reason in the design notes of the repository):
   row b; u = o0 | o1 << 32; t = floor(u * T / 2^64); s_k = min{i : C_i > t}
   with C the inclusive prefix sums of w.
 * A token whose weights are all zero (x_j = 0) is encoded as 0.
+* Eq. 6 mode: v_i = fp32(rho_i * rho_i) (one IEEE float32 multiply of the
+  float32 row norm), then the same fixed-point weights, prefix sums, random
+  stream and inverse CDF. The table depends on W only, so it is built once and
+  every token draws from it; a token with x_j = 0 still draws, with
+  coefficients 0, so its H~[j] is 0.
 """
 from __future__ import annotations
 
@@ -54,6 +62,9 @@ import numpy as np
 
 D_HEAD = 64
 MASK32 = 0xFFFFFFFF
+
+SAMPLING_TOKEN = "token"    # Eq. 4: p_ji proportional to |x_ji| ||W[i]||
+SAMPLING_WEIGHT = "weight"  # Eq. 6: p_i proportional to ||W[i]||^2
 
 # Philox4x32 constants as published by Salmon, Moraes, Dror and Shaw,
 # "Parallel Random Numbers: As Easy as 1, 2, 3" (SC'11): two round multipliers
@@ -157,17 +168,11 @@ def sample_counts(m: np.ndarray, lens, alpha: float, d_in: int) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- O5
-def fixed_point_weights(x: np.ndarray, rho: np.ndarray):
-    """Integer sampling weights of one token (Eq. 4 with B = W: p_i is proportional
-    to |x_i| * ||W[i]||).
-
-    v_i = fp32(|x_i| * rho_i); e such that v_max = f * 2^e, f in [0.5, 1);
-    w_i = floor(v_i * 2^(32-e)) (exact: a power-of-two scaling of a float32
-    value in float64). Returns (w as Python ints, prefix sums C, total T), or
-    None when every v_i is 0.
-    """
-    v = np.abs(np.asarray(x, dtype=np.float32)) * np.asarray(rho, dtype=np.float32)
-    v = v.astype(np.float32)
+def quantise(v: np.ndarray):
+    """32-bit fixed point of non-negative float32 values: e such that
+    v_max = f * 2^e, f in [0.5, 1); w_i = floor(v_i * 2^(32-e)) (exact: a
+    power-of-two scaling of a float32 value in float64). Returns (w as Python
+    ints, inclusive prefix sums C, total T), or None when every v_i is 0."""
     vmax = float(v.max()) if v.size else 0.0
     if vmax == 0.0:
         return None
@@ -179,6 +184,21 @@ def fixed_point_weights(x: np.ndarray, rho: np.ndarray):
         acc += wi
         C.append(acc)
     return w, C, acc
+
+
+def fixed_point_weights(x: np.ndarray, rho: np.ndarray):
+    """Integer sampling weights of one token (Eq. 4 with B = W: p_i is proportional
+    to |x_i| * ||W[i]||): v_i = fp32(|x_i| * rho_i), quantised."""
+    v = np.abs(np.asarray(x, dtype=np.float32)) * np.asarray(rho, dtype=np.float32)
+    return quantise(v.astype(np.float32))
+
+
+def weight_fixed_point(rho: np.ndarray):
+    """Integer sampling weights of the paper's input-independent distribution
+    (Eq. 6: p_i = ||W[i]||^2 / ||W||_F^2): v_i = fp32(rho_i * rho_i), quantised.
+    One table per weight matrix."""
+    r32 = np.asarray(rho, dtype=np.float32)
+    return quantise((r32 * r32).astype(np.float32))
 
 
 def index_from_u(u: int, C, T: int) -> int:
@@ -210,15 +230,19 @@ def estimate_from_indices(x: np.ndarray, W: np.ndarray, w, T: int, idx, r: int) 
     return out
 
 
-def encode_token(x, W, rho, r: int, seed: int, b: int, j: int):
-    """H~[j] for one token. Returns (H~[j], indices, coefficients)."""
+def encode_token(x, W, rho, r: int, seed: int, b: int, j: int, *, sampling=SAMPLING_TOKEN, table=None):
+    """H~[j] for one token. Returns (H~[j], indices, coefficients). In Eq. 6 mode
+    ``table`` is weight_fixed_point(rho) (computed here when not given)."""
     d_in = W.shape[0]
     if r <= 0:
         return np.zeros(W.shape[1]), [], np.zeros(0)
     if r >= d_in:  # O8: saturated, exact encoding
         return np.asarray(x, np.float64) @ np.asarray(W, np.float64), [], np.zeros(0)
-    fp = fixed_point_weights(x, rho)
-    if fp is None:  # all-zero token
+    if sampling == SAMPLING_WEIGHT:
+        fp = table if table is not None else weight_fixed_point(rho)
+    else:
+        fp = fixed_point_weights(x, rho)
+    if fp is None:  # all-zero token (Eq. 4) or all-zero W (Eq. 6)
         return np.zeros(W.shape[1]), [], np.zeros(0)
     w, C, T = fp
     idx = draw_indices(C, T, r, seed, b, j)
@@ -230,7 +254,7 @@ def encode_token(x, W, rho, r: int, seed: int, b: int, j: int):
 
 # --------------------------------------------------------------------------- forward
 def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_override=None,
-                rho=None, y_rows=None, want_samples=False, want_exact=False):
+                rho=None, y_rows=None, want_samples=False, want_exact=False, sampling=SAMPLING_TOKEN):
     """Full MCA forward (O1-O9) for right-padded sequences.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W: [d_in, heads*64] (all float32
@@ -240,6 +264,8 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
     tokens, because every query row depends on all of them).
     Returns a dict with rho, m, r, Htilde, Y (or Y at y_rows), and optionally
     samples (per token: indices, coefficients) and the exact Y* of Eq. 1.
+    ``sampling`` selects the probability: SAMPLING_TOKEN (Eq. 4, per token) or
+    SAMPLING_WEIGHT (Eq. 6, one table per weight matrix).
     """
     B, n, d_in = X.shape
     d_out = W.shape[1]
@@ -254,11 +280,14 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
         r = np.clip(r, 0, d_in)
         for b in range(B):
             r[b, int(lens[b]):] = 0
+    if sampling not in (SAMPLING_TOKEN, SAMPLING_WEIGHT):
+        raise ValueError(f"unknown sampling mode {sampling!r}")
+    table = weight_fixed_point(rho) if sampling == SAMPLING_WEIGHT else None
     Ht = np.zeros((B, n, d_out), dtype=np.float64)
     samples = {}
     for b in range(B):
         for j in range(n):
-            H, idx, coef = encode_token(X[b, j], W, rho, int(r[b, j]), seed, b, j)
+            H, idx, coef = encode_token(X[b, j], W, rho, int(r[b, j]), seed, b, j, sampling=sampling, table=table)
             Ht[b, j] = H
             if want_samples:
                 samples[(b, j)] = (idx, coef)
