@@ -49,6 +49,13 @@ typedef enum mca_dtype {
   MCA_BF16 = 1   /* bfloat16 inputs; bf16 MFMA with fp32 accumulation */
 } mca_dtype;
 
+/* Sampling probability of the encoding (Sec. "Formulation of Sampling Probability"). */
+typedef enum mca_sampling {
+  MCA_SAMPLING_TOKEN = 0,   /* Eq. 4 per token: p_ji proportional to |x_ji| * ||W_v[i, :]|| */
+  MCA_SAMPLING_WEIGHT = 1   /* Eq. 6, input independent: p_i proportional to ||W_v[i, :]||^2
+                               (the paper's own MCA); one distribution for every token */
+} mca_sampling;
+
 /* Stages of the forward pass, in launch order (profiler slots). */
 typedef enum mca_stage {
   MCA_STAGE_SCORES_COLMAX = 0,  /* softmax(Q K^T / 8) row statistics and column-max partials */
@@ -77,7 +84,7 @@ typedef struct mca_forward_desc {
   int64_t d_head;    /* must be 64 (MCA_ERR_UNSUPPORTED otherwise) */
   int64_t d_in;      /* 1 .. 2048 */
   int32_t dtype;     /* mca_dtype of Q, K, X and W_v */
-  int32_t reserved;  /* must be 0 */
+  int32_t sampling;  /* mca_sampling */
   double alpha;      /* attention error coefficient of Eq. 9; finite and > 0 */
   uint64_t seed;     /* Philox4x32-10 key (low word, high word) */
   /* device [B] int32 valid lengths (right padding), clamped to 1..n; NULL = all n */
@@ -151,7 +158,7 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  * `workspace` must hold at least mca_workspace_size bytes; its contents on entry do not
  * matter and are overwritten.
  * Errors: MCA_ERR_INVALID_ARGUMENT (null required pointer, size < 1, non-finite or
- * non-positive alpha, reserved != 0, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
+ * non-positive alpha, unknown sampling mode, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
  * != 64, d_out not a multiple of 256 or > 2048, d_in > 2048), MCA_ERR_WORKSPACE_TOO_SMALL,
  * MCA_ERR_HIP.
  */

@@ -22,6 +22,15 @@ MCA_ERR_WORKSPACE_TOO_SMALL = 3
 MCA_ERR_HIP = 4
 MCA_F32 = 0
 MCA_BF16 = 1
+MCA_SAMPLING_TOKEN = 0   # Eq. 4 per token
+MCA_SAMPLING_WEIGHT = 1  # Eq. 6, input independent
+SAMPLING = {"token": MCA_SAMPLING_TOKEN, "weight": MCA_SAMPLING_WEIGHT}
+
+
+def _sampling_code(sampling) -> int:
+    if sampling not in SAMPLING:
+        raise ValueError(f"sampling must be one of {sorted(SAMPLING)} (got {sampling!r})")
+    return SAMPLING[sampling]
 NUM_STAGES = 4
 STAGES = ("scores_colmax", "sample", "gather", "attn_out")
 
@@ -34,7 +43,7 @@ class ForwardDesc(ctypes.Structure):
         ("d_head", ctypes.c_int64),
         ("d_in", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
-        ("reserved", ctypes.c_int32),
+        ("sampling", ctypes.c_int32),
         ("alpha", ctypes.c_double),
         ("seed", ctypes.c_uint64),
         ("seq_lens", ctypes.c_void_p),
@@ -122,10 +131,10 @@ def _stream_handle(device) -> int:
 
 def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None, r_in=None,
               colmax_out=None, sample_idx_out=None, sample_coef_out=None, encoded_out=None,
-              profiler=None) -> ForwardDesc:
+              profiler=None, sampling=0) -> ForwardDesc:
     d = ForwardDesc()
     d.batch, d.seq, d.heads, d.d_head, d.d_in = batch, seq, heads, 64, d_in
-    d.dtype, d.reserved = dtype_code, 0
+    d.dtype, d.sampling = dtype_code, sampling
     d.alpha, d.seed = float(alpha), int(seed) & 0xFFFFFFFFFFFFFFFF
     d.seq_lens, d.r_in = _ptr(seq_lens), _ptr(r_in)
     d.colmax_out, d.sample_idx_out = _ptr(colmax_out), _ptr(sample_idx_out)
@@ -180,7 +189,7 @@ class ForwardResult:
 
 def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int,
                       seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
-                      workspace=None, out=None, profiler=None) -> ForwardResult:
+                      workspace=None, out=None, profiler=None, sampling: str = "token") -> ForwardResult:
     """One MCA forward pass through libmca on the current HIP stream.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
@@ -188,7 +197,8 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     seq_lens: optional int32 [B]. r_in: optional int32 [B, n] overriding the count
     rule. ``export`` also returns the column max and H~ (float32); ``export_samples``
     the per-draw indices and coefficients ([B, n, d_in], first r_j entries valid).
-    ``out`` may pass preallocated (Y, r).
+    ``out`` may pass preallocated (Y, r). ``sampling``: "token" (Eq. 4, per token) or
+    "weight" (Eq. 6, the paper's input-independent probability).
     """
     import torch
 
@@ -218,7 +228,8 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
         res.sample_coef = torch.zeros((B, n, d_in), dtype=torch.float32, device=dev)
     desc = make_desc(B, n, heads, d_in, dt, alpha, seed, seq_lens=seq_lens, r_in=r_in,
                      colmax_out=res.colmax, sample_idx_out=res.sample_idx,
-                     sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler)
+                     sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler,
+                     sampling=_sampling_code(sampling))
     ws_bytes = workspace_size(desc)
     if workspace is None or workspace.numel() < ws_bytes:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
@@ -267,7 +278,7 @@ class ForwardPlan:
     stream), so that ``run()`` is a single C call: for timing loops and serving."""
 
     def __init__(self, Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
-                 r_in=None, profiler=None):
+                 r_in=None, profiler=None, sampling: str = "token"):
         import torch
 
         lib = load_library()
@@ -276,7 +287,7 @@ class ForwardPlan:
         dev = X.device
         self._keep = (Q, K, X, W_v, prepared, seq_lens, r_in)
         self.desc = make_desc(B, n, heads, d_in, _dtype_code(X), alpha, seed, seq_lens=seq_lens, r_in=r_in,
-                              profiler=profiler)
+                              profiler=profiler, sampling=_sampling_code(sampling))
         ws = workspace_size(self.desc)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
         self.Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)

@@ -6,7 +6,8 @@
 //      [1, d_in]; padded keys get 0. r_j = d_in marks a saturated token, encoded exactly
 //      by the gather kernel's MFMA path (cost of d_in samples, no error).
 //   2. sampling weights of Eq. 4 for the product x_j W_v: v_i = |x_ji| * rho_i in one
-//      float32 multiply, quantised to 32-bit fixed point aligned to the largest v_i,
+//      float32 multiply (or, in the paper's input-independent mode of Eq. 6,
+//      v_i = rho_i * rho_i), quantised to 32-bit fixed point aligned to the largest v_i,
 //      w_i = floor(v_i 2^(32-e)); inclusive prefix sums C (uint64) by a wavefront scan
 //      (each lane owns a contiguous run of rows), stored in the wave's part of the LDS.
 //   3. r_j i.i.d. draws with replacement (Eq. 2): Philox4x32-10 with counter (k, j, b, 0),
@@ -130,6 +131,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   // full: d_in = 64 PER, every lane owns exactly PER rows and its runs of x, rho, C and
   // cnt are 16-byte aligned (i0 = PER lane), so they move as 16-byte vectors
   const bool full = d_in == kWave * PER;
+  const bool ws = p.weight_sampling != 0;
   float xv[PER], vv[PER];
   float lmax = 0.f;
   if (full) {
@@ -138,10 +140,11 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
       const float4 xs = load4_f32(xrow + i0 + k);
       const float4 rs = *reinterpret_cast<const float4*>(p.rownorm + i0 + k);
       xv[k] = xs.x; xv[k + 1] = xs.y; xv[k + 2] = xs.z; xv[k + 3] = xs.w;
-      vv[k] = __fmul_rn(fabsf(xs.x), rs.x);
-      vv[k + 1] = __fmul_rn(fabsf(xs.y), rs.y);
-      vv[k + 2] = __fmul_rn(fabsf(xs.z), rs.z);
-      vv[k + 3] = __fmul_rn(fabsf(xs.w), rs.w);
+      // Eq. 4: |x_i| rho_i; Eq. 6: rho_i^2 (the same for every token)
+      vv[k] = __fmul_rn(ws ? rs.x : fabsf(xs.x), rs.x);
+      vv[k + 1] = __fmul_rn(ws ? rs.y : fabsf(xs.y), rs.y);
+      vv[k + 2] = __fmul_rn(ws ? rs.z : fabsf(xs.z), rs.z);
+      vv[k + 3] = __fmul_rn(ws ? rs.w : fabsf(xs.w), rs.w);
     }
 #pragma unroll
     for (int k = 0; k < PER; ++k) lmax = fmaxf(lmax, vv[k]);
@@ -152,7 +155,8 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
       vv[k] = 0.f;
       if (k < nrows) {
         xv[k] = load_f32(xrow, i0 + k);
-        vv[k] = __fmul_rn(fabsf(xv[k]), p.rownorm[i0 + k]);
+        const float rk = p.rownorm[i0 + k];
+        vv[k] = __fmul_rn(ws ? rk : fabsf(xv[k]), rk);
         lmax = fmaxf(lmax, vv[k]);
       }
     }
@@ -180,7 +184,8 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
     if (lane == 0) p.ucount[tok] = 0;
     return;
   }
-  if (r == 0 || !(vmax > 0.f) || !(vmax <= 3.40282347e38f)) {  // padded, x_j = 0 or non-finite
+  // padded key; no weights (x_j = 0 under Eq. 4, W_v = 0 under Eq. 6); non-finite weights
+  if (r == 0 || !(vmax > 0.f) || !(vmax <= 3.40282347e38f)) {
     if (lane == 0) p.ucount[tok] = 0;
     for (int c = 4 * lane; c < p.d_out; c += 4 * kWave) write_zero4<BF>(p, tok * p.d_out + c);
     return;

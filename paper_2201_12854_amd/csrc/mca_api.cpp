@@ -64,7 +64,8 @@ mca_status check_desc(const mca_forward_desc* d) {
   if (!d) return fail(MCA_ERR_INVALID_ARGUMENT, "desc is NULL");
   if (d->batch < 1 || d->seq < 1 || d->heads < 1 || d->d_in < 1 || d->d_head < 1)
     return fail(MCA_ERR_INVALID_ARGUMENT, "batch, seq, heads, d_head and d_in must be >= 1");
-  if (d->reserved != 0) return fail(MCA_ERR_INVALID_ARGUMENT, "reserved field must be 0");
+  if (d->sampling != MCA_SAMPLING_TOKEN && d->sampling != MCA_SAMPLING_WEIGHT)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "sampling %d is not MCA_SAMPLING_TOKEN or MCA_SAMPLING_WEIGHT", d->sampling);
   if (d->dtype != MCA_F32 && d->dtype != MCA_BF16)
     return fail(MCA_ERR_INVALID_ARGUMENT, "dtype %d is not MCA_F32 or MCA_BF16", d->dtype);
   if (!std::isfinite(d->alpha) || !(d->alpha > 0.0))
@@ -217,6 +218,7 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.d_in = (int)desc->d_in;
   p.d_out = (int)(desc->heads * 64);
   p.bf16 = desc->dtype == MCA_BF16;
+  p.weight_sampling = desc->sampling == MCA_SAMPLING_WEIGHT;
   p.qtiles = L.qtiles;
   p.nparts = L.nparts;
   p.din_pad = (int)mca::prepared_din_pad(desc->d_in);

@@ -28,6 +28,7 @@ inline size_t prepared_bytes(int bf16, int64_t d_in, int64_t d_out) {
 struct FwdParams {
   int B, n, H, d_in, d_out;
   int bf16;     // 0: float32 inputs, 1: bfloat16 inputs
+  int weight_sampling;  // 0: Eq. 4, p_ji ~ |x_ji| rho_i; 1: Eq. 6, p_i ~ rho_i^2
   int qtiles;   // query tiles per sequence = ceil(n / kQueryTile)
   int nparts;   // column-max partials per token = H * qtiles
   int din_pad;  // row length of W_v^T

@@ -32,7 +32,7 @@ def test_header_enums_match_binding():
     text = open(HEADER).read()
     for name, val in [("MCA_OK", 0), ("MCA_ERR_INVALID_ARGUMENT", 1), ("MCA_ERR_UNSUPPORTED", 2),
                       ("MCA_ERR_WORKSPACE_TOO_SMALL", 3), ("MCA_ERR_HIP", 4), ("MCA_F32", 0), ("MCA_BF16", 1),
-                      ("MCA_NUM_STAGES", 4)]:
+                      ("MCA_NUM_STAGES", 4), ("MCA_SAMPLING_TOKEN", 0), ("MCA_SAMPLING_WEIGHT", 1)]:
         assert re.search(rf"\b{name}\s*=\s*{val}\b", text), name
     # struct layout: the binding's ctypes mirror has the header's field order
     body = re.search(r"typedef struct mca_forward_desc \{(.*?)\} mca_forward_desc;", text, re.S).group(1)
@@ -95,7 +95,8 @@ def test_prepared_size_formula():
     ("heads", 36, binding.MCA_ERR_UNSUPPORTED),   # d_out = 2304 > 2048
     ("d_head", 128, binding.MCA_ERR_UNSUPPORTED),
     ("dtype", 7, binding.MCA_ERR_INVALID_ARGUMENT),
-    ("reserved", 1, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("sampling", 2, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("sampling", -1, binding.MCA_ERR_INVALID_ARGUMENT),
 ])
 def test_desc_validation(field, value, status):
     d = _desc()

@@ -30,13 +30,13 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _full_check(L, dev, alpha, seed, *, check_e2e_y=True):
+def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token"):
     """Oracle vs GPU on every stage; returns (#ambiguous tokens, #sampled tokens)."""
     print(f"[case] {L.name} dtype={L.dtype} B={L.batch} n={L.seq} d_in={L.d_in} H={L.heads} "
-          f"alpha={alpha} seed={seed}", flush=True)
-    ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed, want_samples=True)
+          f"alpha={alpha} seed={seed} sampling={sampling}", flush=True)
+    ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed, want_samples=True, sampling=sampling)
     t = to_device(L, dev)
-    g = run_gpu(L, dev, alpha, seed, tensors=t)
+    g = run_gpu(L, dev, alpha, seed, tensors=t, sampling=sampling)
     assert np.array_equal(g["rho"], ref["rho"])
     valid = np.arange(L.seq)[None, :] < L.lens[:, None]
     m_ref = ref["m"]
@@ -51,7 +51,7 @@ def _full_check(L, dev, alpha, seed, *, check_e2e_y=True):
     if check_e2e_y and not amb.any():
         assert row_rel_err(g["Y"], ref["Y"], L.lens) <= TOL_Y[L.dtype]
     # counts fixed to the oracle's: indices, coefficients, H~ and Y
-    g2 = run_gpu(L, dev, alpha, seed, r_in=ref["r"], export_samples=True, tensors=t)
+    g2 = run_gpu(L, dev, alpha, seed, r_in=ref["r"], export_samples=True, tensors=t, sampling=sampling)
     assert np.array_equal(g2["r"], ref["r"])
     n_tok = compare_samples(g2, ref, L)
     assert row_rel_err(g2["H"], ref["Htilde"], L.lens) <= TOL_H
@@ -225,3 +225,49 @@ def test_gpu_estimator_unbiased(dev):
                  - exact[j] ** 2) / 12
         z = (Hs[:, j].mean(axis=0) - exact[j]) / np.sqrt(var_c / S)
         assert np.max(np.abs(z)) < 5.5, (j, np.max(np.abs(z)))
+
+
+# ---------------------------------------------------------------- Eq. 6 sampling mode
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("alpha", [0.2, 0.4, 1.0])
+def test_eq6_small_ragged(dev, dtype, alpha):
+    L = wl.make_layer(2, 40, 96, 4, dtype, data_seed=5, lens=np.array([40, 23]), q_scale=3.0,
+                      token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, alpha, seed=11, sampling="weight")
+    assert n_tok > 0
+
+
+def test_eq6_bert_base_bf16(dev):
+    L = wl.bert_base_bf16()
+    _full_check(L, dev, 0.4, L.seed, sampling="weight")
+
+
+def test_eq6_zero_and_one_hot_tokens(dev):
+    # under Eq. 6 a zero token still draws (coefficients 0, H~ = 0); a one-hot token keeps one row
+    L = wl.make_layer(1, 32, 64, 4, "f32", data_seed=21, q_scale=1.0)
+    L.X[0, 3] = 0.0
+    L.X[0, 5] = 0.0
+    L.X[0, 5, 17] = 2.5
+    r_in = np.full((1, 32), 9, np.int64)
+    print("[case] eq6 zero / one-hot tokens", flush=True)
+    ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, 0.4, 3, r_override=r_in, want_samples=True,
+                             sampling="weight")
+    g = run_gpu(L, dev, 0.4, 3, r_in=r_in, export_samples=True, sampling="weight")
+    compare_samples(g, ref, L)
+    assert np.all(g["H"][0, 3] == 0) and np.all(g["coef"][0, 3, :9] == 0)
+    assert len(ref["samples"][(0, 3)][0]) == 9
+    assert row_rel_err(g["H"], ref["Htilde"], L.lens) <= TOL_H
+
+
+def test_eq6_draws_do_not_depend_on_x(dev):
+    L1 = wl.make_layer(1, 32, 64, 4, "bf16", data_seed=23)
+    L2 = wl.make_layer(1, 32, 64, 4, "bf16", data_seed=23)
+    L2.X = wl.round_to_bf16(L2.X[:, ::-1, :].copy() * 1.5)
+    r_in = np.full((1, 32), 13, np.int64)
+    print("[case] eq6 draws independent of x", flush=True)
+    g1 = run_gpu(L1, dev, 0.4, 7, r_in=r_in, export_samples=True, sampling="weight")
+    g2 = run_gpu(L2, dev, 0.4, 7, r_in=r_in, export_samples=True, sampling="weight")
+    assert np.array_equal(g1["idx"][..., :13], g2["idx"][..., :13])
+    t1 = run_gpu(L1, dev, 0.4, 7, r_in=r_in, export_samples=True)
+    t2 = run_gpu(L2, dev, 0.4, 7, r_in=r_in, export_samples=True)
+    assert not np.array_equal(t1["idx"][..., :13], t2["idx"][..., :13])
