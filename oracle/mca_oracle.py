@@ -172,9 +172,11 @@ def quantise(v: np.ndarray):
     """32-bit fixed point of non-negative float32 values: e such that
     v_max = f * 2^e, f in [0.5, 1); w_i = floor(v_i * 2^(32-e)) (exact: a
     power-of-two scaling of a float32 value in float64). Returns (w as Python
-    ints, inclusive prefix sums C, total T), or None when every v_i is 0."""
+    ints, inclusive prefix sums C, total T), or None when every v_i is 0 or some
+    v_i is not finite (a float32 overflow of |x_i| rho_i or rho_i^2): such a
+    token has no usable distribution and is encoded as 0."""
     vmax = float(v.max()) if v.size else 0.0
-    if vmax == 0.0:
+    if vmax == 0.0 or not math.isfinite(vmax):
         return None
     _, e = math.frexp(vmax)
     w = [int(math.floor(math.ldexp(float(vi), 32 - e))) for vi in v]

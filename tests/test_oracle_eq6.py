@@ -128,3 +128,15 @@ def test_eq6_layer_keeps_counts_and_saturated_tokens():
     np.testing.assert_allclose(b["Htilde"][sat], a["Htilde"][sat], rtol=0, atol=0)
     with pytest.raises(ValueError):
         oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, 0.3, 5, sampling="rows")
+
+
+def test_non_finite_weights_encode_zero():
+    # a row norm whose square overflows float32 leaves no usable distribution
+    W = np.ones((8, 4), np.float32)
+    W[2] = 3e19
+    rho = oracle.row_norms(W)
+    assert oracle.weight_fixed_point(rho) is None
+    x = np.ones(8, np.float32)
+    H, idx, _ = oracle.encode_token(x, W, rho, 3, 0, 0, 0, sampling=W6)
+    assert idx == [] and np.all(H == 0)
+    assert oracle.fixed_point_weights(np.full(8, 3e38, np.float32), rho) is None
