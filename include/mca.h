@@ -123,6 +123,12 @@ typedef struct mca_forward_desc {
  *                                    16 g + r hold W_v[s*KS + g*E + e][16 t + r], e < E
  *                                    (E = 8 bf16 / 4 float32); k zero padded to a multiple
  *                                    of 128, columns to a multiple of 16
+ *   offset round_up(end of W_v^T, 256): uint64 [d_in] inclusive prefix sums C of the
+ *                                    input-independent weights of Eq. 6: v_i =
+ *                                    float32(rownorm[i] * rownorm[i]), w_i =
+ *                                    floor(v_i 2^(32-e)) with max_i v_i = f 2^e, f in
+ *                                    [0.5, 1); all zero when every v_i is 0 or one is
+ *                                    not finite (then every sampled token encodes as 0)
  * mca_prepared_size gives the buffer size (host only). mca_prepare_weights fills it from
  * W_v (device [d_in, d_out] of `dtype`).
  * Errors: MCA_ERR_INVALID_ARGUMENT for null pointers, sizes < 1, d_in > 2048,
@@ -147,10 +153,12 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  *           padded keys. r_j = d_in marks a saturated token.
  *   H~[j] = (1/r_j) sum_k x_{j,s_k} W_v[s_k] / p(s_k)   for 0 < r_j < d_in
  *           with p(i) = w_i / T the 32-bit fixed-point form of |x_ji| * rownorm[i]
- *           (Eq. 4 for the product x_j W_v), s_k drawn i.i.d. with replacement
+ *           (Eq. 4 for the product x_j W_v; MCA_SAMPLING_TOKEN) or of rownorm[i]^2
+ *           (Eq. 6; MCA_SAMPLING_WEIGHT, from the prepared table), s_k drawn i.i.d. with replacement
  *           (Eq. 2) by Philox4x32-10 with key `seed` and counter (k, j, b, 0) and
  *           an inverse-CDF search; H~[j] = x_j W_v exactly when r_j = d_in; H~[j] = 0
- *           when r_j = 0 or x_j = 0.
+ *           when r_j = 0, when x_j = 0 under Eq. 4, and when no distribution can be
+ *           formed (all weights 0 or one of them not finite).
  *   Y_h   = A_h H~_h (per head column slice)
  * Inputs Q, K, X, W_v (device, `desc->dtype`) and `prepared` (filled by
  * mca_prepare_weights from this W_v with the same dtype and sizes). Outputs Y (device [B, n, d_out] float32) and r (device [B, n]

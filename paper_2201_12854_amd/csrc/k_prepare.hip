@@ -2,7 +2,9 @@
 // statistic of W is computed once per weight matrix and cached, not per forward pass):
 //   rho_i = ||W_v[i, :]||, the row norms that scale the sampling weights of Eq. 4;
 //   W_v^T in MFMA fragment order, the B operand of the MFMA products that encode saturated
-//   tokens exactly (one coalesced 1 KB load per 16x16 tile and k step).
+//   tokens exactly (one coalesced 1 KB load per 16x16 tile and k step);
+//   the sampling table of the paper's input-independent probability (Eq. 6), which
+//   depends on W only: fixed-point weights of rho_i^2 and their prefix sums.
 #include "mca_device.h"
 #include "mca_kernels.h"
 
@@ -57,11 +59,57 @@ __global__ __launch_bounds__(256) void k_fragment_wt(const void* Wp, int d_in, i
   for (int e = 0; e < E; ++e) dst[e] = (c < d_out && k0 + e < d_in) ? W[(int64_t)(k0 + e) * d_out + c] : T(0);
 }
 
+// Sampling table of the paper's input-independent probability (Eq. 6): v_i = fp32(rho_i^2),
+// 32-bit fixed point aligned to the largest v_i, inclusive prefix sums. One block; each
+// thread owns rows 2t and 2t + 1 (d_in <= 2048). All zero when every v_i is 0 or some v_i
+// is not finite (no distribution: such tokens are encoded as 0).
+__global__ __launch_bounds__(1024) void k_weight_table(const float* rownorm, int d_in, uint64_t* C) {
+  __shared__ float smax[16];
+  __shared__ uint64_t ssum[16];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int i0 = 2 * tid;
+  float v0 = 0.f, v1 = 0.f;
+  if (i0 < d_in) v0 = __fmul_rn(rownorm[i0], rownorm[i0]);
+  if (i0 + 1 < d_in) v1 = __fmul_rn(rownorm[i0 + 1], rownorm[i0 + 1]);
+  // max with NaN ignored by fmaxf, so test finiteness on the values themselves
+  const float lm = (v0 <= 3.40282347e38f && v1 <= 3.40282347e38f) ? fmaxf(v0, v1) : __int_as_float(0x7f800000);
+  const float m = wave_max(lm);
+  if (lane == 0) smax[wave] = m;
+  __syncthreads();
+  float vmax = smax[0];
+#pragma unroll
+  for (int w = 1; w < 16; ++w) vmax = fmaxf(vmax, smax[w]);
+  if (!(vmax > 0.f) || !(vmax <= 3.40282347e38f)) {
+    if (i0 < d_in) C[i0] = 0;
+    if (i0 + 1 < d_in) C[i0 + 1] = 0;
+    return;
+  }
+  int e;
+  (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
+  const uint32_t w0 = i0 < d_in ? (uint32_t)ldexpf(v0, 32 - e) : 0u;
+  const uint32_t w1 = i0 + 1 < d_in ? (uint32_t)ldexpf(v1, 32 - e) : 0u;
+  const uint64_t s = (uint64_t)w0 + w1;
+  uint64_t incl = s;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint64_t y = __shfl_up(incl, off, 64);
+    if (lane >= off) incl += y;
+  }
+  if (lane == 63) ssum[wave] = incl;
+  __syncthreads();
+  uint64_t base = 0;
+  for (int w = 0; w < wave; ++w) base += ssum[w];
+  const uint64_t run = base + incl - s;
+  if (i0 < d_in) C[i0] = run + w0;
+  if (i0 + 1 < d_in) C[i0 + 1] = run + w0 + w1;
+}
+
 }  // namespace
 
 hipError_t launch_prepare(const void* W, int bf16, int d_in, int d_out, void* prepared, hipStream_t s) {
   float* rownorm = static_cast<float*>(prepared);
   void* Wt = static_cast<char*>(prepared) + prepared_wt_offset(d_in);
+  uint64_t* table = reinterpret_cast<uint64_t*>(static_cast<char*>(prepared) + prepared_table_offset(bf16, d_in, d_out));
   const int nks = (int)(prepared_din_pad(d_in) / (bf16 ? 32 : 16));
   const int64_t nchunks = prepared_dout_pad(d_out) / 16 * nks * 64;
   const dim3 g1((d_in + 63) / 64);
@@ -73,6 +121,8 @@ hipError_t launch_prepare(const void* W, int bf16, int d_in, int d_out, void* pr
     hipLaunchKernelGGL(k_rownorm<0>, g1, dim3(64), 0, s, W, d_in, d_out, rownorm);
     hipLaunchKernelGGL(k_fragment_wt<0>, g2, dim3(256), 0, s, W, d_in, d_out, nks, nchunks, Wt);
   }
+  if (d_in > 2048) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_weight_table, dim3(1), dim3(1024), 0, s, rownorm, d_in, table);
   return hipGetLastError();
 }
 

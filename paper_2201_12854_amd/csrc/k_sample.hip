@@ -6,10 +6,12 @@
 //      [1, d_in]; padded keys get 0. r_j = d_in marks a saturated token, encoded exactly
 //      by the gather kernel's MFMA path (cost of d_in samples, no error).
 //   2. sampling weights of Eq. 4 for the product x_j W_v: v_i = |x_ji| * rho_i in one
-//      float32 multiply (or, in the paper's input-independent mode of Eq. 6,
-//      v_i = rho_i * rho_i), quantised to 32-bit fixed point aligned to the largest v_i,
+//      float32 multiply, quantised to 32-bit fixed point aligned to the largest v_i,
 //      w_i = floor(v_i 2^(32-e)); inclusive prefix sums C (uint64) by a wavefront scan
 //      (each lane owns a contiguous run of rows), stored in the wave's part of the LDS.
+//      In the paper's input-independent mode (Eq. 6, p_i ~ rho_i^2) the prefix sums are
+//      the same for every token: they come precomputed with the prepared weights and are
+//      copied into LDS once per block.
 //   3. r_j i.i.d. draws with replacement (Eq. 2): Philox4x32-10 with counter (k, j, b, 0),
 //      u = o0 | o1 << 32, t = floor(u T / 2^64), s_k = min{i : C_i > t} by binary search
 //      in LDS; draws are counted per row with LDS integer atomics (exact, order-free).
@@ -102,22 +104,42 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const uint64_t* C
 }
 
 // PER: upper bound of the rows one lane owns, ceil(d_in / 64) <= PER.
-template <int BF, int PER>
+// LDS of a block. Per-token weights (Eq. 4): per wave C uint64 [d_in] then cnt uint32
+// [d_in]. Shared table (Eq. 6): C uint64 [d_in] once per block, then cnt per wave.
+__host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
+__host__ __device__ inline int sample_lds_bytes(int d_in, bool table) {
+  return table ? round16(8 * d_in) + kWaves * round16(4 * d_in) : kWaves * sample_lds_per_wave(d_in);
+}
+
+// PER: upper bound of the rows one lane owns, ceil(d_in / 64) <= PER. TABLE: the
+// input-independent probability of Eq. 6, whose prefix sums come from the prepared
+// weights (copied into LDS once per block and shared by its tokens); otherwise the
+// per-token probability of Eq. 4, quantised and scanned per token.
+template <int BF, int PER, bool TABLE>
 __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   using T = typename Elem<BF>::T;
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t ntok = (int64_t)p.B * p.n;
   const int64_t tok = (int64_t)blockIdx.x * kWaves + wave;
-  if (tok >= ntok) return;  // whole waves only; no block barrier follows
   const int d_in = p.d_in, n = p.n;
+  uint64_t* C;
+  uint32_t* cnt;
+  if constexpr (TABLE) {
+    C = reinterpret_cast<uint64_t*>(smem);
+    cnt = reinterpret_cast<uint32_t*>(smem + round16(8 * d_in) + wave * round16(4 * d_in));
+    for (int i = threadIdx.x; i < d_in; i += 64 * kWaves) C[i] = p.wtable[i];
+    __syncthreads();  // the only block barrier; waves without a token return after it
+  } else {
+    unsigned char* wl = smem + wave * sample_lds_per_wave(d_in);
+    C = reinterpret_cast<uint64_t*>(wl);
+    cnt = reinterpret_cast<uint32_t*>(wl + 8 * d_in);
+  }
+  if (tok >= ntok) return;  // whole waves only; no block barrier follows
   const int b = (int)(tok / n), j = (int)(tok - (int64_t)b * n);
-  unsigned char* wl = smem + wave * sample_lds_per_wave(d_in);
-  uint64_t* C = reinterpret_cast<uint64_t*>(wl);
-  uint32_t* cnt = reinterpret_cast<uint32_t*>(wl + 8 * d_in);
 
-  // ---- independent loads first: length, column-max partials, x and rho of this lane's
-  // contiguous run of rows [i0, i0 + cnt_rows)
+  // ---- independent loads first: length, column-max partials, x (and rho under Eq. 4) of
+  // this lane's contiguous run of rows [i0, i0 + nrows)
   int len = p.seq_lens ? p.seq_lens[b] : n;
   len = min(max(len, 1), n);
   const int rin = p.r_in ? p.r_in[tok] : 0;
@@ -131,23 +153,25 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   // full: d_in = 64 PER, every lane owns exactly PER rows and its runs of x, rho, C and
   // cnt are 16-byte aligned (i0 = PER lane), so they move as 16-byte vectors
   const bool full = d_in == kWave * PER;
-  const bool ws = p.weight_sampling != 0;
   float xv[PER], vv[PER];
   float lmax = 0.f;
   if (full) {
 #pragma unroll
     for (int k = 0; k < PER; k += 4) {
       const float4 xs = load4_f32(xrow + i0 + k);
-      const float4 rs = *reinterpret_cast<const float4*>(p.rownorm + i0 + k);
       xv[k] = xs.x; xv[k + 1] = xs.y; xv[k + 2] = xs.z; xv[k + 3] = xs.w;
-      // Eq. 4: |x_i| rho_i; Eq. 6: rho_i^2 (the same for every token)
-      vv[k] = __fmul_rn(ws ? rs.x : fabsf(xs.x), rs.x);
-      vv[k + 1] = __fmul_rn(ws ? rs.y : fabsf(xs.y), rs.y);
-      vv[k + 2] = __fmul_rn(ws ? rs.z : fabsf(xs.z), rs.z);
-      vv[k + 3] = __fmul_rn(ws ? rs.w : fabsf(xs.w), rs.w);
+      if constexpr (!TABLE) {
+        const float4 rs = *reinterpret_cast<const float4*>(p.rownorm + i0 + k);
+        vv[k] = __fmul_rn(fabsf(xs.x), rs.x);
+        vv[k + 1] = __fmul_rn(fabsf(xs.y), rs.y);
+        vv[k + 2] = __fmul_rn(fabsf(xs.z), rs.z);
+        vv[k + 3] = __fmul_rn(fabsf(xs.w), rs.w);
+      }
     }
+    if constexpr (!TABLE) {
 #pragma unroll
-    for (int k = 0; k < PER; ++k) lmax = fmaxf(lmax, vv[k]);
+      for (int k = 0; k < PER; ++k) lmax = fmaxf(lmax, vv[k]);
+    }
   } else {
 #pragma unroll
     for (int k = 0; k < PER; ++k) {
@@ -155,14 +179,14 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
       vv[k] = 0.f;
       if (k < nrows) {
         xv[k] = load_f32(xrow, i0 + k);
-        const float rk = p.rownorm[i0 + k];
-        vv[k] = __fmul_rn(ws ? rk : fabsf(xv[k]), rk);
-        lmax = fmaxf(lmax, vv[k]);
+        if constexpr (!TABLE) {
+          vv[k] = __fmul_rn(fabsf(xv[k]), p.rownorm[i0 + k]);
+          lmax = fmaxf(lmax, vv[k]);
+        }
       }
     }
   }
   m = wave_max(m);
-  const float vmax = wave_max(lmax);
 
   // ---- 1. sample count (Eq. 9)
   int r;
@@ -184,45 +208,64 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
     if (lane == 0) p.ucount[tok] = 0;
     return;
   }
-  // padded key; no weights (x_j = 0 under Eq. 4, W_v = 0 under Eq. 6); non-finite weights
-  if (r == 0 || !(vmax > 0.f) || !(vmax <= 3.40282347e38f)) {
+
+  // ---- 2. the distribution: per-token fixed-point weights and their prefix sums (Eq. 4),
+  // or the shared table (Eq. 6). No distribution (x_j = 0 under Eq. 4, W_v = 0 under
+  // Eq. 6, non-finite weights) or a padded key: H~[j] = 0.
+  uint32_t wv[PER];
+  uint64_t Tw;
+  bool none;
+  if constexpr (TABLE) {
+    Tw = C[d_in - 1];
+    none = Tw == 0;
+  } else {
+    const float vmax = wave_max(lmax);
+    none = !(vmax > 0.f) || !(vmax <= 3.40282347e38f);
+    Tw = 0;
+    if (!none) {
+      int e;
+      (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
+      const int shift = 32 - e;
+      uint64_t lsum = 0;
+#pragma unroll
+      for (int k = 0; k < PER; ++k) {
+        wv[k] = (k < nrows) ? (uint32_t)ldexpf(vv[k], shift) : 0u;
+        lsum += wv[k];
+      }
+      const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum, lane);
+      Tw = __shfl(incl, kWave - 1, kWave);  // = C[d_in - 1]
+      uint64_t run = incl - lsum;
+      if (full) {
+#pragma unroll
+        for (int k = 0; k < PER; k += 2) {
+          const uint64_t c0 = run + wv[k], c1 = c0 + wv[k + 1];
+          run = c1;
+          *reinterpret_cast<uint4*>(C + i0 + k) =
+              make_uint4((uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32));
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+          if (k < nrows) {
+            run += wv[k];
+            C[i0 + k] = run;
+          }
+        }
+      }
+    }
+  }
+  if (r == 0 || none) {
     if (lane == 0) p.ucount[tok] = 0;
     for (int c = 4 * lane; c < p.d_out; c += 4 * kWave) write_zero4<BF>(p, tok * p.d_out + c);
     return;
   }
-
-  // ---- 2. fixed-point weights and their prefix sums
-  int e;
-  (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
-  const int shift = 32 - e;
-  uint32_t wv[PER];
-  uint64_t lsum = 0;
-#pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    wv[k] = (k < nrows) ? (uint32_t)ldexpf(vv[k], shift) : 0u;
-    lsum += wv[k];
-  }
-  const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum, lane);
-  const uint64_t Tw = __shfl(incl, kWave - 1, kWave);  // = C[d_in - 1]
-  uint64_t run = incl - lsum;
   if (full) {
-#pragma unroll
-    for (int k = 0; k < PER; k += 2) {
-      const uint64_t c0 = run + wv[k], c1 = c0 + wv[k + 1];
-      run = c1;
-      *reinterpret_cast<uint4*>(C + i0 + k) = make_uint4((uint32_t)c0, (uint32_t)(c0 >> 32), (uint32_t)c1, (uint32_t)(c1 >> 32));
-    }
 #pragma unroll
     for (int k = 0; k < PER; k += 4) *reinterpret_cast<uint4*>(cnt + i0 + k) = make_uint4(0u, 0u, 0u, 0u);
   } else {
 #pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      if (k < nrows) {
-        run += wv[k];
-        C[i0 + k] = run;
-        cnt[i0 + k] = 0u;
-      }
-    }
+    for (int k = 0; k < PER; ++k)
+      if (k < nrows) cnt[i0 + k] = 0u;
   }
   wave_lds_sync();
 
@@ -251,6 +294,13 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
 #pragma unroll
     for (int k = 0; k < PER; ++k) cv[k] = k < nrows ? cnt[i0 + k] : 0u;
   }
+  if constexpr (TABLE) {  // the weights are differences of the shared prefix sums
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+      const int i = i0 + k;
+      wv[k] = (cv[k] != 0u) ? (uint32_t)(C[i] - (i > 0 ? C[i - 1] : 0ull)) : 1u;
+    }
+  }
   int nloc = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) nloc += cv[k] != 0u;
@@ -261,41 +311,44 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
-    {
-      const uint32_t c = cv[k];
-      if (c) {
-        const float coef = (float)(((double)c * (double)xv[k] * (double)Tw) / ((double)r * (double)wv[k]));
-        lst[pos] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
-        ++pos;
-      }
+    const uint32_t c = cv[k];
+    if (c) {
+      const float coef = (float)(((double)c * (double)xv[k] * (double)Tw) / ((double)r * (double)wv[k]));
+      lst[pos] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
+      ++pos;
     }
   }
   if (lane == 0) p.ucount[tok] = U;
 }
 
-template <int BF, int PER>
+template <int BF, int PER, bool TABLE>
 hipError_t launch_per(const FwdParams& p, hipStream_t s) {
   const int64_t ntok = (int64_t)p.B * p.n;
   const dim3 grid((unsigned)((ntok + kWaves - 1) / kWaves));
-  const size_t lds = (size_t)kWaves * sample_lds_per_wave(p.d_in);
+  const size_t lds = (size_t)sample_lds_bytes(p.d_in, TABLE);
   if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_sample<BF, PER>,
+    const hipError_t e = hipFuncSetAttribute((const void*)k_sample<BF, PER, TABLE>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((k_sample<BF, PER>), grid, dim3(64 * kWaves), lds, s, p);
+  hipLaunchKernelGGL((k_sample<BF, PER, TABLE>), grid, dim3(64 * kWaves), lds, s, p);
   return hipGetLastError();
+}
+
+template <int BF, int PER>
+hipError_t launch_mode(const FwdParams& p, hipStream_t s) {
+  return p.weight_sampling ? launch_per<BF, PER, true>(p, s) : launch_per<BF, PER, false>(p, s);
 }
 
 template <int BF>
 hipError_t launch_bf(const FwdParams& p, hipStream_t s) {
   const int per = (p.d_in + kWave - 1) / kWave;
-  if (per <= 4) return launch_per<BF, 4>(p, s);
-  if (per <= 8) return launch_per<BF, 8>(p, s);
-  if (per <= 12) return launch_per<BF, 12>(p, s);
-  if (per <= 16) return launch_per<BF, 16>(p, s);
-  if (per <= 24) return launch_per<BF, 24>(p, s);
-  if (per <= 32) return launch_per<BF, 32>(p, s);
+  if (per <= 4) return launch_mode<BF, 4>(p, s);
+  if (per <= 8) return launch_mode<BF, 8>(p, s);
+  if (per <= 12) return launch_mode<BF, 12>(p, s);
+  if (per <= 16) return launch_mode<BF, 16>(p, s);
+  if (per <= 24) return launch_mode<BF, 24>(p, s);
+  if (per <= 32) return launch_mode<BF, 32>(p, s);
   return hipErrorInvalidValue;
 }
 

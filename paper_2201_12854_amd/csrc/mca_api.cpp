@@ -233,6 +233,8 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.W = W_v;
   p.rownorm = static_cast<const float*>(prepared);
   p.Wt = static_cast<const char*>(prepared) + mca::prepared_wt_offset(desc->d_in);
+  p.wtable = reinterpret_cast<const uint64_t*>(static_cast<const char*>(prepared) +
+                                               mca::prepared_table_offset(p.bf16, desc->d_in, p.d_out));
   p.Y = Y;
   p.r = r;
   char* ws = static_cast<char*>(workspace);

@@ -20,8 +20,15 @@ constexpr int kQueryTile = 64;  // queries per attention block
 inline int64_t prepared_din_pad(int64_t d_in) { return (d_in + 127) / 128 * 128; }
 inline int64_t prepared_dout_pad(int64_t d_out) { return (d_out + 15) / 16 * 16; }
 inline size_t prepared_wt_offset(int64_t d_in) { return (size_t)((4 * d_in + 255) / 256 * 256); }
+// Then, at prepared_table_offset, the input-independent sampling table of Eq. 6: uint64
+// [d_in] inclusive prefix sums of the fixed-point weights of rho_i^2 (all zero when no
+// distribution can be formed).
+inline size_t prepared_table_offset(int bf16, int64_t d_in, int64_t d_out) {
+  const size_t end = prepared_wt_offset(d_in) + (size_t)prepared_dout_pad(d_out) * (size_t)prepared_din_pad(d_in) * (bf16 ? 2 : 4);
+  return (end + 255) / 256 * 256;
+}
 inline size_t prepared_bytes(int bf16, int64_t d_in, int64_t d_out) {
-  return prepared_wt_offset(d_in) + (size_t)prepared_dout_pad(d_out) * (size_t)prepared_din_pad(d_in) * (bf16 ? 2 : 4);
+  return prepared_table_offset(bf16, d_in, d_out) + 8 * (size_t)d_in;
 }
 
 // Everything one forward pass needs, with the workspace already carved up.
@@ -41,7 +48,8 @@ struct FwdParams {
   const void* X;
   const void* W;         // [d_in, d_out]
   const float* rownorm;  // [d_in]
-  const void* Wt;        // [d_out, din_pad]
+  const void* Wt;        // W_v^T in MFMA fragment order
+  const uint64_t* wtable;  // [d_in] Eq. 6 prefix sums
   float* Y;
   int32_t* r;
   // workspace

@@ -78,8 +78,10 @@ def test_workspace_size_formula():
 def test_prepared_size_formula():
     for dt, esz in ((0, 4), (1, 2)):
         for d_in, d_out in ((768, 768), (45, 256), (1, 64)):
+            # rownorm, W_v^T in fragment order, the Eq. 6 prefix-sum table (uint64 [d_in])
             off = (4 * d_in + 255) // 256 * 256
-            assert mca.prepared_size(dt, d_in, d_out) == off + ((d_out + 15) // 16 * 16) * ((d_in + 127) // 128 * 128) * esz
+            end_wt = off + ((d_out + 15) // 16 * 16) * ((d_in + 127) // 128 * 128) * esz
+            assert mca.prepared_size(dt, d_in, d_out) == (end_wt + 255) // 256 * 256 + 8 * d_in
 
 
 @pytest.mark.parametrize("field,value,status", [

@@ -88,6 +88,12 @@ def test_prepared_weights_bitexact(dev, dtype):
         ref = np.zeros((cpad, pad), np.float32)
         ref[:d_out, :d_in] = W.T
         assert np.array_equal(wt, ref)
+        # prefix sums of the Eq. 6 weights fp32(rho_i^2) in 32-bit fixed point, uint64
+        toff = (off + cpad * pad * esz + 255) // 256 * 256
+        table = prep[toff: toff + 8 * d_in].cpu().numpy().view(np.uint64)
+        q = oracle.weight_fixed_point(oracle.row_norms(W))
+        expect = np.zeros(d_in, np.uint64) if q is None else np.array(q[1], np.uint64)
+        assert np.array_equal(table, expect)
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
