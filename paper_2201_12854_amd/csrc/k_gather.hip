@@ -8,12 +8,15 @@
 //
 // The slice W_v[:, c0 .. c0 + WC) is converted to float32 once and kept in LDS for the
 // whole block (768 x 32 floats = 96 KB: the 160 KB LDS of a gfx950 CU holds it), so the
-// gather reads LDS instead of L2. A row of the slice is WC / 4 lanes x 16 bytes; a wave
-// works on 64 / (WC / 4) sampled tokens at once, one per lane group, so each 16-byte LDS
-// read instruction fetches one sampled row for each of them and no cross-lane reduction
-// is needed. The list entries (LDS byte offset of the row, coefficient) are loaded one
-// round ahead with coalesced 16-byte loads and shared within each lane group through a
-// small LDS staging area.
+// gather reads LDS instead of L2. A row of the slice is LPR = WC / 4 chunks of 16 bytes; a
+// wave works on 64 / LPR sampled tokens at once, one per group of LPR lanes. Every lane
+// takes its own pair of list entries (LDS byte offset of the row, coefficient) per round,
+// loaded two rounds ahead with one coalesced 16-byte load, reads both rows whole and
+// accumulates all WC columns. Each list holds its even rows first and its odd rows second
+// (even and odd rows lie in opposite halves of the LDS banks); half of a group's lanes take
+// the even part, half the odd part, and the chunk each lane reads at a step is permuted by
+// lane and group so that the 16 lanes the LDS serves together never share a bank. A
+// reduce-scatter within the group (DPP) ends the item.
 //
 // Work distribution: the blocks of a slice split the tokens into contiguous ranges. A block
 // reads r and U of its range, puts the saturated tokens on one LDS list and sorts the
@@ -161,34 +164,25 @@ __device__ __forceinline__ int wave_max_int(int v) {
              max(__builtin_amdgcn_readlane(v, 32), __builtin_amdgcn_readlane(v, 48)));
 }
 
-// acc += coef * W_lds[row] (4 columns) for one list entry (LDS byte offset of the row, coef).
-__device__ __forceinline__ void fma_row(float4& acc, const unsigned char* wl, uint2 e) {
-  const float4 w = *reinterpret_cast<const float4*>(wl + e.x);
-  const float c = __uint_as_float(e.y);
-  acc.x = fmaf(c, w.x, acc.x);
-  acc.y = fmaf(c, w.y, acc.y);
-  acc.z = fmaf(c, w.z, acc.z);
-  acc.w = fmaf(c, w.w, acc.w);
-}
-
 constexpr int kChunk = kThreads;  // tokens classified per block pass (one per thread)
 constexpr int kNumKeys = 48;      // sort keys floor(4 log2 U) for 1 <= U < 4096
-constexpr int kUBits = 12;        // order entry: (local token << 12) | U
 
-// floor(4 log2 U) for 1 <= U < 4096: the octave and the next two bits of U.
+// floor(4 log2 U) for 1 <= U < 4096 (U: list length): the octave and the next two bits.
 __device__ __forceinline__ int sort_key(int U) {
   const int e = 31 - __clz(U);
   const int f = e >= 2 ? (U >> (e - 2)) & 3 : (U << (2 - e)) & 3;
   return 4 * e + f;
 }
 
-constexpr int kWavesPerBlock = kThreads / 64;
+constexpr int kCtrOff = 64;        // counters: [0] saturated, [1 + key] key counts, [60] work
+                                   // queue, [kCtrOff + key] key offsets, [kCtrOff + kNumKeys] sampled
+constexpr int kNumCtr = 128;
 
 __host__ __device__ inline size_t gather_lds_bytes(int d_in, int wc) {
-  return (size_t)(d_in + 1) * wc * 4         // W_v slice, float32, and a zero row
-         + (size_t)kWavesPerBlock * 1024      // list staging, 1 KB per wave
+  return 128                                 // alignment of the slice
+         + (size_t)(d_in + 2) * wc * 4       // W_v slice, float32, and two zero rows
          + (size_t)kChunk * 4 * 2            // sampled order, saturated list
-         + 64 * 4;                           // counters
+         + kNumCtr * 4;                      // counters
 }
 
 // Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
@@ -199,86 +193,131 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
 }
 
-// This lane's two list entries q, q + 1 (q even, 16 bytes) of a list of length U; entries
-// past the end become the zero row with coefficient 0. The load address is clamped into
-// the token's list slot (stride entries, even) and the selection done with masks, so the
-// load needs no branch.
-__device__ __forceinline__ uint4 entry_pair(const uint2* L, int q, int U, int stride, uint32_t zero_row) {
-  const uint4 v = *reinterpret_cast<const uint4*>(L + min(q, stride - 2));
-  const uint32_t k0 = q < U ? 0xffffffffu : 0u, k1 = q + 1 < U ? 0xffffffffu : 0u;
-  return make_uint4((v.x & k0) | (zero_row & ~k0), v.y & k0, (v.z & k1) | (zero_row & ~k1), v.w & k1);
+// LDS reads by 32-bit LDS address (offset into the workgroup's LDS).
+typedef __attribute__((address_space(3))) const float4 lds_float4;
+__device__ __forceinline__ float4 lds_read4(uint32_t addr) {
+#if defined(__HIP_DEVICE_COMPILE__)  // the host pass never runs device code
+  return *reinterpret_cast<lds_float4*>((uintptr_t)addr);
+#else
+  return float4{};
+#endif
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char*)p;  // address-space cast
 }
 
-// G = 64 / (RB / 16) sampled tokens s0 .. s0 + G - 1 of the sorted order, one per lane group:
-// group g accumulates its token's rows for the 4 columns 4 cl .. 4 cl + 3 of every lane.
-// A round covers RB / 8 list entries of every group: the wave loads them with one
-// coalesced 16-byte load per lane (lane cl of group g: entries 2 cl, 2 cl + 1 of its
-// token), one round ahead, writes them to its LDS staging area and every group reads its
-// own entries back as broadcast reads. A wave's LDS instructions execute in issue order,
-// so one staging buffer per wave suffices.
+// Entries 2 h + q, + 1 (q multiple of 2) of one part of a token's list: part 0 (even rows)
+// at list index 0, part 1 (odd rows) at nepad; each part has even length. The load address
+// is clamped into the token's list slot; the caller masks entries past the part's end.
+__device__ __forceinline__ uint4 entry_pair_raw(const uint2* L, int part_base, int q, int stride) {
+  return *reinterpret_cast<const uint4*>(L + min(part_base + q, stride - 2));
+}
+__device__ __forceinline__ uint4 entry_mask(uint4 v, bool in_part, uint32_t zero_row) {
+  const uint32_t k = in_part ? 0xffffffffu : 0u;
+  return make_uint4((v.x & k) | (zero_row & ~k), v.y & k, (v.z & k) | (zero_row & ~k), v.w & k);
+}
+
+// acc[c] += coef * chunk (c ^ v) of a slice row: a_cl = LDS address of the row + 16 v
+// (rows are RB-aligned, so bits 4.. of a_cl hold v). LPR 16-byte reads, then the FMAs.
+template <int LPR>
+__device__ __forceinline__ void row_fma(float4* acc, uint32_t a_cl, float coef) {
+  float4 w[LPR];
+#pragma unroll
+  for (int c = 0; c < LPR; ++c) w[c] = lds_read4(a_cl ^ (uint32_t)(c << 4));
+#pragma unroll
+  for (int c = 0; c < LPR; ++c) {
+    acc[c].x = fmaf(coef, w[c].x, acc[c].x);
+    acc[c].y = fmaf(coef, w[c].y, acc[c].y);
+    acc[c].z = fmaf(coef, w[c].z, acc[c].z);
+    acc[c].w = fmaf(coef, w[c].w, acc[c].w);
+  }
+}
+
+// Order entry of a sampled token: (local token << 22) | (list length << 10) | (even part / 2).
+constexpr int kTokShift = 22, kLenShift = 10;
+
+// G = 64 / LPR sampled tokens s0 .. s0 + G - 1 of the sorted order, one per group of LPR
+// lanes. Lanes cl < LPR / 2 of a group take the even part of its token's list, the others
+// the odd part; round t gives lane cl the entries 2 h + LPR t, + 1 of its part (h = cl mod
+// LPR / 2). The lane reads chunk c ^ v of both rows at step c (v = cl, or cl ^ LPR / 2 in
+// odd groups) and adds coef * chunk into acc[c]. The two groups the LDS serves together
+// then read 2 LPR distinct (row parity, chunk) pairs, i.e. distinct banks. A reduce-scatter
+// butterfly over the group (partners v ^ 4, v ^ 2, v ^ 1) leaves chunk v in lane cl: the
+// same addition tree over the lanes' partial sums wherever the token sits, so a token's
+// H~ does not depend on the other tokens of its item.
 template <int BF, int RB>
-__device__ void sampled_item(const FwdParams& p, const float* Ws, uint4* stage, const uint32_t* order, int s0,
-                             int nsampled, int64_t t0, int c0, int lane) {
-  constexpr int LPR = RB / 16;    // lanes per row and per group
-  constexpr int NE = 2 * LPR;     // entries per group per round
+__device__ void sampled_item(const FwdParams& p, const float* Ws, const uint32_t* order, int s0, int nsampled,
+                             int64_t t0, int c0, int lane) {
+  constexpr int LPR = RB / 16;  // lanes per group, 16-byte chunks per slice row
+  constexpr int HALF = LPR / 2;
+  static_assert(LPR == 4 || LPR == 8, "slice rows of 64 or 128 bytes");
   const int g = lane / LPR, cl = lane % LPR;
   const bool valid = s0 + g < nsampled;  // groups past the end repeat the item's first token
   const uint32_t e = order[valid ? s0 + g : s0];
-  const int64_t tk = t0 + (e >> kUBits);
-  const int U = (int)(e & ((1u << kUBits) - 1u));  // >= 1
+  const int64_t tk = t0 + (e >> kTokShift);
+  const int len = (int)((e >> kLenShift) & 0xfffu);
+  const int nepad = (int)(e & 0x3ffu) * 2;
   const int stride = list_stride(p.d_in);
   const uint2* L = p.list + tk * stride;
-  const int maxU = wave_max_int(U);
-  const uint32_t zero_row = (uint32_t)p.d_in * RB;
-  const unsigned char* wl = reinterpret_cast<const unsigned char*>(Ws) + cl * 16;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  uint4 nxt = entry_pair(L, 2 * cl, U, stride, zero_row);
-  for (int q0 = 0; q0 < maxU; q0 += NE) {
-    uint4* st = stage;
-    wave_lds_sync();  // the previous round's reads stay ahead of this write
-    st[lane] = nxt;
-    wave_lds_sync();
-    nxt = entry_pair(L, q0 + NE + 2 * cl, U, stride, zero_row);  // next round (unused after the last)
-    const uint4* mine = st + g * LPR;                      // this group's NE entries
-    // all entry reads, then all row reads (distinct registers, so they are in flight
-    // together), then the FMAs
-    uint4 two[LPR];
+  const bool odd_part = cl >= HALF;
+  const int part_base = odd_part ? nepad : 0;
+  const int part_len = odd_part ? len - nepad : nepad;
+  const int maxpart = wave_max_int(max(nepad, len - nepad));
+  const uint32_t zero_row = (uint32_t)(odd_part ? zero_row_odd(p.d_in) : zero_row_even(p.d_in)) * RB;
+  const int v = cl ^ ((g & 1) ? HALF : 0);
+  const int h2 = 2 * (cl % HALF);
+  const uint32_t lane_base = lds_addr(Ws) + (uint32_t)v * 16;  // the slice is 128-byte aligned
+  float4 acc[LPR];
 #pragma unroll
-    for (int k = 0; k < LPR; ++k) two[k] = mine[k];
-    float4 w[2 * LPR];
+  for (int c = 0; c < LPR; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
+  // entries two rounds ahead; masked when consumed, so the loads stay in flight
+  uint4 n1 = entry_pair_raw(L, part_base, h2, stride);
+  uint4 n2 = entry_pair_raw(L, part_base, LPR + h2, stride);
+  for (int q0 = 0; q0 < maxpart; q0 += LPR) {
+    const uint4 en = entry_mask(n1, q0 + h2 < part_len, zero_row);
+    n1 = n2;
+    n2 = entry_pair_raw(L, part_base, q0 + 2 * LPR + h2, stride);
+    __builtin_amdgcn_sched_barrier(0);  // keep the load two rounds ahead of its use
+    row_fma<LPR>(acc, lane_base + en.x, __uint_as_float(en.y));
+    row_fma<LPR>(acc, lane_base + en.z, __uint_as_float(en.w));
+  }
+  // reduce-scatter: acc[c] holds chunk c ^ v; the partner v ^ m holds it in register c ^ m
+#define MCA_ADDX(a, CTRL, b) make_float4(a.x + dpp_f32<CTRL>(b.x), a.y + dpp_f32<CTRL>(b.y), \
+                                       a.z + dpp_f32<CTRL>(b.z), a.w + dpp_f32<CTRL>(b.w))
+  if constexpr (LPR == 8) {
+    // xor 4 within 8 lanes = half-row mirror (xor 7) after quad permutation xor 3
 #pragma unroll
-    for (int k = 0; k < LPR; ++k) {
-      w[2 * k] = *reinterpret_cast<const float4*>(wl + two[k].x);
-      w[2 * k + 1] = *reinterpret_cast<const float4*>(wl + two[k].z);
-    }
-#pragma unroll
-    for (int k = 0; k < 2 * LPR; ++k) {
-      const float c = __uint_as_float((k & 1) ? two[k >> 1].w : two[k >> 1].y);
-      acc.x = fmaf(c, w[k].x, acc.x);
-      acc.y = fmaf(c, w[k].y, acc.y);
-      acc.z = fmaf(c, w[k].z, acc.z);
-      acc.w = fmaf(c, w[k].w, acc.w);
+    for (int c = 0; c < 4; ++c) {
+      const float4 b = acc[c + 4];
+      const float4 b3 = make_float4(dpp_f32<0x1B>(b.x), dpp_f32<0x1B>(b.y), dpp_f32<0x1B>(b.z), dpp_f32<0x1B>(b.w));
+      acc[c] = MCA_ADDX(acc[c], 0x141, b3);
     }
   }
-  if (valid) store_h4<BF>(p, tk * p.d_out + c0 + 4 * cl, acc);
+  acc[0] = MCA_ADDX(acc[0], 0x4E, acc[2]);  // xor 2
+  acc[1] = MCA_ADDX(acc[1], 0x4E, acc[3]);
+  acc[0] = MCA_ADDX(acc[0], 0xB1, acc[1]);  // xor 1
+#undef MCA_ADDX
+  if (valid) store_h4<BF>(p, tk * p.d_out + c0 + 4 * v, acc[0]);
 }
 
 template <int BF, int WC, bool VEC>
 __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   constexpr int RB = WC * 4;   // bytes per slice row in LDS
   constexpr int G = 64 / (RB / 16);  // sampled tokens per work item
-  extern __shared__ __align__(16) unsigned char smem[];
+  extern __shared__ __align__(128) unsigned char smem_raw[];
+  // the slice starts 128-byte aligned (row chunks are addressed by XOR of the chunk index)
+  unsigned char* smem = smem_raw + ((128u - (lds_addr(smem_raw) & 127u)) & 127u);
   const int d_in = p.d_in, d_out = p.d_out;
   const int nslices = d_out / WC;
   const int slice = blockIdx.x % nslices, bis = blockIdx.x / nslices;
   const int c0 = slice * WC;
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t ntok = (int64_t)p.B * p.n;
-  float* Ws = reinterpret_cast<float*>(smem);  // [d_in + 1][WC], the last row zero
-  uint4* stage = reinterpret_cast<uint4*>(smem + (size_t)(d_in + 1) * WC * 4) + (tid >> 6) * 64;  // 64 per wave
-  uint32_t* order = reinterpret_cast<uint32_t*>(smem + (size_t)(d_in + 1) * WC * 4 + kWavesPerBlock * 1024);
+  float* Ws = reinterpret_cast<float*>(smem);  // [d_in + 2][WC], the last two rows zero
+  uint32_t* order = reinterpret_cast<uint32_t*>(smem + (size_t)(d_in + 2) * WC * 4);  // [kChunk]
   int* satl = reinterpret_cast<int*>(order + kChunk);                                // [kChunk]
-  int* ctr = satl + kChunk;  // [0] saturated, [1 + key] sort-key counts, [60] work queue
+  int* ctr = satl + kChunk;                                                          // [kNumCtr]
+  const int stride = list_stride(d_in);
 
   const int64_t per_block = (ntok + p.gather_bps - 1) / p.gather_bps;
   const int64_t t_begin = (int64_t)bis * per_block, t_end = min(t_begin + per_block, ntok);
@@ -289,9 +328,9 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
     u_first = p.ucount[t_begin + tid];
   }
 
-  // ---- the slice of W_v, as float32, into LDS, then a zero row: 16-byte global loads,
+  // ---- the slice of W_v, as float32, into LDS, then two zero rows: 16-byte global loads,
   // four per thread in flight before the conversions and LDS stores
-  if (tid < WC) Ws[d_in * WC + tid] = 0.f;
+  if (tid < 2 * WC) Ws[d_in * WC + tid] = 0.f;
   {
     using T = typename Elem<BF>::T;
     constexpr int CE = BF ? 8 : 4;  // elements per 16-byte chunk
@@ -328,30 +367,42 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
 
   for (int64_t t0 = t_begin; t0 < t_end; t0 += kChunk) {
     const int m = (int)min((int64_t)kChunk, t_end - t0);
-    if (tid < 64) ctr[tid] = 0;
+    if (tid < kNumCtr) ctr[tid] = 0;
     __syncthreads();  // also: the slice is in LDS, the previous pass is done
     // ---- classify this pass's tokens (one per thread) and sort the sampled ones by key
-    int key = -1, rank = 0, U = 0;
+    int key = -1, rank = 0;
+    uint32_t ent = 0;
     if (tid < m) {
       const int r = t0 == t_begin ? r_first : p.r[t0 + tid];
-      U = min(max(t0 == t_begin ? u_first : p.ucount[t0 + tid], 0), d_in);
+      const int uc = t0 == t_begin ? u_first : p.ucount[t0 + tid];
+      const int len = min(uc & 0xffff, stride);
+      const int nepad = min(min((uc >> 16) & 0xffff, len), 2046) & ~1;
       if (r >= d_in) {
         satl[atomicAdd(ctr, 1)] = tid;
-      } else if (r > 0 && U > 0) {
-        key = sort_key(U);
+      } else if (r > 0 && len > 0) {
+        key = sort_key(len);
         rank = atomicAdd(ctr + 1 + key, 1);
+        ent = ((uint32_t)tid << kTokShift) | ((uint32_t)len << kLenShift) | (uint32_t)(nepad >> 1);
       }
     }
     __syncthreads();
-    if (key >= 0) {
-      int off = 0;  // longer lists first
-      for (int k = kNumKeys - 1; k > key; --k) off += ctr[1 + k];
-      order[off + rank] = ((uint32_t)tid << kUBits) | (uint32_t)U;
+    if (tid < 64) {  // one wave: offset of every key, longest lists first
+      const int k = kNumKeys - 1 - tid;  // lane l holds key kNumKeys - 1 - l
+      const int c = k >= 0 ? ctr[1 + k] : 0;
+      int incl = c;
+#pragma unroll
+      for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(incl, off, 64);
+        if (tid >= off) incl += y;
+      }
+      if (k >= 0) ctr[kCtrOff + k] = incl - c;
+      if (tid == 63) ctr[kCtrOff + kNumKeys] = incl;
     }
     __syncthreads();
+    if (key >= 0) order[ctr[kCtrOff + key] + rank] = ent;
+    __syncthreads();
     const int nsat = ctr[0];
-    int nsampled = 0;
-    for (int k = 0; k < kNumKeys; ++k) nsampled += ctr[1 + k];
+    const int nsampled = ctr[kCtrOff + kNumKeys];
     const int ngroups = (nsat + 15) / 16;
     const int nitems = ngroups + (nsampled + G - 1) / G;
 
@@ -362,7 +413,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
       it = __builtin_amdgcn_readfirstlane(it);
       if (it >= nitems) break;
       if (it < ngroups) saturated_group<BF, WC, VEC>(p, satl, t0, it, nsat, c0, lane);
-      else sampled_item<BF, RB>(p, Ws, stage, order, (it - ngroups) * G, nsampled, t0, c0, lane);
+      else sampled_item<BF, RB>(p, Ws, order, (it - ngroups) * G, nsampled, t0, c0, lane);
     }
     __syncthreads();  // the lists of this pass are rewritten next
   }

@@ -16,12 +16,15 @@
 //      u = o0 | o1 << 32, t = floor(u T / 2^64), s_k = min{i : C_i > t} by binary search
 //      in LDS; draws are counted per row with LDS integer atomics (exact, order-free).
 //   4. duplicates merged: coefficient of row i = count_i x_ji T / (r_j w_i) (float64,
-//      rounded once); the distinct rows, ascending, with their coefficients form the
-//      token's list (rows as byte offsets into the gather kernel's LDS slice), and its
-//      length U goes to ucount (0 for tokens without a list).
-// A wave works on its own token and its own LDS region only: the kernel has no block
-// barriers and no global atomics (on a multi-die GPU, device-scope atomics on a few hot
-// counters serialise). Everything it writes is deterministic.
+//      rounded once); the distinct rows with their coefficients form the token's list
+//      (rows as byte offsets into the gather kernel's LDS slice): even rows first, then
+//      odd rows, each part ascending and padded to an even length with a zero row of its
+//      parity. ucount gets (even part length << 16) | total length, 0 for tokens without
+//      a list.
+// A wave works on its own token and its own LDS region only (under Eq. 6 the block first
+// shares the copied table behind one barrier): no global atomics (on a multi-die GPU,
+// device-scope atomics on a few hot counters serialise). Everything it writes is
+// deterministic.
 #include "mca_device.h"
 #include "mca_kernels.h"
 
@@ -301,12 +304,24 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
       wv[k] = (cv[k] != 0u) ? (uint32_t)(C[i] - (i > 0 ? C[i - 1] : 0ull)) : 1u;
     }
   }
-  int nloc = 0;
+  // even rows first, then odd rows (the gather kernel pairs lane groups of opposite row
+  // parity so that their LDS reads fall in different banks); each part ascending and
+  // padded to an even length with a zero row of its parity
+  int ne = 0, no = 0;
 #pragma unroll
-  for (int k = 0; k < PER; ++k) nloc += cv[k] != 0u;
-  const int incl_u = wave_inclusive_scan<int>(nloc, lane);
-  const int U = __shfl(incl_u, kWave - 1, kWave);
-  int pos = incl_u - nloc;
+  for (int k = 0; k < PER; ++k) {
+    if (cv[k] != 0u) {
+      if ((i0 + k) & 1) ++no;
+      else ++ne;
+    }
+  }
+  const int cnt2 = ne | (no << 16);  // both counts <= d_in < 2^16
+  const int incl2 = wave_inclusive_scan<int>(cnt2, lane);
+  const int tot2 = __builtin_amdgcn_readlane(incl2, kWave - 1);
+  const int NE = tot2 & 0xffff, NO = tot2 >> 16;
+  const int nepad = (NE + 1) & ~1, nopad = (NO + 1) & ~1;
+  int pe = (incl2 - cnt2) & 0xffff;
+  int po = nepad + ((incl2 - cnt2) >> 16);
   uint2* lst = p.list + tok * list_stride(d_in);
   const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
 #pragma unroll
@@ -314,11 +329,15 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
     const uint32_t c = cv[k];
     if (c) {
       const float coef = (float)(((double)c * (double)xv[k] * (double)Tw) / ((double)r * (double)wv[k]));
-      lst[pos] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
-      ++pos;
+      const int at = ((i0 + k) & 1) ? po++ : pe++;
+      lst[at] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
     }
   }
-  if (lane == 0) p.ucount[tok] = U;
+  if (lane == 0) {
+    if (NE & 1) lst[NE] = make_uint2((uint32_t)(zero_row_even(d_in) * rb), 0u);
+    if (NO & 1) lst[nepad + NO] = make_uint2((uint32_t)(zero_row_odd(d_in) * rb), 0u);
+    p.ucount[tok] = (nepad << 16) | (nepad + nopad);
+  }
 }
 
 template <int BF, int PER, bool TABLE>

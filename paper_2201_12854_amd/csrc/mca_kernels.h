@@ -58,8 +58,12 @@ struct FwdParams {
   float* row_inv_sum;  // [B*H*n]
   void* Henc;          // [B*n*d_out] H~ in the input dtype
   uint2* list;         // [B*n][list_stride(d_in)] distinct sampled rows of a token:
-                       // (row * gather_row_bytes(d_in), float32 bits of coef)
-  int32_t* ucount;     // [B*n] number of distinct rows U of a sampled token, else 0
+                       // (row * gather_row_bytes(d_in), float32 bits of coef); the even
+                       // rows first, then the odd rows, each part padded to an even
+                       // length with a zero row of its parity (rows d_in, d_in + 1 of the
+                       // gather's LDS slice are zero)
+  int32_t* ucount;     // [B*n] list layout of a sampled token: (even part length << 16) |
+                       // total length; 0 when the token has no list
   int wc;              // W_v columns per gather slice (32 or 16)
   int gather_bps;      // gather blocks per slice
   // optional outputs
@@ -72,11 +76,15 @@ struct FwdParams {
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s);
 hipError_t launch_sample(const FwdParams& p, hipStream_t s);
 hipError_t launch_gather(const FwdParams& p, hipStream_t s);
-// Columns per gather slice for d_in (the slice, float32, must fit the LDS with the staging area).
+// Columns per gather slice for d_in (the slice, float32, must fit the LDS).
 __host__ __device__ inline int gather_slice_cols(int d_in) { return d_in <= 1024 ? 32 : 16; }
-// Entries reserved per token in the sample list: d_in rounded up to even, so that every
-// list starts 16-byte aligned and entries can be read in pairs.
-__host__ __device__ inline int list_stride(int d_in) { return (d_in + 1) & ~1; }
+// Entries reserved per token in the sample list: at most d_in - 1 distinct rows plus one
+// pad entry per parity part, rounded up to even so that every list starts 16-byte aligned
+// and entries can be read in pairs.
+__host__ __device__ inline int list_stride(int d_in) { return (d_in + 2) & ~1; }
+// The two zero rows of the gather's LDS slice: even and odd row index.
+__host__ __device__ inline int zero_row_even(int d_in) { return d_in + (d_in & 1); }
+__host__ __device__ inline int zero_row_odd(int d_in) { return d_in + 1 - (d_in & 1); }
 // Bytes of one slice row in LDS (float32); list entries hold row * gather_row_bytes.
 __host__ __device__ inline int gather_row_bytes(int d_in) { return 4 * gather_slice_cols(d_in); }
 // Gather blocks per column slice: at most one block per CU over all slices (a block holds
