@@ -36,8 +36,6 @@ template <> struct Elem<1> { using T = uint16_t; };
 
 constexpr int kWaves = 4;  // tokens per block
 
-// LDS of one wave: C uint64 [d_in], then cnt uint32 [d_in].
-__host__ __device__ inline int sample_lds_per_wave(int d_in) { return (12 * d_in + 15) / 16 * 16; }
 
 // Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
 // LDS instructions in issue order, so only compiler reordering has to be prevented.
@@ -64,60 +62,95 @@ __device__ __forceinline__ void write_zero4(const FwdParams& p, int64_t off) {
   if (p.enc_out) *reinterpret_cast<float4*>(p.enc_out + off) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
-// W draws of one lane, k = k0 + 64 u (u < W), searched together so that their LDS reads
-// overlap. The search runs a fixed number of halvings (ceil(log2 d_in)) without branches;
-// once lo == hi it stays put, since C[lo] > t there.
-template <int W>
-__device__ __forceinline__ void draw_batch(const FwdParams& p, const uint64_t* C, uint32_t* cnt, const void* xrow,
-                                           int k0, int r, int j, int b, int64_t tok, uint64_t Tw, int nsteps) {
+// Per-wave results of phase 1, shared with the block for the pooled draws.
+struct TokInfo {
+  int r[kWaves];        // draws of the wave's token (0: no draws)
+  int j[kWaves], b[kWaves];
+  uint32_t pad[kWaves];
+  uint64_t T[kWaves];   // total weight C[d_in - 1]
+};
+constexpr int kHeader = 128;  // bytes of LDS before the per-token regions
+static_assert(sizeof(TokInfo) <= kHeader, "header");
+
+// LDS of a block: the header, then
+//   Eq. 4: per wave C uint64 [d_in] (after the draws: record x float32 [d_in], record w
+//          uint32 [d_in]), then cnt uint32 [d_in] (after the draws: record row | count);
+//   Eq. 6: the shared C uint64 [d_in], then per wave cnt uint32 [d_in] and record x
+//          float32 [d_in].
+__host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
+__host__ __device__ inline int sample_region_bytes(int d_in, bool table) {
+  return table ? 2 * round16(4 * d_in) : round16(8 * d_in) + round16(4 * d_in);
+}
+__host__ __device__ inline int sample_lds_bytes(int d_in, bool table) {
+  return kHeader + (table ? round16(8 * d_in) : 0) + kWaves * sample_region_bytes(d_in, table);
+}
+
+// W draws of one thread of the block's pool: draw d = d0 + 256 u (u < W) of the
+// concatenated draws of the block's tokens (token w owns [P_w, P_w + r_w)). Each is draw
+// k = d - P_w of its token: Philox4x32-10 with counter (k, j, b, 0), t = floor(u T / 2^64)
+// and s = min{i : C_i > t} by a fixed number of halvings (ceil(log2 d_in)) without
+// branches (once lo == hi it stays put, since C[lo] > t there), searched together so that
+// their LDS reads overlap; then the token's count of row s goes up by one.
+template <int W, bool TABLE>
+__device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I, unsigned char* smem, int d0, int P1,
+                                           int P2, int P3, int D, int nsteps) {
+  const int d_in = p.d_in;
   uint64_t t[W];
-  int lo[W], hi[W];
+  int lo[W], hi[W], wt[W], kk[W];
+  const uint64_t* Cw[W];
 #pragma unroll
   for (int u = 0; u < W; ++u) {
-    const int k = k0 + u * kWave;
-    const u32x4 o = philox4x32_10(u32x4{(uint32_t)k, (uint32_t)j, (uint32_t)b, 0u}, p.seed_lo, p.seed_hi);
-    t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), Tw);  // in [0, T)
+    const int d = min(d0 + u * 64 * kWaves, D - 1);  // clamped: only d < D is counted
+    const int w = (d >= P1) + (d >= P2) + (d >= P3);
+    const int base = w == 0 ? 0 : (w == 1 ? P1 : (w == 2 ? P2 : P3));
+    wt[u] = w;
+    kk[u] = d - base;
+    const u32x4 o = philox4x32_10(u32x4{(uint32_t)kk[u], (uint32_t)I.j[w], (uint32_t)I.b[w], 0u}, p.seed_lo,
+                                  p.seed_hi);
+    t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), I.T[w]);  // in [0, T)
+    Cw[u] = reinterpret_cast<const uint64_t*>(
+        smem + kHeader + (TABLE ? 0 : w * sample_region_bytes(d_in, false)));
     lo[u] = 0;
-    hi[u] = p.d_in - 1;  // C[d_in-1] = T > t, so the answer is in range
+    hi[u] = d_in - 1;  // C[d_in-1] = T > t, so the answer is in range
   }
   for (int st = 0; st < nsteps; ++st) {
 #pragma unroll
     for (int u = 0; u < W; ++u) {
       const int mid = (lo[u] + hi[u]) >> 1;
-      const bool right = C[mid] <= t[u];
+      const bool right = Cw[u][mid] <= t[u];
       lo[u] = right ? mid + 1 : lo[u];
       hi[u] = right ? hi[u] : mid;
     }
   }
 #pragma unroll
   for (int u = 0; u < W; ++u) {
-    const int k = k0 + u * kWave;
-    if (k < r) {
+    if (d0 + u * 64 * kWaves < D) {
+      const int w = wt[u];
+      uint32_t* cnt = reinterpret_cast<uint32_t*>(
+          smem + kHeader + (TABLE ? round16(8 * d_in) + w * sample_region_bytes(d_in, true)
+                                  : w * sample_region_bytes(d_in, false) + round16(8 * d_in)));
       atomicAdd(cnt + lo[u], 1u);
-      const int64_t o2 = tok * p.d_in + k;
+      const int64_t tok = (int64_t)I.b[w] * p.n + I.j[w];
+      const int64_t o2 = tok * d_in + kk[u];
       if (p.idx_out) p.idx_out[o2] = lo[u];
       if (p.coef_out) {
-        const uint64_t ws = C[lo[u]] - (lo[u] > 0 ? C[lo[u] - 1] : 0ull);
-        const double xs = p.bf16 ? (double)load_f32(static_cast<const uint16_t*>(xrow), lo[u])
-                                 : (double)load_f32(static_cast<const float*>(xrow), lo[u]);
-        p.coef_out[o2] = (float)((xs * (double)Tw) / ((double)r * (double)ws));
+        const uint64_t ws = Cw[u][lo[u]] - (lo[u] > 0 ? Cw[u][lo[u] - 1] : 0ull);
+        const double xs = p.bf16 ? (double)load_f32(static_cast<const uint16_t*>(p.X) + tok * d_in, lo[u])
+                                 : (double)load_f32(static_cast<const float*>(p.X) + tok * d_in, lo[u]);
+        p.coef_out[o2] = (float)((xs * (double)I.T[w]) / ((double)I.r[w] * (double)ws));
       }
     }
   }
-}
-
-// PER: upper bound of the rows one lane owns, ceil(d_in / 64) <= PER.
-// LDS of a block. Per-token weights (Eq. 4): per wave C uint64 [d_in] then cnt uint32
-// [d_in]. Shared table (Eq. 6): C uint64 [d_in] once per block, then cnt per wave.
-__host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
-__host__ __device__ inline int sample_lds_bytes(int d_in, bool table) {
-  return table ? round16(8 * d_in) + kWaves * round16(4 * d_in) : kWaves * sample_lds_per_wave(d_in);
 }
 
 // PER: upper bound of the rows one lane owns, ceil(d_in / 64) <= PER. TABLE: the
 // input-independent probability of Eq. 6, whose prefix sums come from the prepared
 // weights (copied into LDS once per block and shared by its tokens); otherwise the
 // per-token probability of Eq. 4, quantised and scanned per token.
+// Phase 1: every wave prepares its own token (count, distribution, zeroed counts).
+// Phase 2: the block's draws are pooled over all its threads. Phase 3: every wave merges
+// its token's counts into the list. Two block barriers separate the phases; no wave
+// leaves before them.
 template <int BF, int PER, bool TABLE>
 __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   using T = typename Elem<BF>::T;
@@ -126,33 +159,41 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const int64_t ntok = (int64_t)p.B * p.n;
   const int64_t tok = (int64_t)blockIdx.x * kWaves + wave;
   const int d_in = p.d_in, n = p.n;
-  uint64_t* C;
-  uint32_t* cnt;
+  TokInfo& I = *reinterpret_cast<TokInfo*>(smem);
+  uint64_t* C;      // this token's prefix sums (Eq. 6: the shared table)
+  uint32_t* cnt;    // this token's draw counts, then record row | count
+  float* rec_x;     // record x
+  uint32_t* rec_w;  // record w (Eq. 4 only)
   if constexpr (TABLE) {
-    C = reinterpret_cast<uint64_t*>(smem);
-    cnt = reinterpret_cast<uint32_t*>(smem + round16(8 * d_in) + wave * round16(4 * d_in));
+    C = reinterpret_cast<uint64_t*>(smem + kHeader);
+    unsigned char* wl = smem + kHeader + round16(8 * d_in) + wave * sample_region_bytes(d_in, true);
+    cnt = reinterpret_cast<uint32_t*>(wl);
+    rec_x = reinterpret_cast<float*>(wl + round16(4 * d_in));
+    rec_w = nullptr;
     for (int i = threadIdx.x; i < d_in; i += 64 * kWaves) C[i] = p.wtable[i];
-    __syncthreads();  // the only block barrier; waves without a token return after it
   } else {
-    unsigned char* wl = smem + wave * sample_lds_per_wave(d_in);
+    unsigned char* wl = smem + kHeader + wave * sample_region_bytes(d_in, false);
     C = reinterpret_cast<uint64_t*>(wl);
-    cnt = reinterpret_cast<uint32_t*>(wl + 8 * d_in);
+    cnt = reinterpret_cast<uint32_t*>(wl + round16(8 * d_in));
+    rec_x = reinterpret_cast<float*>(wl);
+    rec_w = reinterpret_cast<uint32_t*>(wl + 4 * d_in);
   }
-  if (tok >= ntok) return;  // whole waves only; no block barrier follows
-  const int b = (int)(tok / n), j = (int)(tok - (int64_t)b * n);
+  const bool live = tok < ntok;
+  const int64_t tk = live ? tok : ntok - 1;  // a wave without a token reads a valid one
+  const int b = (int)(tk / n), j = (int)(tk - (int64_t)b * n);
 
-  // ---- independent loads first: length, column-max partials, x (and rho under Eq. 4) of
-  // this lane's contiguous run of rows [i0, i0 + nrows)
+  // ---- phase 1. independent loads first: length, column-max partials, x (and rho under
+  // Eq. 4) of this lane's contiguous run of rows [i0, i0 + nrows)
   int len = p.seq_lens ? p.seq_lens[b] : n;
   len = min(max(len, 1), n);
-  const int rin = p.r_in ? p.r_in[tok] : 0;
-  const float* part = p.colmax_part + tok * p.nparts;
+  const int rin = p.r_in ? p.r_in[tk] : 0;
+  const float* part = p.colmax_part + tk * p.nparts;
   float m = 0.f;
   for (int t = lane; t < p.nparts; t += kWave) m = fmaxf(m, part[t]);
   const int per = (d_in + kWave - 1) / kWave;
   const int i0 = min(lane * per, d_in);
   const int nrows = min(per, d_in - i0);
-  const T* xrow = static_cast<const T*>(p.X) + tok * d_in;
+  const T* xrow = static_cast<const T*>(p.X) + tk * d_in;
   // full: d_in = 64 PER, every lane owns exactly PER rows and its runs of x, rho, C and
   // cnt are 16-byte aligned (i0 = PER lane), so they move as 16-byte vectors
   const bool full = d_in == kWave * PER;
@@ -190,8 +231,9 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
     }
   }
   m = wave_max(m);
+  if constexpr (TABLE) __syncthreads();  // the shared table is in LDS
 
-  // ---- 1. sample count (Eq. 9)
+  // 1a. sample count (Eq. 9)
   int r;
   if (j >= len) {
     r = 0;
@@ -203,20 +245,16 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
     const double tt = t * t;
     r = (tt >= (double)d_in) ? d_in : max((int)ceil(tt), 1);
   }
-  if (lane == 0) {
+  if (live && lane == 0) {
     p.r[tok] = r;
     if (p.colmax_out) p.colmax_out[tok] = m;
   }
-  if (r >= d_in) {  // saturated: exact encoding on the MFMA path of the gather kernel
-    if (lane == 0) p.ucount[tok] = 0;
-    return;
-  }
-
-  // ---- 2. the distribution: per-token fixed-point weights and their prefix sums (Eq. 4),
-  // or the shared table (Eq. 6). No distribution (x_j = 0 under Eq. 4, W_v = 0 under
-  // Eq. 6, non-finite weights) or a padded key: H~[j] = 0.
+  // 1b. the distribution: per-token fixed-point weights and their prefix sums (Eq. 4), or
+  // the shared table (Eq. 6). No distribution (x_j = 0 under Eq. 4, W_v = 0 under Eq. 6,
+  // non-finite weights) or a padded key: H~[j] = 0. A saturated token (r = d_in) is
+  // encoded exactly by the gather kernel's MFMA path and has no list either.
   uint32_t wv[PER];
-  uint64_t Tw;
+  uint64_t Tw = 0;
   bool none;
   if constexpr (TABLE) {
     Tw = C[d_in - 1];
@@ -224,8 +262,7 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   } else {
     const float vmax = wave_max(lmax);
     none = !(vmax > 0.f) || !(vmax <= 3.40282347e38f);
-    Tw = 0;
-    if (!none) {
+    if (!none && r > 0 && r < d_in) {
       int e;
       (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
       const int shift = 32 - e;
@@ -257,35 +294,52 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
       }
     }
   }
-  if (r == 0 || none) {
+  const bool sampled = live && r > 0 && r < d_in && !none;
+  if (live && !sampled) {
     if (lane == 0) p.ucount[tok] = 0;
-    for (int c = 4 * lane; c < p.d_out; c += 4 * kWave) write_zero4<BF>(p, tok * p.d_out + c);
-    return;
+    if (r < d_in)
+      for (int c = 4 * lane; c < p.d_out; c += 4 * kWave) write_zero4<BF>(p, tok * p.d_out + c);
   }
-  if (full) {
+  if (sampled) {
+    if (full) {
 #pragma unroll
-    for (int k = 0; k < PER; k += 4) *reinterpret_cast<uint4*>(cnt + i0 + k) = make_uint4(0u, 0u, 0u, 0u);
-  } else {
+      for (int k = 0; k < PER; k += 4) *reinterpret_cast<uint4*>(cnt + i0 + k) = make_uint4(0u, 0u, 0u, 0u);
+    } else {
 #pragma unroll
-    for (int k = 0; k < PER; ++k)
-      if (k < nrows) cnt[i0 + k] = 0u;
+      for (int k = 0; k < PER; ++k)
+        if (k < nrows) cnt[i0 + k] = 0u;
+    }
   }
-  wave_lds_sync();
-
-  // ---- 3. draws: ceil(r / 64) per lane, in batches of up to 4 searched together
-  const int nsteps = 32 - __clz(max(d_in - 1, 1));
-  const int nper = (r + kWave - 1) / kWave;
-  for (int u0 = 0; u0 < nper; u0 += 4) {
-    const int k0 = lane + u0 * kWave;
-    const int w = min(4, nper - u0);
-    if (w == 4) draw_batch<4>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
-    else if (w == 3) draw_batch<3>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
-    else if (w == 2) draw_batch<2>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
-    else draw_batch<1>(p, C, cnt, xrow, k0, r, j, b, tok, Tw, nsteps);
+  if (lane == 0) {
+    I.r[wave] = sampled ? r : 0;
+    I.j[wave] = j;
+    I.b[wave] = b;
+    I.T[wave] = Tw;
   }
-  wave_lds_sync();
+  __syncthreads();
 
-  // ---- 4. merge duplicates into the token's list, ascending row order
+  // ---- phase 2. the block's draws, 64 kWaves threads, up to 4 per thread in flight
+  {
+    const int P1 = I.r[0], P2 = P1 + I.r[1], P3 = P2 + I.r[2], D = P3 + I.r[3];
+    const int nsteps = 32 - __clz(max(d_in - 1, 1));
+    const int nper = (D + 64 * kWaves - 1) / (64 * kWaves);
+    for (int u0 = 0; u0 < nper; u0 += 4) {
+      const int d0 = threadIdx.x + u0 * 64 * kWaves;
+      const int w = min(4, nper - u0);
+      if (w == 4) draw_batch<4, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
+      else if (w == 3) draw_batch<3, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
+      else if (w == 2) draw_batch<2, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
+      else draw_batch<1, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
+    }
+  }
+  __syncthreads();
+  if (!sampled) return;
+
+  // ---- phase 3. merge duplicates into the token's list: even rows first, then odd rows
+  // (the gather kernel pairs lane groups of opposite row parity so that their LDS reads
+  // fall in different banks), each part ascending and padded to an even length with a zero
+  // row of its parity. The owners of the rows write compact records (row | count, x, w) in
+  // list order; then each lane turns records lane, lane + 64, ... into list entries.
   uint32_t cv[PER];
   if (full) {
 #pragma unroll
@@ -297,16 +351,6 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
 #pragma unroll
     for (int k = 0; k < PER; ++k) cv[k] = k < nrows ? cnt[i0 + k] : 0u;
   }
-  if constexpr (TABLE) {  // the weights are differences of the shared prefix sums
-#pragma unroll
-    for (int k = 0; k < PER; ++k) {
-      const int i = i0 + k;
-      wv[k] = (cv[k] != 0u) ? (uint32_t)(C[i] - (i > 0 ? C[i - 1] : 0ull)) : 1u;
-    }
-  }
-  // even rows first, then odd rows (the gather kernel pairs lane groups of opposite row
-  // parity so that their LDS reads fall in different banks); each part ascending and
-  // padded to an even length with a zero row of its parity
   int ne = 0, no = 0;
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
@@ -318,20 +362,34 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   const int cnt2 = ne | (no << 16);  // both counts <= d_in < 2^16
   const int incl2 = wave_inclusive_scan<int>(cnt2, lane);
   const int tot2 = __builtin_amdgcn_readlane(incl2, kWave - 1);
-  const int NE = tot2 & 0xffff, NO = tot2 >> 16;
-  const int nepad = (NE + 1) & ~1, nopad = (NO + 1) & ~1;
+  const int NE = tot2 & 0xffff, NO = tot2 >> 16, U = NE + NO;
   int pe = (incl2 - cnt2) & 0xffff;
-  int po = nepad + ((incl2 - cnt2) >> 16);
-  uint2* lst = p.list + tok * list_stride(d_in);
-  const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
+  int po = NE + ((incl2 - cnt2) >> 16);
+  wave_lds_sync();  // every lane has its counts before the records overwrite them
 #pragma unroll
   for (int k = 0; k < PER; ++k) {
     const uint32_t c = cv[k];
     if (c) {
-      const float coef = (float)(((double)c * (double)xv[k] * (double)Tw) / ((double)r * (double)wv[k]));
       const int at = ((i0 + k) & 1) ? po++ : pe++;
-      lst[at] = make_uint2((uint32_t)((i0 + k) * rb), __float_as_uint(coef));
+      cnt[at] = (uint32_t)(i0 + k) | (c << 16);
+      rec_x[at] = xv[k];
+      if constexpr (!TABLE) rec_w[at] = wv[k];
     }
+  }
+  wave_lds_sync();
+  const int nepad = (NE + 1) & ~1, nopad = (NO + 1) & ~1;
+  uint2* lst = p.list + tok * list_stride(d_in);
+  const int rb = gather_row_bytes(d_in);  // the gather kernel reads rows of its LDS slice
+  for (int q = lane; q < U; q += kWave) {
+    const uint32_t e = cnt[q];
+    const int row = (int)(e & 0xffffu);
+    const uint32_t c = e >> 16;
+    const float x = rec_x[q];
+    uint32_t w;
+    if constexpr (TABLE) w = (uint32_t)(C[row] - (row > 0 ? C[row - 1] : 0ull));
+    else w = rec_w[q];
+    const float coef = (float)(((double)c * (double)x * (double)Tw) / ((double)r * (double)w));
+    lst[q < NE ? q : q + (nepad - NE)] = make_uint2((uint32_t)(row * rb), __float_as_uint(coef));
   }
   if (lane == 0) {
     if (NE & 1) lst[NE] = make_uint2((uint32_t)(zero_row_even(d_in) * rb), 0u);
