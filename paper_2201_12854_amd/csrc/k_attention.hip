@@ -158,13 +158,21 @@ __device__ __forceinline__ void score_tile(f32x4_t acc[4], const float* Ks, cons
   }
 }
 
-// Scaled logit a * (q . k) with a = 1/sqrt(64) = 1/8 (exact), kept free of contraction.
-__device__ __forceinline__ float logit(float dot) { return __fmul_rn(dot, 0.125f); }
+// Scaled logit in base-2 units: a (q . k) log2(e) with a = 1/sqrt(64), one float32
+// multiply by the rounded constant log2(e) / 8, so that softmax needs only exp2 (one
+// hardware instruction): exp(a x - m) = exp2(a log2(e) x - m log2(e)). Kept free of
+// contraction.
+constexpr float kLog2eOver8 = (float)(1.4426950408889634 / 8.0);
+__device__ __forceinline__ float logit(float dot) { return __fmul_rn(dot, kLog2eOver8); }
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
 
-// Attention probability from the logit and the row statistics (max, 1/sum).
+// Attention probability from the base-2 logit and the row statistics (max, 1/sum).
 __device__ __forceinline__ float prob(float lg, float row_max, float row_inv) {
-  return __fmul_rn(expf(__fsub_rn(lg, row_max)), row_inv);
+  return __fmul_rn(exp2_fast(__fsub_rn(lg, row_max)), row_inv);
 }
+
+// max(a, b) of floats by compare and select (no NaN canonicalisation of the operands).
+__device__ __forceinline__ float max_sel(float a, float b) { return a > b ? a : b; }
 
 __device__ __forceinline__ int valid_len(const FwdParams& p, int b) {
   int len = p.seq_lens ? p.seq_lens[b] : p.n;
@@ -226,7 +234,16 @@ __device__ __forceinline__ BlockCtx block_ctx(const FwdParams& p) {
 }
 
 // Max over the wave's 16 queries (the 16 lanes of a row, same l / 16) of a probability.
-__device__ __forceinline__ float max_over_queries(float a) { return row16_max(a); }
+// Probabilities are non-negative, so their bit patterns order like the values: an
+// unsigned max with DPP operands (one instruction per step).
+__device__ __forceinline__ float max_over_queries(float a) {
+  uint32_t v = __float_as_uint(a);
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true));   // lane ^ 1
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true));   // lane ^ 2
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, true));  // half-row mirror
+  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, true));  // row mirror
+  return __uint_as_float(v);
+}
 
 // Writes Y rows of the wave's queries: y[cc][i] = Y[query 4 g + i][column 16 cc + l % 16].
 __device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, const f32x4_t y[4]) {
@@ -244,7 +261,7 @@ __device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, c
 // ------------------------------------------------------------------ score pass
 // Resident variant: all ntl <= NT tiles in LDS and all scores in registers.
 template <int BF, int NT>
-__global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_res(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[NT][kTile * S];
@@ -263,25 +280,28 @@ __global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
     if (kt < c.ntl) tile_store<BF>(kr[kt], Ks[kt], c.tid);
   lds_barrier();
 
-  // row statistics: exact max over the valid keys, then the sum of exp
+  // row statistics: exact max over the valid keys, then the sum of exp2. Only the last
+  // tile can hold keys past the valid length (lim < kTile): the masks are applied there.
   f32x4_t acc[NT][4];
   float M = -INFINITY;
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
       score_tile(acc[kt], Ks[kt], qf, c.r16, c.g);
+      const int lim = c.len - kt * kTile;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = kt * kTile + 16 * s + 4 * c.g + i;
-          if (key < c.len) M = fmaxf(M, logit(acc[kt][s][i]));
+          const float lg = logit(acc[kt][s][i]);
+          acc[kt][s][i] = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? lg : -INFINITY;
+          M = max_sel(M, acc[kt][s][i]);
         }
     }
   }
-  M = fmaxf(M, __shfl_xor(M, 16, kWave));
-  M = fmaxf(M, __shfl_xor(M, 32, kWave));
-  // e = exp(logit - M), kept in acc for the column max (masked keys: 0)
+  M = max_sel(M, __shfl_xor(M, 16, kWave));
+  M = max_sel(M, __shfl_xor(M, 32, kWave));
+  // e = exp2(logit - M), kept in acc for the column max (masked keys: exp2(-inf) = 0)
   float L = 0.f;
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
@@ -290,8 +310,7 @@ __global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = kt * kTile + 16 * s + 4 * c.g + i;
-          const float e = key < c.len ? expf(__fsub_rn(logit(acc[kt][s][i]), M)) : 0.f;
+          const float e = exp2_fast(__fsub_rn(acc[kt][s][i], M));
           acc[kt][s][i] = e;
           L += e;
         }
@@ -306,8 +325,10 @@ __global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
     p.row_inv_sum[o] = inv;
   }
 
-  // column max of the valid queries, every tile in its own LDS slot (one barrier)
-  const bool qvalid = c.q < c.len;
+  // column max of the valid queries, every tile in its own LDS slot (one barrier).
+  // probability = e * (1/L), bitwise the value prob() gives in the output pass; queries
+  // past the valid length contribute 0
+  const float inv_q = c.q < c.len ? inv : 0.f;
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
@@ -315,9 +336,7 @@ __global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = kt * kTile + 16 * s + 4 * c.g + i;
-          // probability = e * (1/L), bitwise the value prob() gives in the output pass
-          const float a = max_over_queries((qvalid && key < c.len) ? __fmul_rn(acc[kt][s][i], inv) : 0.f);
+          const float a = max_over_queries(__fmul_rn(acc[kt][s][i], inv_q));
           if (c.r16 == 0) cm[kt][c.wave][16 * s + 4 * c.g + i] = a;
         }
     }
@@ -326,14 +345,15 @@ __global__ __launch_bounds__(kThreads) void k_scores_res(FwdParams p) {
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
   for (int e = c.tid; e < c.ntl * kTile; e += kThreads) {
     const int kt = e / kTile, k = e % kTile;
-    const float v = fmaxf(fmaxf(cm[kt][0][k], cm[kt][1][k]), fmaxf(cm[kt][2][k], cm[kt][3][k]));
+    const float v = __uint_as_float(max(max(__float_as_uint(cm[kt][0][k]), __float_as_uint(cm[kt][1][k])),
+                                        max(__float_as_uint(cm[kt][2][k]), __float_as_uint(cm[kt][3][k]))));
     if (e < c.n) part[(int64_t)e * p.nparts] = v;
   }
 }
 
 // Streaming variant: tiles double buffered, next tile prefetched; two sweeps.
 template <int BF>
-__global__ __launch_bounds__(kThreads) void k_scores_stream(FwdParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[2][kTile * S];
@@ -356,26 +376,26 @@ __global__ __launch_bounds__(kThreads) void k_scores_stream(FwdParams p) {
     f32x4_t acc[4];
     score_tile(acc, buf, qf, c.r16, c.g);
     float mx = -INFINITY;
+    const int lim = c.len - kt * kTile;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kt * kTile + 16 * s + 4 * c.g + i;
-        const float lg = key < c.len ? logit(acc[s][i]) : -INFINITY;
+        const float lg = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? logit(acc[s][i]) : -INFINITY;
         acc[s][i] = lg;
-        mx = fmaxf(mx, lg);
+        mx = max_sel(mx, lg);
       }
-    mx = fmaxf(mx, __shfl_xor(mx, 16, kWave));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
-    const float Mn = fmaxf(M, mx);  // finite: key 0 of tile 0 is valid
+    mx = max_sel(mx, __shfl_xor(mx, 16, kWave));
+    mx = max_sel(mx, __shfl_xor(mx, 32, kWave));
+    const float Mn = max_sel(M, mx);  // finite: key 0 of tile 0 is valid
     float sum = 0.f;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sum += expf(__fsub_rn(acc[s][i], Mn));  // masked: exp(-inf) = 0
+      for (int i = 0; i < 4; ++i) sum += exp2_fast(__fsub_rn(acc[s][i], Mn));  // masked: exp2(-inf) = 0
     sum += __shfl_xor(sum, 16, kWave);
     sum += __shfl_xor(sum, 32, kWave);
-    L = (M == -INFINITY ? 0.f : __fmul_rn(L, expf(__fsub_rn(M, Mn)))) + sum;
+    L = (M == -INFINITY ? 0.f : __fmul_rn(L, exp2_fast(__fsub_rn(M, Mn)))) + sum;
     M = Mn;
   }
   const float inv = 1.0f / L;
@@ -390,7 +410,7 @@ __global__ __launch_bounds__(kThreads) void k_scores_stream(FwdParams p) {
   // store also orders the reads of tile kt - 2's slot before this tile's writes.
   lds_barrier();  // sweep 1 is done with both K buffers
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
-  const bool qvalid = c.q < c.len;
+  const float inv_q = c.q < c.len ? inv : 0.f;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
   for (int kt = 0; kt < c.ntl; ++kt) {
     T* buf = Ks[kt & 1];
@@ -400,17 +420,19 @@ __global__ __launch_bounds__(kThreads) void k_scores_stream(FwdParams p) {
     kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
     f32x4_t acc[4];
     score_tile(acc, buf, qf, c.r16, c.g);
+    const int lim = c.len - kt * kTile;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kt * kTile + 16 * s + 4 * c.g + i;
-        const float a = max_over_queries((qvalid && key < c.len) ? prob(logit(acc[s][i]), M, inv) : 0.f);
+        const bool kvalid = lim >= kTile || 16 * s + 4 * c.g + i < lim;
+        const float a = max_over_queries(kvalid ? prob(logit(acc[s][i]), M, inv_q) : 0.f);
         if (c.r16 == 0) cmk[c.wave][16 * s + 4 * c.g + i] = a;
       }
     lds_barrier();
     if (c.tid < kTile) {
-      const float v = fmaxf(fmaxf(cmk[0][c.tid], cmk[1][c.tid]), fmaxf(cmk[2][c.tid], cmk[3][c.tid]));
+      const float v = __uint_as_float(max(max(__float_as_uint(cmk[0][c.tid]), __float_as_uint(cmk[1][c.tid])),
+                                          max(__float_as_uint(cmk[2][c.tid]), __float_as_uint(cmk[3][c.tid]))));
       const int key = kt * kTile + c.tid;
       if (key < c.n) part[(int64_t)key * p.nparts] = v;
     }
@@ -457,12 +479,13 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
     if (kt < c.ntl) {
       f32x4_t acc[4];
       score_tile(acc, Ks[kt], qf, c.r16, c.g);
+      const int lim = c.len - kt * kTile;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int key = kt * kTile + 16 * s + 4 * c.g + i;
-          acc[s][i] = key < c.len ? prob(logit(acc[s][i]), M, inv) : 0.f;
+          const float pr = prob(logit(acc[s][i]), M, inv);
+          acc[s][i] = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? pr : 0.f;
         }
       pv_tile(y, acc, Vs[kt], c.r16, c.g);
     }
@@ -503,12 +526,13 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
     vr = tile_load<BF>(Vb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
     f32x4_t acc[4];
     score_tile(acc, kb, qf, c.r16, c.g);
+    const int lim = c.len - kt * kTile;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kt * kTile + 16 * s + 4 * c.g + i;
-        acc[s][i] = key < c.len ? prob(logit(acc[s][i]), M, inv) : 0.f;
+        const float pr = prob(logit(acc[s][i]), M, inv);
+        acc[s][i] = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? pr : 0.f;
       }
     pv_tile(y, acc, vb, c.r16, c.g);
   }
