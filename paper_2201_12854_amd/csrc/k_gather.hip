@@ -98,7 +98,6 @@ __device__ void saturated_group(const FwdParams& p, const int* satl, int64_t t0,
   using T = typename Elem<BF>::T;
   constexpr int NC = WC / 16;     // 16-column MFMA tiles
   constexpr int KS = BF ? 32 : 16;  // k per step
-  constexpr int DEPTH = 4;          // steps per round (din_pad / KS is a multiple of 4)
   const int r16 = lane & 15, g = lane >> 4;
   const int d_in = p.d_in;
   const int din_pad = p.din_pad;
@@ -113,35 +112,53 @@ __device__ void saturated_group(const FwdParams& p, const int* satl, int64_t t0,
   f32x4_t acc[NC];
 #pragma unroll
   for (int c = 0; c < NC; ++c) acc[c] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  // rounds of DEPTH steps: all loads of the round, then its MFMAs. din_pad is a multiple of
-  // 128 elements, so every round is whole and the loop has no conditional code (the
-  // padded k carry zero weights; x past d_in reads as zero).
-  for (int ks0 = 0; ks0 < nks; ks0 += DEPTH) {
-    uint4 a[DEPTH], w[DEPTH][NC];
-#pragma unroll
-    for (int u = 0; u < DEPTH; ++u) {
-      const int ks = ks0 + u;
-      a[u] = load_x_chunk<BF, VEC>(xrow, ks * KS + (BF ? 8 : 4) * g, d_in);
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-        w[u][c] = *reinterpret_cast<const uint4*>(wt + ((int64_t)c * nks + ks) * 64 * E);
+  // rounds of RD steps, software pipelined (16-byte x loads): the loads of round t + 1 are
+  // issued before the MFMAs of round t. din_pad is a multiple of 128 elements, so every round is whole and
+  // the loop has no conditional code (the padded k carry zero weights; x past d_in reads
+  // as zero); the round after the last reloads the last one (unused).
+  constexpr int RD = VEC ? 2 : 4;
+  const int nrounds = nks / RD;
+  uint4 a0[RD], w0[RD][NC], a1[RD], w1[RD][NC];
+#define MCA_LOAD_ROUND(A, Wr, RND)                                                              \
+  _Pragma("unroll") for (int u = 0; u < RD; ++u) {                                             \
+    const int ks = (RND) * RD + u;                                                             \
+    A[u] = load_x_chunk<BF, VEC>(xrow, ks * KS + (BF ? 8 : 4) * g, d_in);                      \
+    _Pragma("unroll") for (int c = 0; c < NC; ++c)                                             \
+      Wr[u][c] = *reinterpret_cast<const uint4*>(wt + ((int64_t)c * nks + ks) * 64 * E);       \
+  }
+#define MCA_MFMA_ROUND(A, Wr)                                                                   \
+  _Pragma("unroll") for (int u = 0; u < RD; ++u) {                                             \
+    _Pragma("unroll") for (int c = 0; c < NC; ++c) {                                           \
+      if constexpr (BF) {                                                                      \
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A[u]),   \
+                                                        __builtin_bit_cast(bf16x8_t, Wr[u][c]), \
+                                                        acc[c], 0, 0, 0);                       \
+      } else {                                                                                 \
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u].x), __uint_as_float(Wr[u][c].x), acc[c], 0, 0, 0); \
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u].y), __uint_as_float(Wr[u][c].y), acc[c], 0, 0, 0); \
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u].z), __uint_as_float(Wr[u][c].z), acc[c], 0, 0, 0); \
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u].w), __uint_as_float(Wr[u][c].w), acc[c], 0, 0, 0); \
+      }                                                                                        \
+    }                                                                                          \
+  }
+  if constexpr (VEC) {
+    MCA_LOAD_ROUND(a0, w0, 0)
+    for (int rd = 0; rd < nrounds; rd += 2) {  // nrounds is even (nks is a multiple of 4)
+      MCA_LOAD_ROUND(a1, w1, rd + 1)
+      __builtin_amdgcn_sched_barrier(0);  // the next round's loads stay ahead of these MFMAs
+      MCA_MFMA_ROUND(a0, w0)
+      MCA_LOAD_ROUND(a0, w0, min(rd + 2, nrounds - 1))
+      __builtin_amdgcn_sched_barrier(0);
+      MCA_MFMA_ROUND(a1, w1)
     }
-#pragma unroll
-    for (int u = 0; u < DEPTH; ++u) {
-#pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        if constexpr (BF) {
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[u]),
-                                                          __builtin_bit_cast(bf16x8_t, w[u][c]), acc[c], 0, 0, 0);
-        } else {
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[u].x), __uint_as_float(w[u][c].x), acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[u].y), __uint_as_float(w[u][c].y), acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[u].z), __uint_as_float(w[u][c].z), acc[c], 0, 0, 0);
-          acc[c] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[u].w), __uint_as_float(w[u][c].w), acc[c], 0, 0, 0);
-        }
-      }
+  } else {  // element-wise x loads take more registers: one buffer
+    for (int rd = 0; rd < nrounds; ++rd) {
+      MCA_LOAD_ROUND(a0, w0, rd)
+      MCA_MFMA_ROUND(a0, w0)
     }
   }
+#undef MCA_LOAD_ROUND
+#undef MCA_MFMA_ROUND
   // acc[c][i] = H~[token of list row 4 g + i][c0 + 16 c + r16]; lane 4 g + i holds that token
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
@@ -150,6 +167,58 @@ __device__ void saturated_group(const FwdParams& p, const int* satl, int64_t t0,
       const int64_t base = (int64_t)tok_i * p.d_out + c0 + r16;
 #pragma unroll
       for (int c = 0; c < NC; ++c) store_h<BF>(p, base + 16 * c, acc[c][i]);
+    }
+  }
+}
+
+// The same for bfloat16 with d_in <= 768 and 16-byte x loads, with the B operand (the
+// slice's two 16-column tiles of the prepared W_v^T, fragment order) copied into LDS once
+// per block: the x chunks of (at most 24) k steps are loaded in two batches of 12, so an
+// item waits for global memory twice; steps past din_pad / 32 read zero x (k >= d_in) and
+// the last B fragment.
+constexpr int kLdsbSteps = 24;  // din_pad <= 768
+__device__ void saturated_group_ldsb(const FwdParams& p, const int* satl, int64_t t0, int gi, int nsat, int c0,
+                                     int lane, const uint4* Bl) {
+  const int r16 = lane & 15, g = lane >> 4;
+  const int d_in = p.d_in;
+  const int nks = p.din_pad / 32;
+  const int64_t tk = t0 + satl[min(16 * gi + r16, nsat - 1)];
+  const uint16_t* xrow = static_cast<const uint16_t*>(p.X) + (int64_t)tk * d_in;
+  constexpr int HALF = kLdsbSteps / 2;
+  // the chunk offsets depend only on the lane: kept inside the item (an empty asm hides the
+  // value), or the compiler keeps all 24 addresses alive across the item loop
+  int kb = 8 * g;
+  asm volatile("" : "+v"(kb));
+  const uint16_t* xr = xrow + kb;
+  const int klast = d_in - 8 - kb;  // last in-row chunk start, relative to kb
+  f32x4_t acc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+  for (int h0 = 0; h0 < kLdsbSteps; h0 += HALF) {
+    uint4 a[HALF];
+#pragma unroll
+    for (int u = 0; u < HALF; ++u) {
+      const int k = (h0 + u) * 32;  // relative to kb; past the row reads zero
+      const uint4 v = *reinterpret_cast<const uint4*>(xr + min(k, klast));
+      const uint32_t keep = k <= klast ? 0xffffffffu : 0u;
+      a[u] = make_uint4(v.x & keep, v.y & keep, v.z & keep, v.w & keep);
+    }
+#pragma unroll
+    for (int u = 0; u < HALF; ++u) {
+      const int ks = min(h0 + u, nks - 1);
+#pragma unroll
+      for (int c = 0; c < 2; ++c)
+        acc[c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[u]),
+                                                        __builtin_bit_cast(bf16x8_t, Bl[(c * nks + ks) * 64 + lane]),
+                                                        acc[c], 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int64_t tok_i = t0 + satl[min(16 * gi + 4 * g + i, nsat - 1)];
+    if (16 * gi + 4 * g + i < nsat) {
+      const int64_t base = (int64_t)tok_i * p.d_out + c0 + r16;
+#pragma unroll
+      for (int c = 0; c < 2; ++c) store_h<1>(p, base + 16 * c, acc[c][i]);
     }
   }
 }
@@ -178,9 +247,10 @@ constexpr int kCtrOff = 64;        // counters: [0] saturated, [1 + key] key cou
                                    // queue, [kCtrOff + key] key offsets, [kCtrOff + kNumKeys] sampled
 constexpr int kNumCtr = 128;
 
-__host__ __device__ inline size_t gather_lds_bytes(int d_in, int wc) {
+__host__ __device__ inline size_t gather_lds_bytes(int d_in, int wc, bool ldsb) {
   return 128                                 // alignment of the slice
          + (size_t)(d_in + 2) * wc * 4       // W_v slice, float32, and two zero rows
+         + (ldsb ? (size_t)2 * kLdsbSteps * 1024 : 0)  // B fragments of the MFMA path
          + (size_t)kChunk * 4 * 2            // sampled order, saturated list
          + kNumCtr * 4;                      // counters
 }
@@ -300,7 +370,7 @@ __device__ void sampled_item(const FwdParams& p, const float* Ws, const uint32_t
   if (valid) store_h4<BF>(p, tk * p.d_out + c0 + 4 * v, acc[0]);
 }
 
-template <int BF, int WC, bool VEC>
+template <int BF, int WC, bool VEC, bool LDSB>
 __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   constexpr int RB = WC * 4;   // bytes per slice row in LDS
   constexpr int G = 64 / (RB / 16);  // sampled tokens per work item
@@ -314,7 +384,9 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t ntok = (int64_t)p.B * p.n;
   float* Ws = reinterpret_cast<float*>(smem);  // [d_in + 2][WC], the last two rows zero
-  uint32_t* order = reinterpret_cast<uint32_t*>(smem + (size_t)(d_in + 2) * WC * 4);  // [kChunk]
+  uint4* Bl = reinterpret_cast<uint4*>(smem + (size_t)(d_in + 2) * WC * 4);          // LDSB: [2][nks][64]
+  uint32_t* order = reinterpret_cast<uint32_t*>(smem + (size_t)(d_in + 2) * WC * 4 +
+                                                (LDSB ? (size_t)2 * kLdsbSteps * 1024 : 0));  // [kChunk]
   int* satl = reinterpret_cast<int*>(order + kChunk);                                // [kChunk]
   int* ctr = satl + kChunk;                                                          // [kNumCtr]
   const int stride = list_stride(d_in);
@@ -329,62 +401,88 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   }
 
   // ---- the slice of W_v, as float32, into LDS, then two zero rows: 16-byte global loads,
-  // four per thread in flight before the conversions and LDS stores
+  // four per thread in flight. The first four are issued now and stored after the first
+  // pass has classified its tokens, so that the classification overlaps their latency.
+  using TW = typename Elem<BF>::T;
+  constexpr int CE = BF ? 8 : 4;  // elements per 16-byte chunk
+  constexpr int CPR = WC / CE;    // chunks per slice row
+  const TW* Wg = static_cast<const TW*>(p.W);
+  const int nchunk = d_in * CPR;
+  uint4 su[4];
+#define MCA_SLICE_LOAD(V0)                                                                     \
+  _Pragma("unroll") for (int h = 0; h < 4; ++h) {                                            \
+    const int v = min((V0) + h * kThreads, nchunk - 1); /* clamped: stored only if in range */ \
+    su[h] = *reinterpret_cast<const uint4*>(Wg + (int64_t)(v / CPR) * d_out + c0 + (v % CPR) * CE); \
+  }
+#define MCA_SLICE_STORE(V0)                                                                    \
+  _Pragma("unroll") for (int h = 0; h < 4; ++h) {                                            \
+    const int v = (V0) + h * kThreads;                                                         \
+    if (v < nchunk) {                                                                          \
+      float* dst = Ws + (v / CPR) * WC + (v % CPR) * CE;                                       \
+      if constexpr (BF) {                                                                      \
+        reinterpret_cast<float4*>(dst)[0] =                                                    \
+            make_float4(__uint_as_float(su[h].x << 16), __uint_as_float(su[h].x & 0xffff0000u), \
+                        __uint_as_float(su[h].y << 16), __uint_as_float(su[h].y & 0xffff0000u)); \
+        reinterpret_cast<float4*>(dst)[1] =                                                    \
+            make_float4(__uint_as_float(su[h].z << 16), __uint_as_float(su[h].z & 0xffff0000u), \
+                        __uint_as_float(su[h].w << 16), __uint_as_float(su[h].w & 0xffff0000u)); \
+      } else {                                                                                 \
+        *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(su[h].x), __uint_as_float(su[h].y), \
+                                                      __uint_as_float(su[h].z), __uint_as_float(su[h].w)); \
+      }                                                                                        \
+    }                                                                                          \
+  }
+  MCA_SLICE_LOAD(tid)
+  // LDSB: the slice's B fragments (2 tiles x nks steps x 1 KB, contiguous in the prepared
+  // weights), at most 3 16-byte chunks per thread
+  const int nfrag = LDSB ? 2 * (p.din_pad / 32) * 64 : 1;
+  uint4 fu0, fu1, fu2;
+  if constexpr (LDSB) {
+    const uint4* src = static_cast<const uint4*>(p.Wt) + (size_t)(c0 / 16) * (p.din_pad / 32) * 64;
+    fu0 = src[min(tid, nfrag - 1)];
+    fu1 = src[min(tid + kThreads, nfrag - 1)];
+    fu2 = src[min(tid + 2 * kThreads, nfrag - 1)];
+  }
   if (tid < 2 * WC) Ws[d_in * WC + tid] = 0.f;
-  {
-    using T = typename Elem<BF>::T;
-    constexpr int CE = BF ? 8 : 4;  // elements per 16-byte chunk
-    constexpr int CPR = WC / CE;    // chunks per slice row
-    const T* W = static_cast<const T*>(p.W);
-    const int nchunk = d_in * CPR;
-    for (int v0 = tid; v0 < nchunk; v0 += 4 * kThreads) {
-      uint4 u[4];
-#pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const int v = min(v0 + h * kThreads, nchunk - 1);  // clamped: in range, stored only if v < nchunk
-        u[h] = *reinterpret_cast<const uint4*>(W + (int64_t)(v / CPR) * d_out + c0 + (v % CPR) * CE);
-      }
-#pragma unroll
-      for (int h = 0; h < 4; ++h) {
-        const int v = v0 + h * kThreads;
-        if (v < nchunk) {
-          float* dst = Ws + (v / CPR) * WC + (v % CPR) * CE;
-          if constexpr (BF) {
-            reinterpret_cast<float4*>(dst)[0] =
-                make_float4(__uint_as_float(u[h].x << 16), __uint_as_float(u[h].x & 0xffff0000u),
-                            __uint_as_float(u[h].y << 16), __uint_as_float(u[h].y & 0xffff0000u));
-            reinterpret_cast<float4*>(dst)[1] =
-                make_float4(__uint_as_float(u[h].z << 16), __uint_as_float(u[h].z & 0xffff0000u),
-                            __uint_as_float(u[h].w << 16), __uint_as_float(u[h].w & 0xffff0000u));
-          } else {
-            *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(u[h].x), __uint_as_float(u[h].y),
-                                                          __uint_as_float(u[h].z), __uint_as_float(u[h].w));
-          }
-        }
-      }
-    }
+
+  // ---- classify a pass's tokens (one per thread) and sort the sampled ones by key
+  int key, rank;
+  uint32_t ent;
+#define MCA_CLASSIFY(T0, RV, UV)                                                                \
+  {                                                                                            \
+    const int m = (int)min((int64_t)kChunk, t_end - (T0));                                     \
+    key = -1;                                                                                  \
+    rank = 0;                                                                                  \
+    ent = 0;                                                                                   \
+    if (tid < m) {                                                                             \
+      const int r = (RV), uc = (UV);                                                           \
+      const int len = min(uc & 0xffff, stride);                                                \
+      const int nepad = min(min((uc >> 16) & 0xffff, len), 2046) & ~1;                         \
+      if (r >= d_in) {                                                                         \
+        satl[atomicAdd(ctr, 1)] = tid;                                                         \
+      } else if (r > 0 && len > 0) {                                                           \
+        key = sort_key(len);                                                                   \
+        rank = atomicAdd(ctr + 1 + key, 1);                                                    \
+        ent = ((uint32_t)tid << kTokShift) | ((uint32_t)len << kLenShift) | (uint32_t)(nepad >> 1); \
+      }                                                                                        \
+    }                                                                                          \
+  }
+  if (tid < kNumCtr) ctr[tid] = 0;
+  __syncthreads();  // the counters are clear
+  MCA_CLASSIFY(t_begin, r_first, u_first)
+  // the slice into LDS while the first pass is being sorted (published by the barriers below)
+  MCA_SLICE_STORE(tid)
+  if constexpr (LDSB) {
+    if (tid < nfrag) Bl[tid] = fu0;
+    if (tid + kThreads < nfrag) Bl[tid + kThreads] = fu1;
+    if (tid + 2 * kThreads < nfrag) Bl[tid + 2 * kThreads] = fu2;
+  }
+  for (int v0 = tid + 4 * kThreads; v0 < nchunk; v0 += 4 * kThreads) {
+    MCA_SLICE_LOAD(v0)
+    MCA_SLICE_STORE(v0)
   }
 
-  for (int64_t t0 = t_begin; t0 < t_end; t0 += kChunk) {
-    const int m = (int)min((int64_t)kChunk, t_end - t0);
-    if (tid < kNumCtr) ctr[tid] = 0;
-    __syncthreads();  // also: the slice is in LDS, the previous pass is done
-    // ---- classify this pass's tokens (one per thread) and sort the sampled ones by key
-    int key = -1, rank = 0;
-    uint32_t ent = 0;
-    if (tid < m) {
-      const int r = t0 == t_begin ? r_first : p.r[t0 + tid];
-      const int uc = t0 == t_begin ? u_first : p.ucount[t0 + tid];
-      const int len = min(uc & 0xffff, stride);
-      const int nepad = min(min((uc >> 16) & 0xffff, len), 2046) & ~1;
-      if (r >= d_in) {
-        satl[atomicAdd(ctr, 1)] = tid;
-      } else if (r > 0 && len > 0) {
-        key = sort_key(len);
-        rank = atomicAdd(ctr + 1 + key, 1);
-        ent = ((uint32_t)tid << kTokShift) | ((uint32_t)len << kLenShift) | (uint32_t)(nepad >> 1);
-      }
-    }
+  for (int64_t t0 = t_begin;;) {
     __syncthreads();
     if (tid < 64) {  // one wave: offset of every key, longest lists first
       const int k = kNumKeys - 1 - tid;  // lane l holds key kNumKeys - 1 - l
@@ -412,11 +510,22 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
       if (lane == 0) it = atomicAdd(ctr + 60, 1);
       it = __builtin_amdgcn_readfirstlane(it);
       if (it >= nitems) break;
-      if (it < ngroups) saturated_group<BF, WC, VEC>(p, satl, t0, it, nsat, c0, lane);
+      if (it < ngroups) {
+        if constexpr (LDSB) saturated_group_ldsb(p, satl, t0, it, nsat, c0, lane, Bl);
+        else saturated_group<BF, WC, VEC>(p, satl, t0, it, nsat, c0, lane);
+      }
       else sampled_item<BF, RB>(p, Ws, order, (it - ngroups) * G, nsampled, t0, c0, lane);
     }
-    __syncthreads();  // the lists of this pass are rewritten next
+    __syncthreads();  // the order and the counters are rewritten next
+    t0 += kChunk;
+    if (t0 >= t_end) break;
+    if (tid < kNumCtr) ctr[tid] = 0;
+    __syncthreads();
+    MCA_CLASSIFY(t0, p.r[t0 + tid], p.ucount[t0 + tid])
   }
+#undef MCA_CLASSIFY
+#undef MCA_SLICE_LOAD
+#undef MCA_SLICE_STORE
 }
 
 int device_cus() {
@@ -431,22 +540,26 @@ int device_cus() {
   return cached[dev];
 }
 
-template <int BF, int WC, bool VEC>
+template <int BF, int WC, bool VEC, bool LDSB>
 hipError_t launch_wc(const FwdParams& p, hipStream_t s) {
-  const size_t lds = gather_lds_bytes(p.d_in, WC);
+  const size_t lds = gather_lds_bytes(p.d_in, WC, LDSB);
   if (lds > 160 * 1024) return hipErrorInvalidValue;  // gfx950: 160 KB of LDS per workgroup
-  // the largest slice (2048 x 16 or 1024 x 32 floats) plus the lists; allowed once per device
+  if (LDSB && p.din_pad > 32 * kLdsbSteps) return hipErrorInvalidValue;
+  // the largest slice of the variant plus the lists; allowed once per device
   static int allowed[64] = {0};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
   if (!allowed[dev]) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_gather<BF, WC, VEC>, hipFuncAttributeMaxDynamicSharedMemorySize,
-                                             (int)gather_lds_bytes(WC == 32 ? 1024 : 2048, WC));
+    const int dmax = LDSB ? 32 * kLdsbSteps : (WC == 32 ? 1024 : 2048);
+    const hipError_t e = hipFuncSetAttribute((const void*)k_gather<BF, WC, VEC, LDSB>,
+                                             hipFuncAttributeMaxDynamicSharedMemorySize,
+                                             (int)gather_lds_bytes(dmax, WC, LDSB));
     if (e != hipSuccess) return e;
     allowed[dev] = 1;
   }
   const int nslices = p.d_out / WC;
-  hipLaunchKernelGGL((k_gather<BF, WC, VEC>), dim3((unsigned)(nslices * p.gather_bps)), dim3(kThreads), lds, s, p);
+  hipLaunchKernelGGL((k_gather<BF, WC, VEC, LDSB>), dim3((unsigned)(nslices * p.gather_bps)), dim3(kThreads), lds,
+                     s, p);
   return hipGetLastError();
 }
 
@@ -462,11 +575,15 @@ hipError_t launch_gather(const FwdParams& p, hipStream_t s) {
   if (p.wc != gather_slice_cols(p.d_in) || p.d_out % p.wc != 0 || p.gather_bps < 1) return hipErrorInvalidValue;
   const bool vec = p.d_in % (p.bf16 ? 8 : 4) == 0;
   if (p.bf16) {
-    if (p.wc == 32) return vec ? launch_wc<1, 32, true>(p, s) : launch_wc<1, 32, false>(p, s);
-    return vec ? launch_wc<1, 16, true>(p, s) : launch_wc<1, 16, false>(p, s);
+    if (p.wc == 32) {
+      // bfloat16, d_in <= 768: the saturated tokens' B operand fits in LDS next to the slice
+      if (vec && p.din_pad <= 32 * kLdsbSteps) return launch_wc<1, 32, true, true>(p, s);
+      return vec ? launch_wc<1, 32, true, false>(p, s) : launch_wc<1, 32, false, false>(p, s);
+    }
+    return vec ? launch_wc<1, 16, true, false>(p, s) : launch_wc<1, 16, false, false>(p, s);
   }
-  if (p.wc == 32) return vec ? launch_wc<0, 32, true>(p, s) : launch_wc<0, 32, false>(p, s);
-  return vec ? launch_wc<0, 16, true>(p, s) : launch_wc<0, 16, false>(p, s);
+  if (p.wc == 32) return vec ? launch_wc<0, 32, true, false>(p, s) : launch_wc<0, 32, false, false>(p, s);
+  return vec ? launch_wc<0, 16, true, false>(p, s) : launch_wc<0, 16, false, false>(p, s);
 }
 
 }  // namespace mca

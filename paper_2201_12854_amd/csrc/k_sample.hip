@@ -34,7 +34,7 @@ namespace {
 template <int BF> struct Elem { using T = float; };
 template <> struct Elem<1> { using T = uint16_t; };
 
-constexpr int kWaves = 4;  // tokens per block
+constexpr int kMaxWaves = 16;  // tokens (waves) per block: 16, 8 or 4, as the LDS allows
 
 
 // Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
@@ -64,54 +64,68 @@ __device__ __forceinline__ void write_zero4(const FwdParams& p, int64_t off) {
 
 // Per-wave results of phase 1, shared with the block for the pooled draws.
 struct TokInfo {
-  int r[kWaves];        // draws of the wave's token (0: no draws)
-  int j[kWaves], b[kWaves];
-  uint32_t pad[kWaves];
-  uint64_t T[kWaves];   // total weight C[d_in - 1]
+  int r[kMaxWaves];     // draws of the wave's token (0: no draws)
+  int j[kMaxWaves], b[kMaxWaves];
+  int P[kMaxWaves + 1];  // exclusive prefix sums of r: the token's first pooled draw
+  uint64_t T[kMaxWaves];  // total weight C[d_in - 1]
 };
-constexpr int kHeader = 128;  // bytes of LDS before the per-token regions
+constexpr int kHeader = 512;  // bytes of LDS before the per-token regions
 static_assert(sizeof(TokInfo) <= kHeader, "header");
 
 // LDS of a block: the header, then
 //   Eq. 4: per wave C uint64 [d_in] (after the draws: record x float32 [d_in], record w
-//          uint32 [d_in]), then cnt uint32 [d_in] (after the draws: record row | count);
+//          uint32 [d_in]) and cnt uint32 [d_in] (after the draws: record row | count);
 //   Eq. 6: the shared C uint64 [d_in], then per wave cnt uint32 [d_in] and record x
 //          float32 [d_in].
 __host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
+__host__ __device__ inline int sample_shared_bytes(int d_in, bool table) { return table ? round16(8 * d_in) : 0; }
 __host__ __device__ inline int sample_region_bytes(int d_in, bool table) {
   return table ? 2 * round16(4 * d_in) : round16(8 * d_in) + round16(4 * d_in);
 }
-__host__ __device__ inline int sample_lds_bytes(int d_in, bool table) {
-  return kHeader + (table ? round16(8 * d_in) : 0) + kWaves * sample_region_bytes(d_in, table);
+__host__ __device__ inline int sample_lds_bytes(int d_in, bool table, int nw) {
+  return kHeader + sample_shared_bytes(d_in, table) + nw * sample_region_bytes(d_in, table);
+}
+__device__ __forceinline__ int region_off(int d_in, bool table, int w) {
+  return kHeader + sample_shared_bytes(d_in, table) + w * sample_region_bytes(d_in, table);
+}
+__device__ __forceinline__ int c_off(int d_in, bool table, int w) { return table ? kHeader : region_off(d_in, false, w); }
+__device__ __forceinline__ int cnt_off(int d_in, bool table, int w) {
+  return region_off(d_in, table, w) + (table ? 0 : round16(8 * d_in));
 }
 
-// W draws of one thread of the block's pool: draw d = d0 + 256 u (u < W) of the
+// W draws of one thread of the block's pool: draw d = d0 + 64 NW u (u < W) of the
 // concatenated draws of the block's tokens (token w owns [P_w, P_w + r_w)). Each is draw
 // k = d - P_w of its token: Philox4x32-10 with counter (k, j, b, 0), t = floor(u T / 2^64)
-// and s = min{i : C_i > t} by a fixed number of halvings (ceil(log2 d_in)) without
-// branches (once lo == hi it stays put, since C[lo] > t there), searched together so that
-// their LDS reads overlap; then the token's count of row s goes up by one.
-template <int W, bool TABLE>
-__device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I, unsigned char* smem, int d0, int P1,
-                                           int P2, int P3, int D, int nsteps) {
+// and s = min{i : C_i > t}, the W searches together so that their LDS reads overlap;
+// then the token's count of row s goes up by one.
+template <int W, int NW, bool TABLE>
+__device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I, unsigned char* smem, int d0,
+                                           const int* Ps, int D, int nsteps) {
   const int d_in = p.d_in;
   uint64_t t[W];
-  int lo[W], hi[W], wt[W], kk[W];
+  int lo[W], wt[W], kk[W];
   const uint64_t* Cw[W];
 #pragma unroll
   for (int u = 0; u < W; ++u) {
-    const int d = min(d0 + u * 64 * kWaves, D - 1);  // clamped: only d < D is counted
-    const int w = (d >= P1) + (d >= P2) + (d >= P3);
-    const int base = w == 0 ? 0 : (w == 1 ? P1 : (w == 2 ? P2 : P3));
+    const int d = min(d0 + u * 64 * NW, D - 1);  // clamped: only d < D is counted
+    int w = 0;  // the token: number of token starts P_1 .. P_{NW-1} at or below d
+#pragma unroll
+    for (int i = 1; i < NW; ++i) w += d >= Ps[i];
     wt[u] = w;
-    kk[u] = d - base;
+    kk[u] = d - I.P[w];
     const u32x4 o = philox4x32_10(u32x4{(uint32_t)kk[u], (uint32_t)I.j[w], (uint32_t)I.b[w], 0u}, p.seed_lo,
                                   p.seed_hi);
     t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), I.T[w]);  // in [0, T)
-    Cw[u] = reinterpret_cast<const uint64_t*>(
-        smem + kHeader + (TABLE ? 0 : w * sample_region_bytes(d_in, false)));
+    Cw[u] = reinterpret_cast<const uint64_t*>(smem + c_off(d_in, TABLE, w));
+  }
+  // fixed-step halving (ceil(log2 d_in) steps, no branches), step-major so that the W
+  // searches' LDS reads are in flight together; C[d_in-1] = T > t, so the answer is in
+  // range, and once lo == hi it stays put
+  int hi[W];
+#pragma unroll
+  for (int u = 0; u < W; ++u) {
     lo[u] = 0;
-    hi[u] = d_in - 1;  // C[d_in-1] = T > t, so the answer is in range
+    hi[u] = d_in - 1;
   }
   for (int st = 0; st < nsteps; ++st) {
 #pragma unroll
@@ -124,11 +138,9 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
   }
 #pragma unroll
   for (int u = 0; u < W; ++u) {
-    if (d0 + u * 64 * kWaves < D) {
+    if (d0 + u * 64 * NW < D) {
       const int w = wt[u];
-      uint32_t* cnt = reinterpret_cast<uint32_t*>(
-          smem + kHeader + (TABLE ? round16(8 * d_in) + w * sample_region_bytes(d_in, true)
-                                  : w * sample_region_bytes(d_in, false) + round16(8 * d_in)));
+      uint32_t* cnt = reinterpret_cast<uint32_t*>(smem + cnt_off(d_in, TABLE, w));
       atomicAdd(cnt + lo[u], 1u);
       const int64_t tok = (int64_t)I.b[w] * p.n + I.j[w];
       const int64_t o2 = tok * d_in + kk[u];
@@ -151,32 +163,28 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
 // Phase 2: the block's draws are pooled over all its threads. Phase 3: every wave merges
 // its token's counts into the list. Two block barriers separate the phases; no wave
 // leaves before them.
-template <int BF, int PER, bool TABLE>
-__global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
+template <int BF, int PER, bool TABLE, int NW>
+__global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   using T = typename Elem<BF>::T;
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t ntok = (int64_t)p.B * p.n;
-  const int64_t tok = (int64_t)blockIdx.x * kWaves + wave;
+  const int64_t tok = (int64_t)blockIdx.x * NW + wave;
   const int d_in = p.d_in, n = p.n;
   TokInfo& I = *reinterpret_cast<TokInfo*>(smem);
   uint64_t* C;      // this token's prefix sums (Eq. 6: the shared table)
   uint32_t* cnt;    // this token's draw counts, then record row | count
   float* rec_x;     // record x
   uint32_t* rec_w;  // record w (Eq. 4 only)
+  C = reinterpret_cast<uint64_t*>(smem + c_off(d_in, TABLE, wave));
+  cnt = reinterpret_cast<uint32_t*>(smem + cnt_off(d_in, TABLE, wave));
   if constexpr (TABLE) {
-    C = reinterpret_cast<uint64_t*>(smem + kHeader);
-    unsigned char* wl = smem + kHeader + round16(8 * d_in) + wave * sample_region_bytes(d_in, true);
-    cnt = reinterpret_cast<uint32_t*>(wl);
-    rec_x = reinterpret_cast<float*>(wl + round16(4 * d_in));
+    rec_x = reinterpret_cast<float*>(smem + cnt_off(d_in, true, wave) + round16(4 * d_in));
     rec_w = nullptr;
-    for (int i = threadIdx.x; i < d_in; i += 64 * kWaves) C[i] = p.wtable[i];
+    for (int i = threadIdx.x; i < d_in; i += 64 * NW) C[i] = p.wtable[i];
   } else {
-    unsigned char* wl = smem + kHeader + wave * sample_region_bytes(d_in, false);
-    C = reinterpret_cast<uint64_t*>(wl);
-    cnt = reinterpret_cast<uint32_t*>(wl + round16(8 * d_in));
-    rec_x = reinterpret_cast<float*>(wl);
-    rec_w = reinterpret_cast<uint32_t*>(wl + 4 * d_in);
+    rec_x = reinterpret_cast<float*>(C);
+    rec_w = reinterpret_cast<uint32_t*>(reinterpret_cast<unsigned char*>(C) + 4 * d_in);
   }
   const bool live = tok < ntok;
   const int64_t tk = live ? tok : ntok - 1;  // a wave without a token reads a valid one
@@ -318,18 +326,31 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   }
   __syncthreads();
 
-  // ---- phase 2. the block's draws, 64 kWaves threads, up to 4 per thread in flight
+  if (threadIdx.x == 0) {  // where each token's draws start in the pool
+    int acc = 0;
+    for (int w = 0; w < NW; ++w) {
+      I.P[w] = acc;
+      acc += I.r[w];
+    }
+    I.P[NW] = acc;
+  }
+  __syncthreads();
+
+  // ---- phase 2. the block's draws, 64 NW threads, up to 4 per thread in flight
   {
-    const int P1 = I.r[0], P2 = P1 + I.r[1], P3 = P2 + I.r[2], D = P3 + I.r[3];
+    int Ps[NW];  // block-uniform: scalar registers
+#pragma unroll
+    for (int i = 0; i < NW; ++i) Ps[i] = __builtin_amdgcn_readfirstlane(I.P[i]);
+    const int D = __builtin_amdgcn_readfirstlane(I.P[NW]);
     const int nsteps = 32 - __clz(max(d_in - 1, 1));
-    const int nper = (D + 64 * kWaves - 1) / (64 * kWaves);
+    const int nper = (D + 64 * NW - 1) / (64 * NW);
     for (int u0 = 0; u0 < nper; u0 += 4) {
-      const int d0 = threadIdx.x + u0 * 64 * kWaves;
+      const int d0 = threadIdx.x + u0 * 64 * NW;
       const int w = min(4, nper - u0);
-      if (w == 4) draw_batch<4, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
-      else if (w == 3) draw_batch<3, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
-      else if (w == 2) draw_batch<2, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
-      else draw_batch<1, TABLE>(p, I, smem, d0, P1, P2, P3, D, nsteps);
+      if (w == 4) draw_batch<4, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
+      else if (w == 3) draw_batch<3, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
+      else if (w == 2) draw_batch<2, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
+      else draw_batch<1, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
     }
   }
   __syncthreads();
@@ -398,18 +419,29 @@ __global__ __launch_bounds__(64 * kWaves) void k_sample(FwdParams p) {
   }
 }
 
-template <int BF, int PER, bool TABLE>
-hipError_t launch_per(const FwdParams& p, hipStream_t s) {
+template <int BF, int PER, bool TABLE, int NW>
+hipError_t launch_nw(const FwdParams& p, hipStream_t s) {
   const int64_t ntok = (int64_t)p.B * p.n;
-  const dim3 grid((unsigned)((ntok + kWaves - 1) / kWaves));
-  const size_t lds = (size_t)sample_lds_bytes(p.d_in, TABLE);
+  const dim3 grid((unsigned)((ntok + NW - 1) / NW));
+  const size_t lds = (size_t)sample_lds_bytes(p.d_in, TABLE, NW);
   if (lds > 65536) {
-    const hipError_t e = hipFuncSetAttribute((const void*)k_sample<BF, PER, TABLE>,
+    const hipError_t e = hipFuncSetAttribute((const void*)k_sample<BF, PER, TABLE, NW>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((k_sample<BF, PER, TABLE>), grid, dim3(64 * kWaves), lds, s, p);
+  hipLaunchKernelGGL((k_sample<BF, PER, TABLE, NW>), grid, dim3(64 * NW), lds, s, p);
   return hipGetLastError();
+}
+
+// As many tokens per block as the LDS holds (16, 8 or 4): more tokens per block spread the
+// pooled draws over more threads.
+template <int BF, int PER, bool TABLE>
+hipError_t launch_per(const FwdParams& p, hipStream_t s) {
+  constexpr int kLds = 160 * 1024;
+  if (sample_lds_bytes(p.d_in, TABLE, 16) <= kLds) return launch_nw<BF, PER, TABLE, 16>(p, s);
+  if (sample_lds_bytes(p.d_in, TABLE, 8) <= kLds) return launch_nw<BF, PER, TABLE, 8>(p, s);
+  if (sample_lds_bytes(p.d_in, TABLE, 4) <= kLds) return launch_nw<BF, PER, TABLE, 4>(p, s);
+  return hipErrorInvalidValue;
 }
 
 template <int BF, int PER>
