@@ -245,7 +245,8 @@ def main():
     value = L.tokens / (ms * 1e-3)
     log(f"mca forward: {ms * 1e3:.1f} us/step, {value:.4g} tokens/s (wall {wall:.2f} s)")
 
-    # per-stage kernel times: HIP events around every launch on the library's stream
+    # per-stage kernel times: a HIP event pair per stage kernel, stamped by its dispatch at the
+    # kernel's start and end (on the library's stream)
     prof = mca.Profiler()
     pplan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
                             seq_lens=lens, profiler=prof)
@@ -321,6 +322,12 @@ def main():
             ms_a, _ = time_loop(p2.run, args.steps, args.warmup)
             other[str(a)] = {"ms_per_step": ms_a, "tokens_per_s": L.tokens / (ms_a * 1e-3)}
         record["other_alphas"] = other
+        # the paper's input-independent probability (Eq. 6), same workload and alpha
+        p6 = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
+                             seq_lens=lens, sampling="weight")
+        ms6, _ = time_loop(p6.run, args.steps, args.warmup)
+        record["sampling_eq6"] = {"ms_per_step": ms6, "tokens_per_s": L.tokens / (ms6 * 1e-3)}
+        log(f"mca forward, Eq. 6 sampling: {ms6 * 1e3:.1f} us/step")
     if args.calibrate_copy:
         copy_calibration(args.calibrate_copy)
     if not args.no_cpu_baseline:

@@ -546,32 +546,30 @@ hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
   const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
-    if (nt <= 1) hipLaunchKernelGGL((k_scores_res<1, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) hipLaunchKernelGGL((k_scores_res<1, 2>), grid, blk, 0, s, p);
-    else if (nt <= 4) hipLaunchKernelGGL((k_scores_res<1, 4>), grid, blk, 0, s, p);
-    else hipLaunchKernelGGL(k_scores_stream<1>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_scores_res<1, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2>), grid, blk, 0, s, p);
+    else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4>), grid, blk, 0, s, p);
+    else return launch_stage_kernel(k_scores_stream<1>, grid, blk, 0, s, p);
   } else {
-    if (nt <= 1) hipLaunchKernelGGL((k_scores_res<0, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) hipLaunchKernelGGL((k_scores_res<0, 2>), grid, blk, 0, s, p);
-    else hipLaunchKernelGGL(k_scores_stream<0>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2>), grid, blk, 0, s, p);
+    else return launch_stage_kernel(k_scores_stream<0>, grid, blk, 0, s, p);
   }
-  return hipGetLastError();
 }
 
 hipError_t launch_attn_out(const FwdParams& p, hipStream_t s) {
   const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
-    if (nt <= 1) hipLaunchKernelGGL((k_attn_res<1, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) hipLaunchKernelGGL((k_attn_res<1, 2>), grid, blk, 0, s, p);
-    else if (nt <= 4) hipLaunchKernelGGL((k_attn_res<1, 4>), grid, blk, 0, s, p);
-    else hipLaunchKernelGGL(k_attn_stream<1>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_attn_res<1, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_attn_res<1, 2>), grid, blk, 0, s, p);
+    else if (nt <= 4) return launch_stage_kernel((k_attn_res<1, 4>), grid, blk, 0, s, p);
+    else return launch_stage_kernel(k_attn_stream<1>, grid, blk, 0, s, p);
   } else {
-    if (nt <= 1) hipLaunchKernelGGL((k_attn_res<0, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) hipLaunchKernelGGL((k_attn_res<0, 2>), grid, blk, 0, s, p);
-    else hipLaunchKernelGGL(k_attn_stream<0>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_attn_res<0, 1>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_attn_res<0, 2>), grid, blk, 0, s, p);
+    else return launch_stage_kernel(k_attn_stream<0>, grid, blk, 0, s, p);
   }
-  return hipGetLastError();
 }
 
 }  // namespace mca

@@ -558,9 +558,8 @@ hipError_t launch_wc(const FwdParams& p, hipStream_t s) {
     allowed[dev] = 1;
   }
   const int nslices = p.d_out / WC;
-  hipLaunchKernelGGL((k_gather<BF, WC, VEC, LDSB>), dim3((unsigned)(nslices * p.gather_bps)), dim3(kThreads), lds,
-                     s, p);
-  return hipGetLastError();
+  return launch_stage_kernel(k_gather<BF, WC, VEC, LDSB>, dim3((unsigned)(nslices * p.gather_bps)), dim3(kThreads),
+                             lds, s, p);
 }
 
 }  // namespace

@@ -429,8 +429,7 @@ hipError_t launch_nw(const FwdParams& p, hipStream_t s) {
                                              hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
     if (e != hipSuccess) return e;
   }
-  hipLaunchKernelGGL((k_sample<BF, PER, TABLE, NW>), grid, dim3(64 * NW), lds, s, p);
-  return hipGetLastError();
+  return launch_stage_kernel(k_sample<BF, PER, TABLE, NW>, grid, dim3(64 * NW), lds, s, p);
 }
 
 // As many tokens per block as the LDS holds (16, 8 or 4): more tokens per block spread the

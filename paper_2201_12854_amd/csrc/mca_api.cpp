@@ -122,16 +122,17 @@ int prof_slot(Profiler* pr, int stage) {
   return pr->used++;
 }
 
+// Launches one stage; with a profiler, its kernel carries a start and a stop event that the
+// dispatch records at the kernel's start and end.
 template <typename F>
-mca_status run_stage(Profiler* pr, int stage, hipStream_t s, F&& launch) {
-  int slot = pr ? prof_slot(pr, stage) : -1;
-  if (slot >= 0 && hipEventRecord(pr->start[slot], s) != hipSuccess)
-    return fail(MCA_ERR_HIP, "hipEventRecord failed");
-  hipError_t e = launch();
+mca_status run_stage(Profiler* pr, int stage, mca::FwdParams& p, F&& launch) {
+  const int slot = pr ? prof_slot(pr, stage) : -1;
+  p.ev_start = slot >= 0 ? pr->start[slot] : nullptr;
+  p.ev_stop = slot >= 0 ? pr->stop[slot] : nullptr;
+  const hipError_t e = launch();
+  p.ev_start = p.ev_stop = nullptr;
   if (e != hipSuccess)
     return fail(MCA_ERR_HIP, "stage %s launch failed: %s", mca_stage_name(stage), hipGetErrorString(e));
-  if (slot >= 0 && hipEventRecord(pr->stop[slot], s) != hipSuccess)
-    return fail(MCA_ERR_HIP, "hipEventRecord failed");
   return MCA_OK;
 }
 
@@ -253,11 +254,11 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
 
   hipStream_t s = static_cast<hipStream_t>(stream);
   Profiler* pr = static_cast<Profiler*>(desc->profiler);
-  if ((st = run_stage(pr, MCA_STAGE_SCORES_COLMAX, s, [&] { return mca::launch_scores_colmax(p, s); })) != MCA_OK)
+  if ((st = run_stage(pr, MCA_STAGE_SCORES_COLMAX, p, [&] { return mca::launch_scores_colmax(p, s); })) != MCA_OK)
     return st;
-  if ((st = run_stage(pr, MCA_STAGE_SAMPLE, s, [&] { return mca::launch_sample(p, s); })) != MCA_OK) return st;
-  if ((st = run_stage(pr, MCA_STAGE_GATHER, s, [&] { return mca::launch_gather(p, s); })) != MCA_OK) return st;
-  if ((st = run_stage(pr, MCA_STAGE_ATTN_OUT, s, [&] { return mca::launch_attn_out(p, s); })) != MCA_OK) return st;
+  if ((st = run_stage(pr, MCA_STAGE_SAMPLE, p, [&] { return mca::launch_sample(p, s); })) != MCA_OK) return st;
+  if ((st = run_stage(pr, MCA_STAGE_GATHER, p, [&] { return mca::launch_gather(p, s); })) != MCA_OK) return st;
+  if ((st = run_stage(pr, MCA_STAGE_ATTN_OUT, p, [&] { return mca::launch_attn_out(p, s); })) != MCA_OK) return st;
   return ok();
 }
 

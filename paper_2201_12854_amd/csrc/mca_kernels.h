@@ -1,6 +1,7 @@
 // Host-side launch interface of the MCA kernels (internal to libmca).
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
@@ -71,7 +72,18 @@ struct FwdParams {
   int32_t* idx_out;
   float* coef_out;
   float* enc_out;
+  // profiling: when set, the stage's kernel is launched with these events, which the
+  // dispatch stamps at the kernel's start and end (kernel execution time only)
+  hipEvent_t ev_start, ev_stop;
 };
+
+// Launches a stage kernel (one per stage), with the profiling events when they are set.
+template <typename K>
+inline hipError_t launch_stage_kernel(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const FwdParams& p) {
+  if (p.ev_start) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, p.ev_start, p.ev_stop, 0u, p);
+  else hipLaunchKernelGGL(kernel, grid, block, lds, s, p);
+  return hipGetLastError();
+}
 
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s);
 hipError_t launch_sample(const FwdParams& p, hipStream_t s);
