@@ -276,12 +276,9 @@ __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const unsigned char*)p;  // address-space cast
 }
 
-// Entries 2 h + q, + 1 (q multiple of 2) of one part of a token's list: part 0 (even rows)
-// at list index 0, part 1 (odd rows) at nepad; each part has even length. The load address
-// is clamped into the token's list slot; the caller masks entries past the part's end.
-__device__ __forceinline__ uint4 entry_pair_raw(const uint2* L, int part_base, int q, int stride) {
-  return *reinterpret_cast<const uint4*>(L + min(part_base + q, stride - 2));
-}
+// Entry pairs are read through a pointer that advances one round (LPR entries) at a time,
+// up to three rounds past the end of a part: those entries are masked, and the list buffer
+// has slack after the last token's slot so that the reads stay inside it.
 __device__ __forceinline__ uint4 entry_mask(uint4 v, bool in_part, uint32_t zero_row) {
   const uint32_t k = in_part ? 0xffffffffu : 0u;
   return make_uint4((v.x & k) | (zero_row & ~k), v.y & k, (v.z & k) | (zero_row & ~k), v.w & k);
@@ -327,8 +324,7 @@ __device__ void sampled_item(const FwdParams& p, const float* Ws, const uint32_t
   const int64_t tk = t0 + (e >> kTokShift);
   const int len = (int)((e >> kLenShift) & 0xfffu);
   const int nepad = (int)(e & 0x3ffu) * 2;
-  const int stride = list_stride(p.d_in);
-  const uint2* L = p.list + tk * stride;
+  const uint2* L = p.list + tk * list_stride(p.d_in);
   const bool odd_part = cl >= HALF;
   const int part_base = odd_part ? nepad : 0;
   const int part_len = odd_part ? len - nepad : nepad;
@@ -340,14 +336,23 @@ __device__ void sampled_item(const FwdParams& p, const float* Ws, const uint32_t
   float4 acc[LPR];
 #pragma unroll
   for (int c = 0; c < LPR; ++c) acc[c] = make_float4(0.f, 0.f, 0.f, 0.f);
-  // entries two rounds ahead; masked when consumed, so the loads stay in flight
-  uint4 n1 = entry_pair_raw(L, part_base, h2, stride);
-  uint4 n2 = entry_pair_raw(L, part_base, LPR + h2, stride);
-  for (int q0 = 0; q0 < maxpart; q0 += LPR) {
-    const uint4 en = entry_mask(n1, q0 + h2 < part_len, zero_row);
-    n1 = n2;
-    n2 = entry_pair_raw(L, part_base, q0 + 2 * LPR + h2, stride);
+  // entries two rounds ahead; masked when consumed, so the loads stay in flight. Two
+  // rounds per iteration, so the two buffers swap roles without register copies.
+  const uint4* ep = reinterpret_cast<const uint4*>(L + part_base + h2);  // even index: 16-byte aligned
+  constexpr int EPR = LPR / 2;  // entry pairs (uint4) per part per round
+  uint4 n1 = ep[0], n2 = ep[EPR];
+  ep += 2 * EPR;
+  for (int q0 = 0; q0 < maxpart; q0 += 2 * LPR) {
+    uint4 en = entry_mask(n1, q0 + h2 < part_len, zero_row);
+    n1 = ep[0];
     __builtin_amdgcn_sched_barrier(0);  // keep the load two rounds ahead of its use
+    row_fma<LPR>(acc, lane_base + en.x, __uint_as_float(en.y));
+    row_fma<LPR>(acc, lane_base + en.z, __uint_as_float(en.w));
+    if (q0 + LPR >= maxpart) break;
+    en = entry_mask(n2, q0 + LPR + h2 < part_len, zero_row);
+    n2 = ep[EPR];
+    ep += 2 * EPR;
+    __builtin_amdgcn_sched_barrier(0);
     row_fma<LPR>(acc, lane_base + en.x, __uint_as_float(en.y));
     row_fma<LPR>(acc, lane_base + en.z, __uint_as_float(en.w));
   }

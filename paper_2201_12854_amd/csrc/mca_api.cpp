@@ -54,7 +54,8 @@ Layout layout_for(const mca_forward_desc& d) {
   L.row_max = off;     off = align256(off + 4 * tokens * size_t(d.heads));
   L.row_inv = off;     off = align256(off + 4 * tokens * size_t(d.heads));
   L.henc = off;        off = align256(off + helem * tokens * d_out);
-  L.list = off;        off = align256(off + 8 * tokens * size_t(mca::list_stride((int)d.d_in)));
+  L.list = off;
+  off = align256(off + 8 * (tokens * size_t(mca::list_stride((int)d.d_in)) + size_t(mca::list_tail_pad((int)d.d_in))));
   L.ucount = off;      off = align256(off + 4 * tokens);
   L.total = off;
   return L;

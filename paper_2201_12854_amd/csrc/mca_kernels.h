@@ -94,6 +94,10 @@ __host__ __device__ inline int gather_slice_cols(int d_in) { return d_in <= 1024
 // pad entry per parity part, rounded up to even so that every list starts 16-byte aligned
 // and entries can be read in pairs.
 __host__ __device__ inline int list_stride(int d_in) { return (d_in + 2) & ~1; }
+// Entries of slack after the last token's list: the gather kernel reads a few rounds past
+// the end of a list (those entries are masked), which for the last tokens runs past
+// their slots.
+__host__ __device__ inline int list_tail_pad(int d_in) { return 2 * list_stride(d_in) + 64; }
 // The two zero rows of the gather's LDS slice: even and odd row index.
 __host__ __device__ inline int zero_row_even(int d_in) { return d_in + (d_in & 1); }
 __host__ __device__ inline int zero_row_odd(int d_in) { return d_in + 1 - (d_in & 1); }
