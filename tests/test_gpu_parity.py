@@ -277,3 +277,30 @@ def test_eq6_draws_do_not_depend_on_x(dev):
     t1 = run_gpu(L1, dev, 0.4, 7, r_in=r_in, export_samples=True)
     t2 = run_gpu(L2, dev, 0.4, 7, r_in=r_in, export_samples=True)
     assert not np.array_equal(t1["idx"][..., :13], t2["idx"][..., :13])
+
+
+def test_sampled_d_in_1024_bf16(dev):
+    # d_in 1024: 8 tokens per sampler block, the gather's global-memory MFMA operand path
+    L = wl.make_layer(2, 64, 1024, 16, "bf16", data_seed=31, q_scale=3.0, token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=41)
+    assert n_tok > 0
+
+
+def test_bf16_width_not_multiple_of_8(dev):
+    # d_in 100: element-wise x loads in the gather, partial lane runs in the sampler
+    L = wl.make_layer(2, 48, 100, 4, "bf16", data_seed=32, lens=np.array([48, 29]), q_scale=3.0,
+                      token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=42)
+    assert n_tok > 0
+
+
+def test_eq6_max_sizes(dev):
+    # d_in 2048, 32 heads: 8 tokens per block around a 2048-row shared table
+    L = wl.make_layer(1, 24, 2048, 32, "bf16", data_seed=14, w_std=0.01)
+    _full_check(L, dev, 0.6, seed=(1 << 63) + 777, sampling="weight")
+
+
+def test_eq6_d_in_1024(dev):
+    L = wl.make_layer(2, 64, 1024, 16, "bf16", data_seed=33, q_scale=3.0, token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=43, sampling="weight")
+    assert n_tok > 0
