@@ -215,11 +215,24 @@ struct BlockCtx {
   int qt, h, b, tid, wave, lane, r16, g, n, d_out, len, q, ntl;
 };
 
+// One-dimensional grid of qtiles * H * B blocks. Consecutive blocks go to the 8 XCDs in
+// turn, each with its own L2; the query tiles of one (batch row, head) read the same K
+// (and H~) tile, so they are placed 8 block ids apart, on the same XCD, and the second
+// read hits its L2 (when H * B is a multiple of 8; otherwise in plain order).
 __device__ __forceinline__ BlockCtx block_ctx(const FwdParams& p) {
   BlockCtx c;
-  c.qt = blockIdx.x;
-  c.h = blockIdx.y;
-  c.b = blockIdx.z;
+  const int bid = blockIdx.x, Q = p.qtiles, P = p.H * p.B;
+  int pair;
+  if (P % 8 == 0) {
+    const int G = 8 * Q, w = bid % G;
+    pair = bid / G * 8 + w % 8;
+    c.qt = w / 8;
+  } else {
+    pair = bid / Q;
+    c.qt = bid % Q;
+  }
+  c.h = pair % p.H;
+  c.b = pair / p.H;
   c.tid = threadIdx.x;
   c.wave = c.tid >> 6;
   c.lane = c.tid & 63;
@@ -543,7 +556,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
 
 // Resident variants for padded lengths up to 256 keys (bf16) or 128 keys (fp32).
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
-  const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B), blk(kThreads);
+  const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
     if (nt <= 1) return launch_stage_kernel((k_scores_res<1, 1>), grid, blk, 0, s, p);
@@ -558,7 +571,7 @@ hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
 }
 
 hipError_t launch_attn_out(const FwdParams& p, hipStream_t s) {
-  const dim3 grid((p.n + kTile - 1) / kTile, p.H, p.B), blk(kThreads);
+  const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
     if (nt <= 1) return launch_stage_kernel((k_attn_res<1, 1>), grid, blk, 0, s, p);
