@@ -93,6 +93,14 @@ __device__ __forceinline__ int cnt_off(int d_in, bool table, int w) {
   return region_off(d_in, table, w) + (table ? 0 : round16(8 * d_in));
 }
 
+// LDS reads by 32-bit LDS address (offset into the workgroup's LDS).
+__device__ __forceinline__ uint32_t lds_addr_u64(const uint64_t* p) {
+  return (uint32_t)(uintptr_t)(__attribute__((address_space(3))) const uint64_t*)p;  // address-space cast
+}
+__device__ __forceinline__ uint64_t lds_read_u64(uint32_t addr) {
+  return *reinterpret_cast<__attribute__((address_space(3))) const uint64_t*>((uintptr_t)addr);
+}
+
 // W draws of one thread of the block's pool: draw d = d0 + 64 NW u (u < W) of the
 // concatenated draws of the block's tokens (token w owns [P_w, P_w + r_w)). Each is draw
 // k = d - P_w of its token: Philox4x32-10 with counter (k, j, b, 0), t = floor(u T / 2^64)
@@ -100,7 +108,7 @@ __device__ __forceinline__ int cnt_off(int d_in, bool table, int w) {
 // then the token's count of row s goes up by one.
 template <int W, int NW, bool TABLE>
 __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I, unsigned char* smem, int d0,
-                                           const int* Ps, int D, int nsteps) {
+                                           const int* Ps, int D) {
   const int d_in = p.d_in;
   uint64_t t[W];
   int lo[W], wt[W], kk[W];
@@ -118,23 +126,30 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
     t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), I.T[w]);  // in [0, T)
     Cw[u] = reinterpret_cast<const uint64_t*>(smem + c_off(d_in, TABLE, w));
   }
-  // fixed-step halving (ceil(log2 d_in) steps, no branches), step-major so that the W
-  // searches' LDS reads are in flight together; C[d_in-1] = T > t, so the answer is in
-  // range, and once lo == hi it stays put
-  int hi[W];
+  // s = #{i : C_i <= t} (C is non-decreasing and C[d_in-1] = T > t): a halving search
+  // whose length sequence is the same for every lane (uniform), on LDS byte addresses
+  // biased by -8 so that one add gives both the probe address and the candidate base.
+  // Per step: add, 64-bit LDS read, compare, select. Step-major over the W draws so that
+  // their LDS reads are in flight together.
+  uint32_t a[W], a0[W];
 #pragma unroll
   for (int u = 0; u < W; ++u) {
-    lo[u] = 0;
-    hi[u] = d_in - 1;
+    a0[u] = lds_addr_u64(Cw[u]);
+    a[u] = a0[u] - 8;  // address of C[base - 1], base = 0
   }
-  for (int st = 0; st < nsteps; ++st) {
+  for (int len = d_in; len > 1;) {
+    const int half = len >> 1;
 #pragma unroll
     for (int u = 0; u < W; ++u) {
-      const int mid = (lo[u] + hi[u]) >> 1;
-      const bool right = Cw[u][mid] <= t[u];
-      lo[u] = right ? mid + 1 : lo[u];
-      hi[u] = right ? hi[u] : mid;
+      const uint32_t cand = a[u] + 8 * half;  // C[base + half - 1]
+      a[u] = lds_read_u64(cand) <= t[u] ? cand : a[u];
     }
+    len -= half;
+  }
+#pragma unroll
+  for (int u = 0; u < W; ++u) {
+    const uint32_t at = a[u] + 8;  // C[base]
+    lo[u] = (int)((at - a0[u]) >> 3) + (lds_read_u64(at) <= t[u] ? 1 : 0);
   }
 #pragma unroll
   for (int u = 0; u < W; ++u) {
@@ -342,15 +357,14 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
 #pragma unroll
     for (int i = 0; i < NW; ++i) Ps[i] = __builtin_amdgcn_readfirstlane(I.P[i]);
     const int D = __builtin_amdgcn_readfirstlane(I.P[NW]);
-    const int nsteps = 32 - __clz(max(d_in - 1, 1));
     const int nper = (D + 64 * NW - 1) / (64 * NW);
     for (int u0 = 0; u0 < nper; u0 += 4) {
       const int d0 = threadIdx.x + u0 * 64 * NW;
       const int w = min(4, nper - u0);
-      if (w == 4) draw_batch<4, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
-      else if (w == 3) draw_batch<3, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
-      else if (w == 2) draw_batch<2, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
-      else draw_batch<1, NW, TABLE>(p, I, smem, d0, Ps, D, nsteps);
+      if (w == 4) draw_batch<4, NW, TABLE>(p, I, smem, d0, Ps, D);
+      else if (w == 3) draw_batch<3, NW, TABLE>(p, I, smem, d0, Ps, D);
+      else if (w == 2) draw_batch<2, NW, TABLE>(p, I, smem, d0, Ps, D);
+      else draw_batch<1, NW, TABLE>(p, I, smem, d0, Ps, D);
     }
   }
   __syncthreads();
