@@ -492,12 +492,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
     if (tid < 64) {  // one wave: offset of every key, longest lists first
       const int k = kNumKeys - 1 - tid;  // lane l holds key kNumKeys - 1 - l
       const int c = k >= 0 ? ctr[1 + k] : 0;
-      int incl = c;
-#pragma unroll
-      for (int off = 1; off < 64; off <<= 1) {
-        const int y = __shfl_up(incl, off, 64);
-        if (tid >= off) incl += y;
-      }
+      const int incl = (int)wave_inclusive_scan<uint32_t>((uint32_t)c);
       if (k >= 0) ctr[kCtrOff + k] = incl - c;
       if (tid == 63) ctr[kCtrOff + kNumKeys] = incl;
     }

@@ -45,15 +45,7 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
 }
 
-template <typename U>
-__device__ __forceinline__ U wave_inclusive_scan(U v, int lane) {
-#pragma unroll
-  for (int off = 1; off < kWave; off <<= 1) {
-    const U y = __shfl_up(v, off, kWave);
-    if (lane >= off) v += y;
-  }
-  return v;
-}
+
 
 template <int BF>
 __device__ __forceinline__ void write_zero4(const FwdParams& p, int64_t off) {
@@ -295,7 +287,7 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
         wv[k] = (k < nrows) ? (uint32_t)ldexpf(vv[k], shift) : 0u;
         lsum += wv[k];
       }
-      const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum, lane);
+      const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum);
       Tw = __shfl(incl, kWave - 1, kWave);  // = C[d_in - 1]
       uint64_t run = incl - lsum;
       if (full) {
@@ -395,7 +387,7 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
     }
   }
   const int cnt2 = ne | (no << 16);  // both counts <= d_in < 2^16
-  const int incl2 = wave_inclusive_scan<int>(cnt2, lane);
+  const int incl2 = (int)wave_inclusive_scan<uint32_t>((uint32_t)cnt2);
   const int tot2 = __builtin_amdgcn_readlane(incl2, kWave - 1);
   const int NE = tot2 & 0xffff, NO = tot2 >> 16, U = NE + NO;
   int pe = (incl2 - cnt2) & 0xffff;

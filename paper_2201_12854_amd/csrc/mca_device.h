@@ -90,6 +90,31 @@ __device__ __forceinline__ float row16_max(float v) {
 }
 
 // ---------------------------------------------------------------- wave reductions
+// Inclusive prefix sums over the 64 lanes with DPP (no LDS): shifts by 1, 2, 4, 8 within
+// rows of 16 lanes, then lane 15 of rows 0 and 2 into rows 1 and 3, then lane 31 into
+// rows 2 and 3. Lanes without a source, and rows left out, add 0.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t dpp_or_zero(uint32_t v) {
+  return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, CTRL, ROWS, 0xF, false);
+}
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint32_t scan_step(uint32_t v) { return v + dpp_or_zero<CTRL, ROWS>(v); }
+template <int CTRL, int ROWS>
+__device__ __forceinline__ uint64_t scan_step(uint64_t v) {
+  const uint32_t lo = dpp_or_zero<CTRL, ROWS>((uint32_t)v), hi = dpp_or_zero<CTRL, ROWS>((uint32_t)(v >> 32));
+  return v + (((uint64_t)hi << 32) | lo);
+}
+template <typename U>
+__device__ __forceinline__ U wave_inclusive_scan(U v) {
+  v = scan_step<0x111, 0xF>(v);  // row_shr:1
+  v = scan_step<0x112, 0xF>(v);  // row_shr:2
+  v = scan_step<0x114, 0xF>(v);  // row_shr:4
+  v = scan_step<0x118, 0xF>(v);  // row_shr:8
+  v = scan_step<0x142, 0xA>(v);  // row_bcast:15 into rows 1, 3
+  v = scan_step<0x143, 0xC>(v);  // row_bcast:31 into rows 2, 3
+  return v;
+}
+
 // Max over the 64 lanes (DPP within rows of 16, then the four row results), wave-uniform.
 __device__ __forceinline__ float wave_max(float v) {
   v = row16_max(v);
