@@ -174,6 +174,26 @@ __device__ __forceinline__ float prob(float lg, float row_max, float row_inv) {
 // max(a, b) of floats by compare and select (no NaN canonicalisation of the operands).
 __device__ __forceinline__ float max_sel(float a, float b) { return a > b ? a : b; }
 
+// Combination with lane ^ 16 and lane ^ 32 (the four 16-lane rows hold one query's partial
+// results for different keys) by the gfx950 lane swaps: swapping a value with itself gives
+// each lane the pair {own, partner}, in some order, in registers.
+__device__ __forceinline__ float pair16_max(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return max_sel(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair32_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return max_sel(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair16_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+__device__ __forceinline__ float pair32_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ int valid_len(const FwdParams& p, int b) {
   int len = p.seq_lens ? p.seq_lens[b] : p.n;
   return min(max(len, 1), p.n);
@@ -258,6 +278,25 @@ __device__ __forceinline__ float max_over_queries(float a) {
   return __uint_as_float(v);
 }
 
+// The same for a 4 x 4 block of values, step by step over all 16 so that the dependent
+// DPP operations of one value are separated by the others (no hazard waits).
+template <int CTRL>
+__device__ __forceinline__ void max_step16(uint32_t (&v)[16]) {
+#pragma unroll
+  for (int j = 0; j < 16; ++j) v[j] = max(v[j], (uint32_t)__builtin_amdgcn_mov_dpp((int)v[j], CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ void max_over_queries16(float (&a)[4][4]) {
+  uint32_t v[16];
+#pragma unroll
+  for (int j = 0; j < 16; ++j) v[j] = __float_as_uint(a[j >> 2][j & 3]);
+  max_step16<0xB1>(v);
+  max_step16<0x4E>(v);
+  max_step16<0x141>(v);
+  max_step16<0x140>(v);
+#pragma unroll
+  for (int j = 0; j < 16; ++j) a[j >> 2][j & 3] = __uint_as_float(v[j]);
+}
+
 // Writes Y rows of the wave's queries: y[cc][i] = Y[query 4 g + i][column 16 cc + l % 16].
 __device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, const f32x4_t y[4]) {
 #pragma unroll
@@ -312,8 +351,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         }
     }
   }
-  M = max_sel(M, __shfl_xor(M, 16, kWave));
-  M = max_sel(M, __shfl_xor(M, 32, kWave));
+  M = pair32_max(pair16_max(M));
   // e = exp2(logit - M), kept in acc for the column max (masked keys: exp2(-inf) = 0)
   float L = 0.f;
 #pragma unroll
@@ -329,8 +367,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         }
     }
   }
-  L += __shfl_xor(L, 16, kWave);
-  L += __shfl_xor(L, 32, kWave);
+  L = pair32_sum(pair16_sum(L));
   const float inv = 1.0f / L;
   if (c.g == 0 && c.q < c.n) {
     const int64_t o = ((int64_t)c.b * p.H + c.h) * c.n + c.q;
@@ -345,13 +382,18 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
+      float a[4][4];
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float a = max_over_queries(__fmul_rn(acc[kt][s][i], inv_q));
-          if (c.r16 == 0) cm[kt][c.wave][16 * s + 4 * c.g + i] = a;
-        }
+        for (int i = 0; i < 4; ++i) a[s][i] = __fmul_rn(acc[kt][s][i], inv_q);
+      max_over_queries16(a);  // 16 independent reductions, interleaved
+      if (c.r16 == 0) {
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) cm[kt][c.wave][16 * s + 4 * c.g + i] = a[s][i];
+      }
     }
   }
   lds_barrier();
@@ -398,16 +440,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
         acc[s][i] = lg;
         mx = max_sel(mx, lg);
       }
-    mx = max_sel(mx, __shfl_xor(mx, 16, kWave));
-    mx = max_sel(mx, __shfl_xor(mx, 32, kWave));
+    mx = pair32_max(pair16_max(mx));
     const float Mn = max_sel(M, mx);  // finite: key 0 of tile 0 is valid
     float sum = 0.f;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) sum += exp2_fast(__fsub_rn(acc[s][i], Mn));  // masked: exp2(-inf) = 0
-    sum += __shfl_xor(sum, 16, kWave);
-    sum += __shfl_xor(sum, 32, kWave);
+    sum = pair32_sum(pair16_sum(sum));
     L = (M == -INFINITY ? 0.f : __fmul_rn(L, exp2_fast(__fsub_rn(M, Mn)))) + sum;
     M = Mn;
   }
