@@ -19,12 +19,13 @@
 // reduce-scatter within the group (DPP) ends the item.
 //
 // Work distribution: the blocks of a slice split the tokens into contiguous ranges. A block
-// reads r and U of its range, puts the saturated tokens on one LDS list and sorts the
-// sampled tokens by list length (key floor(4 log2 U), longest first) with LDS atomics; its
-// waves then take work items from an LDS counter: groups of 16 saturated tokens first
-// (the heaviest items), then groups of sampled tokens of similar length, longest first,
-// so that the lanes of a wave and the waves of a block finish close together. No global
-// atomics; outputs do not depend on which wave computes them.
+// reads r and the list layout of its range, puts the saturated tokens on one LDS list and
+// sorts the sampled tokens by the longer part of their list (key floor(8 log2), longest
+// first) with LDS atomics; its waves then take work items from an LDS counter: groups of
+// 16 saturated tokens first (the heaviest items), then groups of sampled tokens of
+// similar length, longest first, so that the lanes of a wave and the waves of a block
+// finish close together. No global atomics; outputs do not depend on which wave computes
+// them.
 #include "mca_device.h"
 #include "mca_kernels.h"
 
@@ -234,18 +235,20 @@ __device__ __forceinline__ int wave_max_int(int v) {
 }
 
 constexpr int kChunk = kThreads;  // tokens classified per block pass (one per thread)
-constexpr int kNumKeys = 48;      // sort keys floor(4 log2 U) for 1 <= U < 4096
+constexpr int kNumKeys = 96;      // sort keys floor(8 log2 M) for 1 <= M < 4096
 
-// floor(4 log2 U) for 1 <= U < 4096 (U: list length): the octave and the next two bits.
-__device__ __forceinline__ int sort_key(int U) {
-  const int e = 31 - __clz(U);
-  const int f = e >= 2 ? (U >> (e - 2)) & 3 : (U << (2 - e)) & 3;
-  return 4 * e + f;
+// floor(8 log2 M) for 1 <= M < 4096 (M: the longer part of a token's list, which sets the
+// rounds its lane group runs): the octave and the next three bits.
+__device__ __forceinline__ int sort_key(int M) {
+  const int e = 31 - __clz(M);
+  const int f = e >= 3 ? (M >> (e - 3)) & 7 : (M << (3 - e)) & 7;
+  return 8 * e + f;
 }
 
-constexpr int kCtrOff = 64;        // counters: [0] saturated, [1 + key] key counts, [60] work
-                                   // queue, [kCtrOff + key] key offsets, [kCtrOff + kNumKeys] sampled
-constexpr int kNumCtr = 128;
+// counters: [0] saturated, [1] work queue, [2 + key] key counts, [kCtrOff + key] key
+// offsets, [kCtrOff + kNumKeys] sampled
+constexpr int kCtrOff = 128;
+constexpr int kNumCtr = 256;
 
 __host__ __device__ inline size_t gather_lds_bytes(int d_in, int wc, bool ldsb) {
   return 128                                 // alignment of the slice
@@ -466,8 +469,8 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
       if (r >= d_in) {                                                                         \
         satl[atomicAdd(ctr, 1)] = tid;                                                         \
       } else if (r > 0 && len > 0) {                                                           \
-        key = sort_key(len);                                                                   \
-        rank = atomicAdd(ctr + 1 + key, 1);                                                    \
+        key = sort_key(max(nepad, len - nepad));                                               \
+        rank = atomicAdd(ctr + 2 + key, 1);                                                    \
         ent = ((uint32_t)tid << kTokShift) | ((uint32_t)len << kLenShift) | (uint32_t)(nepad >> 1); \
       }                                                                                        \
     }                                                                                          \
@@ -489,11 +492,15 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
 
   for (int64_t t0 = t_begin;;) {
     __syncthreads();
-    if (tid < 64) {  // one wave: offset of every key, longest lists first
-      const int k = kNumKeys - 1 - tid;  // lane l holds key kNumKeys - 1 - l
-      const int c = k >= 0 ? ctr[1 + k] : 0;
-      const int incl = (int)wave_inclusive_scan<uint32_t>((uint32_t)c);
-      if (k >= 0) ctr[kCtrOff + k] = incl - c;
+    if (tid < 64) {  // one wave: offset of every key, longest first; lane l: keys 95 - 2l, 94 - 2l
+      static_assert(kNumKeys == 96, "two keys per lane of one wave");
+      const int kh = kNumKeys - 1 - 2 * tid, kl = kh - 1;
+      const int ch = kl >= 0 ? ctr[2 + kh] : 0, cl = kl >= 0 ? ctr[2 + kl] : 0;
+      const int incl = (int)wave_inclusive_scan<uint32_t>((uint32_t)(ch + cl));
+      if (kl >= 0) {
+        ctr[kCtrOff + kh] = incl - ch - cl;
+        ctr[kCtrOff + kl] = incl - cl;
+      }
       if (tid == 63) ctr[kCtrOff + kNumKeys] = incl;
     }
     __syncthreads();
@@ -507,7 +514,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
     // ---- work items from the block's queue
     for (;;) {
       int it = 0;
-      if (lane == 0) it = atomicAdd(ctr + 60, 1);
+      if (lane == 0) it = atomicAdd(ctr + 1, 1);
       it = __builtin_amdgcn_readfirstlane(it);
       if (it >= nitems) break;
       if (it < ngroups) {
