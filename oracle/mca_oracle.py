@@ -25,6 +25,16 @@ Mechanism" (AAAI-22), step by step, in the paper's notation:
   O8  saturated tokens (r_j capped at d_in) are encoded exactly
   O9  Y~ = A H~, per head                                      (Eq. 5 / "Y = AH" of Eq. 1)
 
+Local-window attention (Sec. "Longformer" and the document-classification
+experiments: a window of w = 256 keys around each token plus global attention
+for the first, CLS, token). With window w > 0, query i attends key j < len
+when |i - j| <= w / 2, or i = 0, or j = 0; every other score is masked before
+the softmax. The count rule follows the argument that leads to Eq. 9: the
+error of row i sums over the |S_i| keys it attends (Eq. 8), so the factor n
+that cancels that sum becomes |S_i|, and
+  sqrt(r_j) = max over heads and valid queries i of |S_i| A[i, j] / alpha,
+which is Eq. 9 when every row attends all n keys.
+
 Readings taken where the paper is silent or garbled (each is listed with its
 reason in the design notes of the repository):
 
@@ -47,6 +57,10 @@ reason in the design notes of the repository):
   row b; u = o0 | o1 << 32; t = floor(u * T / 2^64); s_k = min{i : C_i > t}
   with C the inclusive prefix sums of w.
 * A token whose weights are all zero (x_j = 0) is encoded as 0.
+* Local-window mode: w / 2 keys on each side (w even), the first token global
+  in both directions; m_j is the largest |S_i| A[i, j] (float64) and
+  t = m_j / alpha, r = ceil(t * t) clamped as above. With w = 0 (full
+  attention) the rule is the one printed, t = (n * m_j) / alpha.
 * Eq. 6 mode: v_i = fp32(rho_i * rho_i) (one IEEE float32 multiply of the
   float32 row norm), then the same fixed-point weights, prefix sums, random
   stream and inverse CDF. The table depends on W only, so it is built once and
@@ -120,14 +134,28 @@ def row_norms(W: np.ndarray) -> np.ndarray:
 
 
 # --------------------------------------------------------------------------- O2
-def attention_probs(Qbh: np.ndarray, Kbh: np.ndarray, valid: int) -> np.ndarray:
-    """A = softmax(a Q K^T) with a = 1/sqrt(d_head); keys at positions >= ``valid``
-    are padding and get probability 0. Rows of padded queries are computed
-    the same way (they are not used for the counts)."""
+def attended(q_pos, n_keys: int, valid: int, window: int = 0) -> np.ndarray:
+    """Boolean [len(q_pos), n_keys]: query at position q attends key j. Keys at or
+    past ``valid`` are padding. window = 0: every valid key (full attention);
+    window w > 0: |q - j| <= w / 2, plus the global first token (query 0 attends
+    every valid key and every query attends key 0)."""
+    q = np.asarray(q_pos, dtype=np.int64)[:, None]
+    j = np.arange(n_keys, dtype=np.int64)[None, :]
+    ok = np.broadcast_to(j < valid, (q.shape[0], n_keys))
+    if window > 0:
+        ok = ok & ((np.abs(q - j) <= window // 2) | (q == 0) | (j == 0))
+    return ok
+
+
+def attention_probs(Qbh: np.ndarray, Kbh: np.ndarray, valid: int, window: int = 0, q0: int = 0) -> np.ndarray:
+    """A = softmax(a Q K^T) with a = 1/sqrt(d_head), over the keys each query attends
+    (``attended``; the rows of Qbh are the queries at positions q0, q0 + 1, ...);
+    every other key gets probability 0. Rows of padded queries are computed the
+    same way (they are not used for the counts)."""
     Q = np.asarray(Qbh, dtype=np.float64)
     K = np.asarray(Kbh, dtype=np.float64)
     S = (Q @ K.T) * (1.0 / math.sqrt(Q.shape[1]))
-    S[:, valid:] = -np.inf
+    S[~attended(np.arange(q0, q0 + Q.shape[0]), K.shape[0], valid, window)] = -np.inf
     S = S - S.max(axis=1, keepdims=True)
     E = np.exp(S)
     return E / E.sum(axis=1, keepdims=True)
@@ -138,30 +166,38 @@ def head_slice(h: int) -> slice:
 
 
 # --------------------------------------------------------------------------- O3
-def column_max(Q, K, lens, heads) -> np.ndarray:
-    """m[b, j] = max over heads h and valid queries i of A_h[b, i, j]; 0 for padded keys."""
+def keys_attended(valid: int, window: int = 0) -> np.ndarray:
+    """|S_i| for the valid queries i < valid: how many keys each one attends."""
+    return attended(np.arange(valid), valid, valid, window).sum(axis=1)
+
+
+def column_max(Q, K, lens, heads, window: int = 0) -> np.ndarray:
+    """m[b, j] = max over heads h and valid queries i of A_h[b, i, j] (window 0), or of
+    |S_i| A_h[b, i, j] (window > 0, the count rule's per-row factor); 0 for padded keys."""
     B, n = Q.shape[0], Q.shape[1]
     m = np.zeros((B, n), dtype=np.float64)
     for b in range(B):
         L = int(lens[b])
+        scale = keys_attended(L, window).astype(np.float64)[:, None] if window > 0 else 1.0
         for h in range(heads):
-            A = attention_probs(Q[b, :, head_slice(h)], K[b, :, head_slice(h)], L)
-            m[b] = np.maximum(m[b], A[:L].max(axis=0))
+            A = attention_probs(Q[b, :, head_slice(h)], K[b, :, head_slice(h)], L, window)
+            m[b] = np.maximum(m[b], (scale * A[:L]).max(axis=0))
         m[b, L:] = 0.0
     return m
 
 
 # --------------------------------------------------------------------------- O4
-def sample_counts(m: np.ndarray, lens, alpha: float, d_in: int) -> np.ndarray:
+def sample_counts(m: np.ndarray, lens, alpha: float, d_in: int, window: int = 0) -> np.ndarray:
     """Eq. 9: sqrt(r_j) = n * m_j / alpha with n the valid length of the sequence;
     r_j = min(max(ceil(t*t), 1), d_in) with t = (n*m_j)/alpha in float64;
-    padded keys get 0."""
+    padded keys get 0. Window mode: m_j already carries the per-row factor
+    |S_i|, so t = m_j / alpha."""
     B, n = m.shape
     r = np.zeros((B, n), dtype=np.int64)
     for b in range(B):
         L = int(lens[b])
         for j in range(L):
-            t = (float(L) * float(m[b, j])) / float(alpha)
+            t = (float(m[b, j]) if window > 0 else float(L) * float(m[b, j])) / float(alpha)
             tt = t * t
             r[b, j] = min(max(math.ceil(tt), 1), d_in) if math.isfinite(tt) else d_in
     return r
@@ -256,7 +292,8 @@ def encode_token(x, W, rho, r: int, seed: int, b: int, j: int, *, sampling=SAMPL
 
 # --------------------------------------------------------------------------- forward
 def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_override=None,
-                rho=None, y_rows=None, want_samples=False, want_exact=False, sampling=SAMPLING_TOKEN):
+                rho=None, y_rows=None, want_samples=False, want_exact=False, sampling=SAMPLING_TOKEN,
+                window: int = 0):
     """Full MCA forward (O1-O9) for right-padded sequences.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W: [d_in, heads*64] (all float32
@@ -267,16 +304,19 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
     Returns a dict with rho, m, r, Htilde, Y (or Y at y_rows), and optionally
     samples (per token: indices, coefficients) and the exact Y* of Eq. 1.
     ``sampling`` selects the probability: SAMPLING_TOKEN (Eq. 4, per token) or
-    SAMPLING_WEIGHT (Eq. 6, one table per weight matrix).
+    SAMPLING_WEIGHT (Eq. 6, one table per weight matrix). ``window`` > 0 selects
+    local-window attention with a global first token (see ``attended``).
     """
+    if window < 0 or window % 2:
+        raise ValueError("window must be 0 (full attention) or a positive even number of keys")
     B, n, d_in = X.shape
     d_out = W.shape[1]
     lens = np.asarray(lens)
     if rho is None:
         rho = row_norms(W)
-    m = column_max(Q, K, lens, heads)
+    m = column_max(Q, K, lens, heads, window)
     if r_override is None:
-        r = sample_counts(m, lens, alpha, d_in)
+        r = sample_counts(m, lens, alpha, d_in, window)
     else:
         r = np.array(r_override, dtype=np.int64).reshape(B, n).copy()
         r = np.clip(r, 0, d_in)
@@ -303,7 +343,7 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
         for b in range(B):
             for h in range(heads):
                 cs = head_slice(h)
-                A = attention_probs(Q[b, :, cs], K[b, :, cs], int(lens[b]))
+                A = attention_probs(Q[b, :, cs], K[b, :, cs], int(lens[b]), window)
                 Y[b, :, cs] = A @ Ht[b, :, cs]
                 if want_exact:
                     Yx[b, :, cs] = A @ Hx[b, :, cs]
@@ -316,7 +356,7 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
         for t, (b, i) in enumerate(rows):
             for h in range(heads):
                 cs = head_slice(h)
-                A = attention_probs(Q[b, i:i + 1, cs], K[b, :, cs], int(lens[b]))
+                A = attention_probs(Q[b, i:i + 1, cs], K[b, :, cs], int(lens[b]), window, q0=i)
                 Y[t, cs] = A[0] @ Ht[b, :, cs]
         out["Y_rows"] = Y
     if want_samples:
@@ -324,7 +364,7 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
     return out
 
 
-def exact_forward(Q, K, X, W, lens, heads: int) -> np.ndarray:
+def exact_forward(Q, K, X, W, lens, heads: int, window: int = 0) -> np.ndarray:
     """Eq. 1: Y[i] = sum_j A[i, j] X[j] W, per head, in float64."""
     B, n, _ = X.shape
     H = np.asarray(X, np.float64) @ np.asarray(W, np.float64)
@@ -332,7 +372,7 @@ def exact_forward(Q, K, X, W, lens, heads: int) -> np.ndarray:
     for b in range(B):
         for h in range(heads):
             cs = head_slice(h)
-            A = attention_probs(Q[b, :, cs], K[b, :, cs], int(lens[b]))
+            A = attention_probs(Q[b, :, cs], K[b, :, cs], int(lens[b]), window)
             Y[b, :, cs] = A @ H[b, :, cs]
     return Y
 

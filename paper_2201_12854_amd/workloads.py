@@ -64,6 +64,7 @@ class Layer:
     seed: int
     alphas: tuple = ()
     meta: dict = field(default_factory=dict)
+    window: int = 0  # 0: full attention; w > 0: local window of w keys, global first token
 
     @property
     def batch(self) -> int:
@@ -89,7 +90,7 @@ class Layer:
         idx = np.asarray(batches)
         return Layer(self.name + f"[{len(idx)}]", self.dtype, self.Q[idx], self.K[idx],
                      self.X[idx], self.Wv, self.lens[idx], self.heads, self.alpha,
-                     self.seed, self.alphas, dict(self.meta))
+                     self.seed, self.alphas, dict(self.meta), self.window)
 
 
 def make_layer(batch: int, seq: int, d_in: int, heads: int, dtype: str = "f32", *,
@@ -97,7 +98,7 @@ def make_layer(batch: int, seq: int, d_in: int, heads: int, dtype: str = "f32", 
                token_scale_sigma: float = 0.0, lens: Optional[np.ndarray] = None,
                ragged_lens: Optional[tuple] = None, salient_keys: int = 0,
                salient_bump: float = 6.0, w_std: float = 0.02, name: str = "custom",
-               alphas: tuple = ()) -> Layer:
+               alphas: tuple = (), window: int = 0) -> Layer:
     if dtype not in ("f32", "bf16"):
         raise ValueError(dtype)
     rng = np.random.default_rng(data_seed)
@@ -138,7 +139,7 @@ def make_layer(batch: int, seq: int, d_in: int, heads: int, dtype: str = "f32", 
         Q, K, X, Wv = (round_to_bf16(t) for t in (Q, K, X, Wv))
     return Layer(name, dtype, np.ascontiguousarray(Q), np.ascontiguousarray(K),
                  np.ascontiguousarray(X), np.ascontiguousarray(Wv), lens, heads,
-                 float(alpha), int(seed), tuple(alphas) or (float(alpha),))
+                 float(alpha), int(seed), tuple(alphas) or (float(alpha),), {}, int(window))
 
 
 # The five BERT-shaped workloads. Error-bound settings: loose 1.0, default 0.4,
@@ -179,10 +180,42 @@ def long_seq_bf16() -> Layer:
                       salient_bump=6.0, name="long_bf16_b4_s4096_salient32")
 
 
+# Document-classification stand-ins for the local-window (Longformer) experiments: a
+# window of 256 keys with a global first token, BERT-base width, documents whose lengths
+# are uniform in [mean / 2, 3 mean / 2] around the paper's average lengths of 167 (AAPD),
+# 300 (IMDB) and 705 (HND) tokens, padded to the longest possible.
+LONGFORMER_WINDOW = 256
+
+
+def _longformer(batch: int, mean_len: int, data_seed: int, name: str) -> Layer:
+    lo, hi = (mean_len + 1) // 2, (3 * mean_len) // 2
+    return make_layer(batch, hi, 768, 12, "bf16", data_seed=data_seed, token_scale_sigma=0.5,
+                      ragged_lens=(lo, hi), name=name, window=LONGFORMER_WINDOW,
+                      alphas=(ALPHA_DEFAULT, ALPHA_LOOSE, ALPHA_TIGHT))
+
+
+def longformer_aapd_bf16() -> Layer:
+    """Local-window layer, bf16: batch 32, lengths around 167 (padded 250), window 256."""
+    return _longformer(32, 167, 1006, "longformer_bf16_b32_len167_w256")
+
+
+def longformer_imdb_bf16() -> Layer:
+    """Local-window layer, bf16: batch 16, lengths around 300 (padded 450), window 256."""
+    return _longformer(16, 300, 1007, "longformer_bf16_b16_len300_w256")
+
+
+def longformer_hnd_bf16() -> Layer:
+    """Local-window layer, bf16: batch 8, lengths around 705 (padded 1057), window 256."""
+    return _longformer(8, 705, 1008, "longformer_bf16_b8_len705_w256")
+
+
 WORKLOADS = {
     "bert_base_f32": bert_base_f32,
     "bert_base_bf16": bert_base_bf16,
     "bert_large_sharp_bf16": bert_large_sharp_bf16,
     "bert_base_padded_bf16": bert_base_padded_bf16,
     "long_seq_bf16": long_seq_bf16,
+    "longformer_aapd_bf16": longformer_aapd_bf16,
+    "longformer_imdb_bf16": longformer_imdb_bf16,
+    "longformer_hnd_bf16": longformer_hnd_bf16,
 }
