@@ -94,6 +94,7 @@ typedef struct mca_forward_desc {
   const int32_t* r_in;
   /* Optional device outputs (NULL = not written):
      colmax_out      [B*n]       float32 m_j = max over heads and valid queries of A[:, j]
+                                 (local window: of |S_i| A[i, j])
      sample_idx_out  [B*n*d_in]  int32: index s_k of draw k of token (b, j) at
                                  (b*n+j)*d_in + k, for k < r_j and 0 < r_j < d_in
      sample_coef_out [B*n*d_in]  float32 x_{s_k} T / (r_j w_{s_k}), same layout
@@ -105,6 +106,12 @@ typedef struct mca_forward_desc {
   /* mca_profiler handle from mca_profiler_create, or NULL. When set, the call records
      a pair of HIP events around every stage launch. */
   void* profiler;
+  /* Attention pattern. 0: full attention. w > 0 (even): local window of w keys with a
+     global first token (Sec. "Longformer": window 256, global attention for CLS):
+     query i attends key j < len when |i - j| <= w / 2, or i = 0, or j = 0. The count
+     rule then uses each query's key count |S_i| in place of n:
+     m_j = max over heads and valid queries i of |S_i| A[i, j], t = m_j / alpha. */
+  int64_t window;
 } mca_forward_desc;
 
 /*
@@ -147,10 +154,12 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
 
 /*
  * One MCA forward pass (Eq. 5, with counts from Eq. 9):
- *   A_h   = softmax(Q_h K_h^T / 8), keys >= seq_lens[b] masked
- *   m_j   = max over heads h and valid queries i of A_h[i, j]
- *   r_j   = min(max(ceil(t*t), 1), d_in), t = (len_b * m_j) / alpha in float64; 0 for
- *           padded keys. r_j = d_in marks a saturated token.
+ *   A_h   = softmax(Q_h K_h^T / 8), keys >= seq_lens[b] masked (and, with a local
+ *           window, the keys outside each query's window)
+ *   m_j   = max over heads h and valid queries i of A_h[i, j] (window: of |S_i| A_h[i, j])
+ *   r_j   = min(max(ceil(t*t), 1), d_in), t = (len_b * m_j) / alpha in float64
+ *           (window: t = m_j / alpha); 0 for padded keys. r_j = d_in marks a saturated
+ *           token.
  *   H~[j] = (1/r_j) sum_k x_{j,s_k} W_v[s_k] / p(s_k)   for 0 < r_j < d_in
  *           with p(i) = w_i / T the 32-bit fixed-point form of |x_ji| * rownorm[i]
  *           (Eq. 4 for the product x_j W_v; MCA_SAMPLING_TOKEN) or of rownorm[i]^2
@@ -166,7 +175,7 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  * `workspace` must hold at least mca_workspace_size bytes; its contents on entry do not
  * matter and are overwritten.
  * Errors: MCA_ERR_INVALID_ARGUMENT (null required pointer, size < 1, non-finite or
- * non-positive alpha, unknown sampling mode, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
+ * non-positive alpha, unknown sampling mode, odd or negative window, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
  * != 64, d_out not a multiple of 256 or > 2048, d_in > 2048), MCA_ERR_WORKSPACE_TOO_SMALL,
  * MCA_ERR_HIP.
  */

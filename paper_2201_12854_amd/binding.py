@@ -53,6 +53,7 @@ class ForwardDesc(ctypes.Structure):
         ("sample_coef_out", ctypes.c_void_p),
         ("encoded_out", ctypes.c_void_p),
         ("profiler", ctypes.c_void_p),
+        ("window", ctypes.c_int64),
     ]
 
 
@@ -131,7 +132,7 @@ def _stream_handle(device) -> int:
 
 def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None, r_in=None,
               colmax_out=None, sample_idx_out=None, sample_coef_out=None, encoded_out=None,
-              profiler=None, sampling=0) -> ForwardDesc:
+              profiler=None, sampling=0, window=0) -> ForwardDesc:
     d = ForwardDesc()
     d.batch, d.seq, d.heads, d.d_head, d.d_in = batch, seq, heads, 64, d_in
     d.dtype, d.sampling = dtype_code, sampling
@@ -140,6 +141,7 @@ def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None
     d.colmax_out, d.sample_idx_out = _ptr(colmax_out), _ptr(sample_idx_out)
     d.sample_coef_out, d.encoded_out = _ptr(sample_coef_out), _ptr(encoded_out)
     d.profiler = None if profiler is None else profiler.handle
+    d.window = int(window)
     return d
 
 
@@ -189,7 +191,8 @@ class ForwardResult:
 
 def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int,
                       seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
-                      workspace=None, out=None, profiler=None, sampling: str = "token") -> ForwardResult:
+                      workspace=None, out=None, profiler=None, sampling: str = "token",
+                      window: int = 0) -> ForwardResult:
     """One MCA forward pass through libmca on the current HIP stream.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
@@ -198,7 +201,9 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     rule. ``export`` also returns the column max and H~ (float32); ``export_samples``
     the per-draw indices and coefficients ([B, n, d_in], first r_j entries valid).
     ``out`` may pass preallocated (Y, r). ``sampling``: "token" (Eq. 4, per token) or
-    "weight" (Eq. 6, the paper's input-independent probability).
+    "weight" (Eq. 6, the paper's input-independent probability). ``window``: 0 for full
+    attention, or an even local window (keys within window / 2 of each query, plus a
+    global first token).
     """
     import torch
 
@@ -229,7 +234,7 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     desc = make_desc(B, n, heads, d_in, dt, alpha, seed, seq_lens=seq_lens, r_in=r_in,
                      colmax_out=res.colmax, sample_idx_out=res.sample_idx,
                      sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler,
-                     sampling=_sampling_code(sampling))
+                     sampling=_sampling_code(sampling), window=window)
     ws_bytes = workspace_size(desc)
     if workspace is None or workspace.numel() < ws_bytes:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
@@ -278,7 +283,7 @@ class ForwardPlan:
     stream), so that ``run()`` is a single C call: for timing loops and serving."""
 
     def __init__(self, Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
-                 r_in=None, profiler=None, sampling: str = "token"):
+                 r_in=None, profiler=None, sampling: str = "token", window: int = 0):
         import torch
 
         lib = load_library()
@@ -287,7 +292,7 @@ class ForwardPlan:
         dev = X.device
         self._keep = (Q, K, X, W_v, prepared, seq_lens, r_in)
         self.desc = make_desc(B, n, heads, d_in, _dtype_code(X), alpha, seed, seq_lens=seq_lens, r_in=r_in,
-                              profiler=profiler, sampling=_sampling_code(sampling))
+                              profiler=profiler, sampling=_sampling_code(sampling), window=window)
         ws = workspace_size(self.desc)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
         self.Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)

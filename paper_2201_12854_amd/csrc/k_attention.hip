@@ -21,6 +21,13 @@
 //   streaming (longer sequences): tiles are double buffered in LDS with the next tile
 //     prefetched into registers; the score pass sweeps twice (online statistics, then
 //     probabilities).
+// Local-window attention (Sec. "Longformer": a window of w keys around each token and a
+// global first token): query q attends key k < len when |q - k| <= w / 2, or q = 0, or
+// k = 0; the other scores are masked like padded keys. The column max is then taken of
+// |S_q| A[q, k], |S_q| the number of keys query q attends (the count rule's per-row factor
+// n of Eq. 9), and the streaming variants visit only the key tiles a query tile's window
+// reaches, plus tile 0 (all tiles for the tile holding query 0).
+//
 // Rows past the padded length are read from the last row instead of being zero-filled:
 // their scores are masked and their probabilities are exactly 0. Tile loads are
 // unconditional (a tile index past the last valid tile is clamped to it), which keeps the
@@ -233,6 +240,8 @@ __device__ __forceinline__ void pv_tile(f32x4_t y[4], const f32x4_t acc[4], cons
 
 struct BlockCtx {
   int qt, h, b, tid, wave, lane, r16, g, n, d_out, len, q, ntl;
+  int half;       // local window: keys within half of the query (0: full attention)
+  int tlo, thi;   // key tiles visited: 0, then tlo .. thi (tlo >= 1)
 };
 
 // One-dimensional grid of qtiles * H * B blocks. Consecutive blocks go to the 8 XCDs in
@@ -263,7 +272,44 @@ __device__ __forceinline__ BlockCtx block_ctx(const FwdParams& p) {
   c.len = valid_len(p, c.b);
   c.q = c.qt * kTile + c.wave * 16 + c.r16;
   c.ntl = (c.len + kTile - 1) / kTile;  // tiles past the valid length are all masked
+  c.half = p.band_half;
+  c.tlo = 1;
+  c.thi = c.ntl - 1;
+  if (c.half > 0 && c.qt > 0) {  // the window of queries q0 .. q0 + 63
+    const int q0 = c.qt * kTile;
+    c.tlo = max(1, max(q0 - c.half, 0) / kTile);
+    c.thi = min(c.ntl - 1, (q0 + kTile - 1 + c.half) / kTile);
+  }
   return c;
+}
+
+// Key tiles a block visits, in order: tile 0, then tlo .. thi.
+__device__ __forceinline__ int tile_count(const BlockCtx& c) { return 1 + max(0, c.thi - c.tlo + 1); }
+__device__ __forceinline__ int tile_at(const BlockCtx& c, int idx) { return idx == 0 ? 0 : c.tlo + idx - 1; }
+
+// Key e of tile kt (e = 16 s + 4 g + i, lim = len - 64 kt) is attended by the lane's query.
+template <bool BAND>
+__device__ __forceinline__ bool key_ok(const BlockCtx& c, int kt, int lim, int e) {
+  if constexpr (BAND) {
+    const int k = kt * kTile + e;
+    return e < lim && (c.q == 0 || k == 0 || abs(c.q - k) <= c.half);
+  } else {
+    return lim >= kTile || e < lim;
+  }
+}
+
+// Weight of the lane's query in the column max: 1 (full attention) or |S_q| (local
+// window); 0 for padded queries.
+template <bool BAND>
+__device__ __forceinline__ float query_weight(const BlockCtx& c) {
+  if (c.q >= c.len) return 0.f;
+  if constexpr (BAND) {
+    if (c.q == 0) return (float)c.len;
+    const int lo = max(0, c.q - c.half), hi = min(c.len - 1, c.q + c.half);
+    return (float)(hi - lo + 1 + (lo > 0 ? 1 : 0));
+  } else {
+    return 1.f;
+  }
 }
 
 // Max over the wave's 16 queries (the 16 lanes of a row, same l / 16) of a probability.
@@ -312,7 +358,7 @@ __device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, c
 
 // ------------------------------------------------------------------ score pass
 // Resident variant: all ntl <= NT tiles in LDS and all scores in registers.
-template <int BF, int NT>
+template <int BF, int NT, bool BAND>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_res(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
@@ -346,7 +392,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float lg = logit(acc[kt][s][i]);
-          acc[kt][s][i] = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? lg : -INFINITY;
+          acc[kt][s][i] = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? lg : -INFINITY;
           M = max_sel(M, acc[kt][s][i]);
         }
     }
@@ -377,7 +423,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 
   // column max of the valid queries, every tile in its own LDS slot (one barrier).
   // probability = e * (1/L), bitwise the value prob() gives in the output pass; queries
-  // past the valid length contribute 0
+  // past the valid length contribute 0; local window: times |S_q|
+  const float wq = query_weight<BAND>(c);
   const float inv_q = c.q < c.len ? inv : 0.f;
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
@@ -386,7 +433,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) a[s][i] = __fmul_rn(acc[kt][s][i], inv_q);
+        for (int i = 0; i < 4; ++i)
+          a[s][i] = BAND ? __fmul_rn(__fmul_rn(acc[kt][s][i], inv), wq) : __fmul_rn(acc[kt][s][i], inv_q);
       max_over_queries16(a);  // 16 independent reductions, interleaved
       if (c.r16 == 0) {
 #pragma unroll
@@ -407,7 +455,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 }
 
 // Streaming variant: tiles double buffered, next tile prefetched; two sweeps.
-template <int BF>
+template <int BF, bool BAND>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
@@ -419,15 +467,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   QFrag<BF> qf;
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
 
-  // Sweep 1: online row max and row sum of exp over the valid keys.
+  // Sweep 1: online row max and row sum of exp over the attended keys.
   float M = -INFINITY, L = 0.f;
+  const int nvis = tile_count(c);
   TileRegs kr;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  for (int kt = 0; kt < c.ntl; ++kt) {
-    T* buf = Ks[kt & 1];
+  for (int t = 0; t < nvis; ++t) {
+    const int kt = tile_at(c, t);
+    T* buf = Ks[t & 1];
     tile_store<BF>(kr, buf, c.tid);
     lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
+    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
     f32x4_t acc[4];
     score_tile(acc, buf, qf, c.r16, c.g);
     float mx = -INFINITY;
@@ -436,12 +486,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float lg = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? logit(acc[s][i]) : -INFINITY;
+        const float lg = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? logit(acc[s][i]) : -INFINITY;
         acc[s][i] = lg;
         mx = max_sel(mx, lg);
       }
     mx = pair32_max(pair16_max(mx));
-    const float Mn = max_sel(M, mx);  // finite: key 0 of tile 0 is valid
+    const float Mn = max_sel(M, mx);  // finite: key 0 of tile 0 is attended by every query
     float sum = 0.f;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
@@ -459,18 +509,26 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   }
 
   // Sweep 2: probabilities and the per-key column max of this block's valid queries.
-  // Tile kt uses K buffer kt & 1 and column-max slot kt & 1; the barrier after its LDS
-  // store also orders the reads of tile kt - 2's slot before this tile's writes.
+  // The t-th visited tile uses K buffer t & 1 and column-max slot t & 1; the barrier after
+  // its LDS store also orders the reads of tile t - 2's slot before this tile's writes.
   lds_barrier();  // sweep 1 is done with both K buffers
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
+  if (BAND) {  // valid keys of the tiles outside the window get a zero partial
+    for (int key = kTile + c.tid; key < c.len; key += kThreads) {
+      const int kt = key / kTile;
+      if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
+    }
+  }
+  const float wq = query_weight<BAND>(c);
   const float inv_q = c.q < c.len ? inv : 0.f;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  for (int kt = 0; kt < c.ntl; ++kt) {
-    T* buf = Ks[kt & 1];
-    float (*cmk)[kTile] = cm[kt & 1];
+  for (int t = 0; t < nvis; ++t) {
+    const int kt = tile_at(c, t);
+    T* buf = Ks[t & 1];
+    float (*cmk)[kTile] = cm[t & 1];
     tile_store<BF>(kr, buf, c.tid);
     lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
+    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
     f32x4_t acc[4];
     score_tile(acc, buf, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
@@ -478,8 +536,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bool kvalid = lim >= kTile || 16 * s + 4 * c.g + i < lim;
-        const float a = max_over_queries(kvalid ? prob(logit(acc[s][i]), M, inv_q) : 0.f);
+        const bool kvalid = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i);
+        const float pr = BAND ? __fmul_rn(prob(logit(acc[s][i]), M, inv), wq) : prob(logit(acc[s][i]), M, inv_q);
+        const float a = max_over_queries(kvalid ? pr : 0.f);
         if (c.r16 == 0) cmk[c.wave][16 * s + 4 * c.g + i] = a;
       }
     lds_barrier();
@@ -493,7 +552,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 }
 
 // ------------------------------------------------------------------ Y = A H~
-template <int BF, int NT>
+template <int BF, int NT, bool BAND>
 __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
@@ -538,7 +597,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float pr = prob(logit(acc[s][i]), M, inv);
-          acc[s][i] = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? pr : 0.f;
+          acc[s][i] = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? pr : 0.f;
         }
       pv_tile(y, acc, Vs[kt], c.r16, c.g);
     }
@@ -546,7 +605,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
   store_y(p, c, y);
 }
 
-template <int BF>
+template <int BF, bool BAND>
 __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
@@ -569,14 +628,17 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   f32x4_t y[4];
 #pragma unroll
   for (int cc = 0; cc < 4; ++cc) y[cc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  for (int kt = 0; kt < c.ntl; ++kt) {
-    T* kb = Ks[kt & 1];
-    T* vb = Vs[kt & 1];
+  const int nvis = tile_count(c);
+  for (int t = 0; t < nvis; ++t) {
+    const int kt = tile_at(c, t);
+    T* kb = Ks[t & 1];
+    T* vb = Vs[t & 1];
     tile_store<BF>(kr, kb, c.tid);
     tile_store_v<BF>(vr, vb, c.tid);
     lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
-    vr = tile_load<BF>(Vb, c.d_out, min(kt + 1, c.ntl - 1) * kTile, c.n, c.tid);
+    const int next = tile_at(c, min(t + 1, nvis - 1)) * kTile;
+    kr = tile_load<BF>(Kb, c.d_out, next, c.n, c.tid);
+    vr = tile_load<BF>(Vb, c.d_out, next, c.n, c.tid);
     f32x4_t acc[4];
     score_tile(acc, kb, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
@@ -585,44 +647,53 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pr = prob(logit(acc[s][i]), M, inv);
-        acc[s][i] = (lim >= kTile || 16 * s + 4 * c.g + i < lim) ? pr : 0.f;
+        acc[s][i] = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? pr : 0.f;
       }
     pv_tile(y, acc, vb, c.r16, c.g);
   }
   store_y(p, c, y);
 }
 
-}  // namespace
-
 // Resident variants for padded lengths up to 256 keys (bf16) or 128 keys (fp32).
-hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
+template <bool BAND>
+hipError_t launch_scores_band(const FwdParams& p, hipStream_t s) {
   const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
-    if (nt <= 1) return launch_stage_kernel((k_scores_res<1, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2>), grid, blk, 0, s, p);
-    else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4>), grid, blk, 0, s, p);
-    else return launch_stage_kernel(k_scores_stream<1>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_scores_res<1, 1, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4, BAND>), grid, blk, 0, s, p);
+    else return launch_stage_kernel((k_scores_stream<1, BAND>), grid, blk, 0, s, p);
   } else {
-    if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2>), grid, blk, 0, s, p);
-    else return launch_stage_kernel(k_scores_stream<0>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2, BAND>), grid, blk, 0, s, p);
+    else return launch_stage_kernel((k_scores_stream<0, BAND>), grid, blk, 0, s, p);
   }
 }
 
-hipError_t launch_attn_out(const FwdParams& p, hipStream_t s) {
+template <bool BAND>
+hipError_t launch_attn_band(const FwdParams& p, hipStream_t s) {
   const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
-    if (nt <= 1) return launch_stage_kernel((k_attn_res<1, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) return launch_stage_kernel((k_attn_res<1, 2>), grid, blk, 0, s, p);
-    else if (nt <= 4) return launch_stage_kernel((k_attn_res<1, 4>), grid, blk, 0, s, p);
-    else return launch_stage_kernel(k_attn_stream<1>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_attn_res<1, 1, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_attn_res<1, 2, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 4) return launch_stage_kernel((k_attn_res<1, 4, BAND>), grid, blk, 0, s, p);
+    else return launch_stage_kernel((k_attn_stream<1, BAND>), grid, blk, 0, s, p);
   } else {
-    if (nt <= 1) return launch_stage_kernel((k_attn_res<0, 1>), grid, blk, 0, s, p);
-    else if (nt <= 2) return launch_stage_kernel((k_attn_res<0, 2>), grid, blk, 0, s, p);
-    else return launch_stage_kernel(k_attn_stream<0>, grid, blk, 0, s, p);
+    if (nt <= 1) return launch_stage_kernel((k_attn_res<0, 1, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 2) return launch_stage_kernel((k_attn_res<0, 2, BAND>), grid, blk, 0, s, p);
+    else return launch_stage_kernel((k_attn_stream<0, BAND>), grid, blk, 0, s, p);
   }
+}
+}  // namespace
+
+hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s) {
+  return p.band_half > 0 ? launch_scores_band<true>(p, s) : launch_scores_band<false>(p, s);
+}
+
+hipError_t launch_attn_out(const FwdParams& p, hipStream_t s) {
+  return p.band_half > 0 ? launch_attn_band<true>(p, s) : launch_attn_band<false>(p, s);
 }
 
 }  // namespace mca

@@ -4,7 +4,9 @@
 //      pass, and the sample count of Eq. 9 (Sec. "Determining Sample Size from
 //      Attention") in float64: t = (len_b * m_j) / alpha, r_j = ceil(t * t) clamped to
 //      [1, d_in]; padded keys get 0. r_j = d_in marks a saturated token, encoded exactly
-//      by the gather kernel's MFMA path (cost of d_in samples, no error).
+//      by the gather kernel's MFMA path (cost of d_in samples, no error). Under local-
+//      window attention the partials hold |S_q| A[q, j] (each query's key count in place
+//      of n) and t = m_j / alpha.
 //   2. sampling weights of Eq. 4 for the product x_j W_v: v_i = |x_ji| * rho_i in one
 //      float32 multiply, quantised to 32-bit fixed point aligned to the largest v_i,
 //      w_i = floor(v_i 2^(32-e)); inclusive prefix sums C (uint64) by a wavefront scan
@@ -256,7 +258,9 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   } else if (p.r_in) {
     r = min(max(rin, 0), d_in);
   } else {
-    const double t = ((double)len * (double)m) / p.alpha;
+    // full attention: t = (len m) / alpha (Eq. 9); local window: m already carries each
+    // query's key count |S_q| (the per-row n of Eq. 9), so t = m / alpha
+    const double t = (p.band_half > 0 ? (double)m : (double)len * (double)m) / p.alpha;
     const double tt = t * t;
     r = (tt >= (double)d_in) ? d_in : max((int)ceil(tt), 1);
   }

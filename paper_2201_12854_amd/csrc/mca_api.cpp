@@ -69,6 +69,9 @@ mca_status check_desc(const mca_forward_desc* d) {
     return fail(MCA_ERR_INVALID_ARGUMENT, "sampling %d is not MCA_SAMPLING_TOKEN or MCA_SAMPLING_WEIGHT", d->sampling);
   if (d->dtype != MCA_F32 && d->dtype != MCA_BF16)
     return fail(MCA_ERR_INVALID_ARGUMENT, "dtype %d is not MCA_F32 or MCA_BF16", d->dtype);
+  if (d->window < 0 || d->window % 2 != 0 || d->window > (int64_t(1) << 25))
+    return fail(MCA_ERR_INVALID_ARGUMENT, "window must be 0 or an even number of keys in 2..2^25 (got %lld)",
+                (long long)d->window);
   if (!std::isfinite(d->alpha) || !(d->alpha > 0.0))
     return fail(MCA_ERR_INVALID_ARGUMENT, "alpha must be finite and > 0 (got %g)", d->alpha);
   if (d->seq > (int64_t(1) << 24) || d->batch > (int64_t(1) << 24) || d->heads > 1024 ||
@@ -221,6 +224,7 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.d_out = (int)(desc->heads * 64);
   p.bf16 = desc->dtype == MCA_BF16;
   p.weight_sampling = desc->sampling == MCA_SAMPLING_WEIGHT;
+  p.band_half = (int)(desc->window / 2);
   p.qtiles = L.qtiles;
   p.nparts = L.nparts;
   p.din_pad = (int)mca::prepared_din_pad(desc->d_in);

@@ -37,6 +37,8 @@ struct FwdParams {
   int B, n, H, d_in, d_out;
   int bf16;     // 0: float32 inputs, 1: bfloat16 inputs
   int weight_sampling;  // 0: Eq. 4, p_ji ~ |x_ji| rho_i; 1: Eq. 6, p_i ~ rho_i^2
+  int band_half;        // local window: query q attends keys within band_half of q and the
+                        // first token attends and is attended by all (0: full attention)
   int qtiles;   // query tiles per sequence = ceil(n / kQueryTile)
   int nparts;   // column-max partials per token = H * qtiles
   int din_pad;  // row length of W_v^T

@@ -33,7 +33,7 @@ def to_device(L, dev):
 
 
 def run_gpu(L, dev, alpha, seed, *, r_in=None, export=True, export_samples=False, tensors=None, prep=None,
-            sampling="token"):
+            sampling="token", window=None):
     import torch
 
     import paper_2201_12854_amd as mca
@@ -44,7 +44,7 @@ def run_gpu(L, dev, alpha, seed, *, r_in=None, export=True, export_samples=False
     rin = None if r_in is None else torch.from_numpy(np.ascontiguousarray(r_in, dtype=np.int32)).to(dev)
     out = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], prep, alpha, seed, heads=L.heads,
                                 seq_lens=t["lens"], r_in=rin, export=export, export_samples=export_samples,
-                                sampling=sampling)
+                                sampling=sampling, window=L.window if window is None else window)
     torch.cuda.synchronize()
     res = {"Y": out.Y.cpu().numpy(), "r": out.r.cpu().numpy(), "rho": mca.rownorm(prep, L.d_in).cpu().numpy()}
     if export:
@@ -73,14 +73,15 @@ def row_rel_err(Y, Yref, lens):
     return worst
 
 
-def ambiguous_tokens(m_ref, lens, alpha, d_in, tol=TOL_M):
+def ambiguous_tokens(m_ref, lens, alpha, d_in, tol=TOL_M, window=0):
     """Tokens whose count could change when m moves by a relative `tol`: the float64
-    rule's t^2 range [t^2 (1-tol)^2, t^2 (1+tol)^2] straddles an integer below d_in."""
+    rule's t^2 range [t^2 (1-tol)^2, t^2 (1+tol)^2] straddles an integer below d_in.
+    (Local window: m carries the per-row factor and t = m / alpha.)"""
     amb = np.zeros(m_ref.shape, bool)
     for b in range(m_ref.shape[0]):
         L = int(lens[b])
         for j in range(L):
-            t = L * float(m_ref[b, j]) / alpha
+            t = (1 if window else L) * float(m_ref[b, j]) / alpha
             lo, hi = (t * (1 - tol)) ** 2, (t * (1 + tol)) ** 2
 
             def rule(tt):
@@ -90,14 +91,15 @@ def ambiguous_tokens(m_ref, lens, alpha, d_in, tol=TOL_M):
     return amb
 
 
-def check_rule_property(r, m, lens, alpha, d_in):
+def check_rule_property(r, m, lens, alpha, d_in, window=0):
     """The counts the GPU reports satisfy Eq. 9 for the m it reports:
-    sqrt(r) >= len * m / alpha and r - 1 < (len * m / alpha)^2 unless clamped."""
+    sqrt(r) >= len * m / alpha and r - 1 < (len * m / alpha)^2 unless clamped
+    (local window: m / alpha in place of len * m / alpha)."""
     for b in range(len(lens)):
         L = int(lens[b])
         assert np.all(r[b, L:] == 0)
         rb = r[b, :L].astype(np.float64)
-        t = L * m[b, :L].astype(np.float64) / alpha
+        t = (1 if window else L) * m[b, :L].astype(np.float64) / alpha
         assert np.all((rb >= 1) & (rb <= d_in))
         free = rb < d_in
         assert np.all(np.sqrt(rb[free]) >= t[free] * (1 - 1e-12))

@@ -99,6 +99,9 @@ def test_prepared_size_formula():
     ("dtype", 7, binding.MCA_ERR_INVALID_ARGUMENT),
     ("sampling", 2, binding.MCA_ERR_INVALID_ARGUMENT),
     ("sampling", -1, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("window", -2, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("window", 3, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("window", 1 << 26, binding.MCA_ERR_INVALID_ARGUMENT),
 ])
 def test_desc_validation(field, value, status):
     d = _desc()

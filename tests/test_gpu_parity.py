@@ -33,8 +33,9 @@ def dev():
 def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token"):
     """Oracle vs GPU on every stage; returns (#ambiguous tokens, #sampled tokens)."""
     print(f"[case] {L.name} dtype={L.dtype} B={L.batch} n={L.seq} d_in={L.d_in} H={L.heads} "
-          f"alpha={alpha} seed={seed} sampling={sampling}", flush=True)
-    ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed, want_samples=True, sampling=sampling)
+          f"alpha={alpha} seed={seed} sampling={sampling} window={L.window}", flush=True)
+    ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed, want_samples=True, sampling=sampling,
+                             window=L.window)
     t = to_device(L, dev)
     g = run_gpu(L, dev, alpha, seed, tensors=t, sampling=sampling)
     assert np.array_equal(g["rho"], ref["rho"])
@@ -43,8 +44,8 @@ def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token"):
     assert np.all(g["m"][~valid] == 0)
     rel_m = np.abs(g["m"][valid] - m_ref[valid]) / m_ref[valid]
     assert rel_m.max() <= TOL_M, rel_m.max()
-    check_rule_property(g["r"], g["m"], L.lens, alpha, L.d_in)
-    amb = ambiguous_tokens(m_ref, L.lens, alpha, L.d_in)
+    check_rule_property(g["r"], g["m"], L.lens, alpha, L.d_in, L.window)
+    amb = ambiguous_tokens(m_ref, L.lens, alpha, L.d_in, window=L.window)
     diff = g["r"] != ref["r"]
     assert not np.any(diff & ~amb), np.argwhere(diff & ~amb)[:5]
     assert np.all(np.abs(g["r"] - ref["r"])[amb] <= 1)
@@ -304,3 +305,39 @@ def test_eq6_d_in_1024(dev):
     L = wl.make_layer(2, 64, 1024, 16, "bf16", data_seed=33, q_scale=3.0, token_scale_sigma=0.5)
     amb, n_tok = _full_check(L, dev, 0.4, seed=43, sampling="weight")
     assert n_tok > 0
+
+
+# ------------------------------------------------------------------ local-window attention
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("window", [2, 16, 78])
+def test_window_small_ragged(dev, dtype, window):
+    # resident kernels (n = 40 <= 256); window 78 covers the whole sequence
+    L = wl.make_layer(2, 40, 96, 4, dtype, data_seed=5, lens=np.array([40, 23]), q_scale=3.0,
+                      token_scale_sigma=0.5, window=window)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=11)
+    assert n_tok > 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("window,lens", [(64, (400, 333)), (128, (300, 1)), (256, (399, 130))])
+def test_window_streaming_ragged(dev, dtype, window, lens):
+    # streaming kernels (n = 400 > 256): query tiles visit tile 0 and the tiles their
+    # window reaches; rows of length 1 and rows shorter than the window
+    L = wl.make_layer(2, 400, 128, 4, dtype, data_seed=6, lens=np.array(lens), q_scale=2.0,
+                      token_scale_sigma=0.5, window=window)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=3)
+    assert n_tok > 0
+
+
+@pytest.mark.parametrize("name", ["longformer_aapd_bf16", "longformer_imdb_bf16", "longformer_hnd_bf16"])
+def test_longformer_workloads(dev, name):
+    # the document-classification stand-ins at full width, on two batch rows each
+    L = wl.WORKLOADS[name]().subset([0, 1])
+    for alpha in (0.4, 0.2):
+        _full_check(L, dev, alpha, seed=0)
+
+
+def test_window_eq6(dev):
+    L = wl.make_layer(2, 300, 128, 4, "bf16", data_seed=8, lens=np.array([300, 201]), token_scale_sigma=0.5,
+                      window=64)
+    _full_check(L, dev, 0.4, seed=1, sampling="weight")
