@@ -12,8 +12,9 @@ weight matrix and are timed separately (prepare_us).
 Prints one JSON line (stdout). Also reported: per-stage kernel times from HIP events
 recorded around each launch on the library's stream, the roofline of the dominant
 kernel, the same layer computed exactly (dense) with torch on the same GPU, the
-realised FLOP reduction, the loose/tight error-bound settings, and the CPU oracle
-timed on this host.
+realised FLOP reduction, the loose/tight error-bound settings, the paper's Eq. 6
+probability, the local-window (Longformer) stand-ins against full attention and the
+exact windowed layer, and the CPU oracle timed on this host.
 """
 from __future__ import annotations
 
@@ -183,6 +184,75 @@ def dense_baseline(t, L, steps, warmup):
     return out
 
 
+def dense_window_baseline(t, L, steps, warmup):
+    """The exact local-window layer with torch: V = X W_v, then softmax over each query's
+    attended keys (window of L.window keys, global first token, key padding) times V."""
+    import torch
+
+    B, n, H, h = L.batch, L.seq, L.heads, L.window // 2
+    dev = t["X"].device
+    i = torch.arange(n, device=dev)
+    band = ((i[:, None] - i[None, :]).abs() <= h) | (i[:, None] == 0) | (i[None, :] == 0)
+    keep = band[None] & (i[None, None, :] < t["lens"].view(B, 1, 1))  # [B, n, n]
+    keep = keep[:, None].expand(B, H, n, n).reshape(B * H, n, n)
+    X2 = t["X"].reshape(B * n, L.d_in)
+    q = t["Q"].view(B, n, H, 64).permute(0, 2, 1, 3).reshape(B * H, n, 64).contiguous()
+    kT = t["K"].view(B, n, H, 64).permute(0, 2, 3, 1).reshape(B * H, 64, n).contiguous()
+
+    def bmm_path():
+        V = (X2 @ t["Wv"]).view(B, n, H, 64).permute(0, 2, 1, 3).reshape(B * H, n, 64).contiguous()
+        S = torch.bmm(q, kT).float() * 0.125
+        P = torch.softmax(S.masked_fill(~keep, float("-inf")), dim=-1).to(q.dtype)
+        return torch.bmm(P, V)
+
+    ms, _ = time_loop(bmm_path, steps, warmup)
+    return {"ms": ms, "tokens_per_s": float(L.tokens) / (ms * 1e-3), "path": "bmm + masked softmax"}
+
+
+def window_extras(mca, wl, dev, alpha, seed, steps, warmup):
+    """The local-window (Longformer) stand-ins: MCA with the window, the same layer with
+    full attention, and the exact windowed layer with torch."""
+    import torch
+
+    out = {}
+    for name in ("longformer_aapd_bf16", "longformer_imdb_bf16", "longformer_hnd_bf16"):
+        L = wl.WORKLOADS[name]()
+        t = {k: torch.from_numpy(getattr(L, k)).to(dev).to(torch.bfloat16).contiguous()
+             for k in ("Q", "K", "X", "Wv")}
+        t["lens"] = torch.from_numpy(L.lens.astype(np.int32)).to(dev)
+        prep = mca.prepare_weights(t["Wv"])
+        res = {"batch": L.batch, "padded_seq": L.seq, "mean_len": float(L.lens.mean()), "window": L.window,
+               "tokens": L.tokens}
+        for w in (L.window, 0):
+            plan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, alpha, seed, heads=L.heads,
+                                   seq_lens=t["lens"], window=w)
+            ms, _ = time_loop(plan.run, steps, warmup)
+            key = "mca_window" if w else "mca_full_attention"
+            res[key] = {"ms_per_step": ms, "tokens_per_s": L.tokens / (ms * 1e-3)}
+            if w:
+                prof = mca.Profiler()
+                pp = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, alpha, seed, heads=L.heads,
+                                     seq_lens=t["lens"], window=w, profiler=prof)
+                for _ in range(steps):
+                    pp.run()
+                torch.cuda.synchronize()
+                st = prof.collect()
+                prof.close()
+                res[key]["stage_us"] = {k: (v[0] / max(v[1], 1)) * 1e3 for k, v in st.items()}
+                torch.cuda.synchronize()
+                r = plan.r.cpu().numpy()
+                res[key]["mean_r"] = float(r[r > 0].mean())
+                res[key]["saturated_frac"] = float((r == L.d_in).sum() / max(1, (r > 0).sum()))
+                res[key]["reduction_vs_dense_xw"] = float(L.tokens * L.d_in) / float(r.sum())
+        dense = dense_window_baseline(t, L, steps, warmup)
+        res["dense_exact_window"] = dense
+        res["speedup_vs_dense"] = dense["ms"] / res["mca_window"]["ms_per_step"]
+        log(f"{name}: window {res['mca_window']['ms_per_step'] * 1e3:.1f} us, full attention "
+            f"{res['mca_full_attention']['ms_per_step'] * 1e3:.1f} us, dense windowed {dense['ms'] * 1e3:.1f} us")
+        out[name] = res
+    return out
+
+
 def cpu_baseline(L, alpha, seed, seconds):
     """The CPU oracle (fp64 numpy), as it stands, on the same layer."""
     import oracle
@@ -328,6 +398,9 @@ def main():
         ms6, _ = time_loop(p6.run, args.steps, args.warmup)
         record["sampling_eq6"] = {"ms_per_step": ms6, "tokens_per_s": L.tokens / (ms6 * 1e-3)}
         log(f"mca forward, Eq. 6 sampling: {ms6 * 1e3:.1f} us/step")
+        # local-window attention (Longformer stand-ins), fewer steps
+        record["local_window"] = window_extras(mca, wl, dev, args.alpha, args.seed, max(1, args.steps // 4),
+                                               max(1, args.warmup // 4))
     if args.calibrate_copy:
         copy_calibration(args.calibrate_copy)
     if not args.no_cpu_baseline:

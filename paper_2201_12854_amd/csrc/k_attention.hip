@@ -242,6 +242,7 @@ struct BlockCtx {
   int qt, h, b, tid, wave, lane, r16, g, n, d_out, len, q, ntl;
   int half;       // local window: keys within half of the query (0: full attention)
   int tlo, thi;   // key tiles visited: 0, then tlo .. thi (tlo >= 1)
+  int klo, kspan; // local window: the lane's query attends keys klo .. klo + kspan, and key 0
 };
 
 // One-dimensional grid of qtiles * H * B blocks. Consecutive blocks go to the 8 XCDs in
@@ -275,6 +276,15 @@ __device__ __forceinline__ BlockCtx block_ctx(const FwdParams& p) {
   c.half = p.band_half;
   c.tlo = 1;
   c.thi = c.ntl - 1;
+  c.klo = 0;
+  c.kspan = 0;
+  if (c.half > 0) {  // the window cut to the valid keys; every valid key for query 0
+    int lo = c.q == 0 ? 0 : max(0, c.q - c.half);
+    int hi = c.q == 0 ? c.len - 1 : min(c.len - 1, c.q + c.half);
+    if (hi < lo) lo = hi = 1 << 30;  // a padded query past the window's reach: key 0 only
+    c.klo = lo;
+    c.kspan = hi - lo;
+  }
   if (c.half > 0 && c.qt > 0) {  // the window of queries q0 .. q0 + 63
     const int q0 = c.qt * kTile;
     c.tlo = max(1, max(q0 - c.half, 0) / kTile);
@@ -287,12 +297,15 @@ __device__ __forceinline__ BlockCtx block_ctx(const FwdParams& p) {
 __device__ __forceinline__ int tile_count(const BlockCtx& c) { return 1 + max(0, c.thi - c.tlo + 1); }
 __device__ __forceinline__ int tile_at(const BlockCtx& c, int idx) { return idx == 0 ? 0 : c.tlo + idx - 1; }
 
-// Key e of tile kt (e = 16 s + 4 g + i, lim = len - 64 kt) is attended by the lane's query.
+// Key e = 16 s + 4 g + i of tile kt (lim = len - 64 kt) is attended by the lane's query:
+// a valid key (full attention), or a key in klo .. klo + kspan or key 0 (local window; one
+// unsigned compare per key).
 template <bool BAND>
-__device__ __forceinline__ bool key_ok(const BlockCtx& c, int kt, int lim, int e) {
+__device__ __forceinline__ bool key_ok(const BlockCtx& c, int kt, int lim, int s, int i) {
+  const int e = 16 * s + 4 * c.g + i;
   if constexpr (BAND) {
-    const int k = kt * kTile + e;
-    return e < lim && (c.q == 0 || k == 0 || abs(c.q - k) <= c.half);
+    const bool in = (unsigned)(kt * kTile + e - c.klo) <= (unsigned)c.kspan;
+    return (s == 0 && i == 0) ? (in || (kt == 0 && c.g == 0)) : in;
   } else {
     return lim >= kTile || e < lim;
   }
@@ -304,9 +317,7 @@ template <bool BAND>
 __device__ __forceinline__ float query_weight(const BlockCtx& c) {
   if (c.q >= c.len) return 0.f;
   if constexpr (BAND) {
-    if (c.q == 0) return (float)c.len;
-    const int lo = max(0, c.q - c.half), hi = min(c.len - 1, c.q + c.half);
-    return (float)(hi - lo + 1 + (lo > 0 ? 1 : 0));
+    return (float)(c.kspan + 1 + (c.klo > 0 ? 1 : 0));  // the window, and key 0 if outside it
   } else {
     return 1.f;
   }
@@ -392,7 +403,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float lg = logit(acc[kt][s][i]);
-          acc[kt][s][i] = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? lg : -INFINITY;
+          acc[kt][s][i] = key_ok<BAND>(c, kt, lim, s, i) ? lg : -INFINITY;
           M = max_sel(M, acc[kt][s][i]);
         }
     }
@@ -486,7 +497,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float lg = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? logit(acc[s][i]) : -INFINITY;
+        const float lg = key_ok<BAND>(c, kt, lim, s, i) ? logit(acc[s][i]) : -INFINITY;
         acc[s][i] = lg;
         mx = max_sel(mx, lg);
       }
@@ -536,7 +547,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const bool kvalid = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i);
+        const bool kvalid = key_ok<BAND>(c, kt, lim, s, i);
         const float pr = BAND ? __fmul_rn(prob(logit(acc[s][i]), M, inv), wq) : prob(logit(acc[s][i]), M, inv_q);
         const float a = max_over_queries(kvalid ? pr : 0.f);
         if (c.r16 == 0) cmk[c.wave][16 * s + 4 * c.g + i] = a;
@@ -597,7 +608,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const float pr = prob(logit(acc[s][i]), M, inv);
-          acc[s][i] = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? pr : 0.f;
+          acc[s][i] = key_ok<BAND>(c, kt, lim, s, i) ? pr : 0.f;
         }
       pv_tile(y, acc, Vs[kt], c.r16, c.g);
     }
@@ -647,7 +658,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float pr = prob(logit(acc[s][i]), M, inv);
-        acc[s][i] = key_ok<BAND>(c, kt, lim, 16 * s + 4 * c.g + i) ? pr : 0.f;
+        acc[s][i] = key_ok<BAND>(c, kt, lim, s, i) ? pr : 0.f;
       }
     pv_tile(y, acc, vb, c.r16, c.g);
   }
