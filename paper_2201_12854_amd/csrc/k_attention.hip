@@ -165,18 +165,12 @@ __device__ __forceinline__ void score_tile(f32x4_t acc[4], const float* Ks, cons
   }
 }
 
-// Scaled logit in base-2 units: a (q . k) log2(e) with a = 1/sqrt(64), one float32
-// multiply by the rounded constant log2(e) / 8, so that softmax needs only exp2 (one
-// hardware instruction): exp(a x - m) = exp2(a log2(e) x - m log2(e)). Kept free of
-// contraction.
+// Logits in base-2 units: a (q . k) log2(e) with a = 1/sqrt(64), the rounded constant
+// log2(e) / 8, so that softmax needs only exp2 (one hardware instruction):
+// exp(a x - m) = exp2(a log2(e) x - m log2(e)). An attention probability is
+// A = exp2(fma(dot, log2(e) / 8, -c)) with the row's c = M + log2(sum of exp2(logit - M)).
 constexpr float kLog2eOver8 = (float)(1.4426950408889634 / 8.0);
-__device__ __forceinline__ float logit(float dot) { return __fmul_rn(dot, kLog2eOver8); }
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
-
-// Attention probability from the base-2 logit and the row statistics (max, 1/sum).
-__device__ __forceinline__ float prob(float lg, float row_max, float row_inv) {
-  return __fmul_rn(exp2_fast(__fsub_rn(lg, row_max)), row_inv);
-}
 
 // max(a, b) of floats by compare and select (no NaN canonicalisation of the operands).
 __device__ __forceinline__ float max_sel(float a, float b) { return a > b ? a : b; }
@@ -368,6 +362,140 @@ __device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, c
 }
 
 // ------------------------------------------------------------------ score pass
+// The score pass computes S = Q K^T (Q as the MFMA A operand): lane (g, r16) of a wave
+// holds the scores of its queries qw + 4 g + i (i < 4, qw = the wave's first query) with
+// keys 16 s + r16 of each tile, so the statistics of a query row reduce over the 16 lanes
+// of a lane row and the column max of a key reduces over four values in registers and the
+// four lane rows. Softmax statistics are kept per query as c = M + log2(sum of exp2(logit -
+// M)), so that A = exp2(dot a log2(e) - c) (one fma, one exp2; the output pass computes A
+// the same way), and the column max is taken on t = dot a log2(e) - c before a single exp2
+// per key: m = exp2(max t) = max A, because exp2 is monotone.
+
+// The wave's four queries of lane row g under a local window: each attends keys
+// klo .. klo + kspan (its window cut to the valid keys; all of them for query 0) and key 0.
+struct RowQ {
+  int klo[4], kspan[4];
+};
+
+template <bool BAND>
+__device__ __forceinline__ RowQ row_queries(const BlockCtx& c) {
+  RowQ r;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    r.klo[i] = 0;
+    r.kspan[i] = 0;
+    if constexpr (BAND) {
+      const int q = c.qt * kTile + c.wave * 16 + 4 * c.g + i;
+      int lo = q == 0 ? 0 : max(0, q - c.half);
+      int hi = q == 0 ? c.len - 1 : min(c.len - 1, q + c.half);
+      if (hi < lo) lo = hi = 1 << 30;  // a padded query past the window's reach: key 0 only
+      r.klo[i] = lo;
+      r.kspan[i] = hi - lo;
+    }
+  }
+  return r;
+}
+
+// Key 16 s + r16 of tile kt (lim = len - 64 kt) is attended by query i of the lane row.
+template <bool BAND>
+__device__ __forceinline__ bool key_ok_q(const BlockCtx& c, const RowQ& rq, int kt, int lim, int s, int i) {
+  if constexpr (BAND) {
+    const bool in = (unsigned)(kt * kTile + 16 * s + c.r16 - rq.klo[i]) <= (unsigned)rq.kspan[i];
+    return s == 0 ? (in || (kt == 0 && c.r16 == 0)) : in;
+  } else {
+    return lim >= kTile || 16 * s + c.r16 < lim;
+  }
+}
+
+// Offset of the column-max argument of query i: c (full attention) or c - log2 |S_q|
+// (local window, the count rule's per-row factor); +inf for padded queries (excluded).
+template <bool BAND>
+__device__ __forceinline__ float colmax_offset(const BlockCtx& c, const RowQ& rq, int i, float cq) {
+  const int q = c.qt * kTile + c.wave * 16 + 4 * c.g + i;
+  if (q >= c.len) return INFINITY;
+  if constexpr (BAND) {
+    const int nk = rq.kspan[i] + 1 + (rq.klo[i] > 0 ? 1 : 0);
+    return cq - __builtin_amdgcn_logf((float)nk);
+  } else {
+    return cq;
+  }
+}
+
+// S = Q K^T for the 64 keys in LDS: acc[s][i] = dot(query 4 g + i, key 16 s + r16).
+__device__ __forceinline__ void score_tile_qk(f32x4_t acc[4], const uint16_t* Ks, const QFrag<1>& q, int r16,
+                                              int g) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    acc[s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 * ks + 8 * g);
+      acc[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q.v[ks], b, acc[s], 0, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void score_tile_qk(f32x4_t acc[4], const float* Ks, const QFrag<0>& q, int r16, int g) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    acc[s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const float* krow = Ks + (16 * s + r16) * kStrideF + 16 * g;
+#pragma unroll
+    for (int t = 0; t < 16; ++t)
+      acc[s] = __builtin_amdgcn_mfma_f32_16x16x4f32(q.v[t], krow[t], acc[s], 0, 0, 0);
+  }
+}
+
+// Reductions over the 16 lanes of a lane row (DPP butterflies; every lane gets the result).
+template <int CTRL>
+__device__ __forceinline__ float row_max_step(float v) { return max_sel(v, dpp_f32<CTRL>(v)); }
+__device__ __forceinline__ float row16_max_sel(float v) {
+  return row_max_step<0x140>(row_max_step<0x141>(row_max_step<0x4E>(row_max_step<0xB1>(v))));
+}
+template <int CTRL>
+__device__ __forceinline__ float row_sum_step(float v) { return v + dpp_f32<CTRL>(v); }
+__device__ __forceinline__ float row16_sum(float v) {
+  return row_sum_step<0x140>(row_sum_step<0x141>(row_sum_step<0x4E>(row_sum_step<0xB1>(v))));
+}
+// (max, sum of exp2(logit - max)) pairs of the 16 lanes of a row combined, rescaled to the
+// common max; a lane with no attended key so far holds (-inf, 0).
+template <int CTRL>
+__device__ __forceinline__ void row_stat_step(float& M, float& L) {
+  const float m2 = dpp_f32<CTRL>(M), l2 = dpp_f32<CTRL>(L);
+  const float Mn = max_sel(M, m2);
+  const float a = M == -INFINITY ? 0.f : __fmul_rn(L, exp2_fast(__fsub_rn(M, Mn)));
+  const float b = m2 == -INFINITY ? 0.f : __fmul_rn(l2, exp2_fast(__fsub_rn(m2, Mn)));
+  L = a + b;
+  M = Mn;
+}
+
+// Column max of one tile: t = dot a log2(e) - cc[i], the max over the lane's four queries,
+// then over the four lane rows; lane row 0 leaves the wave's value of key 16 s + r16 in
+// cmw[16 s + r16].
+__device__ __forceinline__ void tile_colmax(const f32x4_t acc[4], const float cc[4], float* cmw, const BlockCtx& c) {
+  float v[4];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    float t = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) t = max_sel(t, __fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
+    v[s] = pair32_max(pair16_max(t));
+  }
+  if (c.g == 0) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s) cmw[16 * s + c.r16] = v[s];
+  }
+}
+
+// c of query qw + 4 g + i from lane r16 = i of each lane row.
+__device__ __forceinline__ void store_row_c(const FwdParams& p, const BlockCtx& c, const float cq[4]) {
+  const int q = c.qt * kTile + c.wave * 16 + 4 * c.g + c.r16;
+  if (c.r16 < 4 && q < c.n) {
+    const float v = c.r16 == 0 ? cq[0] : c.r16 == 1 ? cq[1] : c.r16 == 2 ? cq[2] : cq[3];
+    p.row_c[((int64_t)c.b * p.H + c.h) * c.n + q] = v;
+  }
+}
+
 // Resident variant: all ntl <= NT tiles in LDS and all scores in registers.
 template <int BF, int NT, bool BAND>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_res(FwdParams p) {
@@ -389,83 +517,64 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     if (kt < c.ntl) tile_store<BF>(kr[kt], Ks[kt], c.tid);
   lds_barrier();
 
-  // row statistics: exact max over the valid keys, then the sum of exp2. Only the last
-  // tile can hold keys past the valid length (lim < kTile): the masks are applied there.
+  // scores in registers (masked keys -inf), the lane's max dot product per query
+  const RowQ rq = row_queries<BAND>(c);
   f32x4_t acc[NT][4];
-  float M = -INFINITY;
+  float dmax[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
-      score_tile(acc[kt], Ks[kt], qf, c.r16, c.g);
+      score_tile_qk(acc[kt], Ks[kt], qf, c.r16, c.g);
       const int lim = c.len - kt * kTile;
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float lg = logit(acc[kt][s][i]);
-          acc[kt][s][i] = key_ok<BAND>(c, kt, lim, s, i) ? lg : -INFINITY;
-          M = max_sel(M, acc[kt][s][i]);
+          const float d = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[kt][s][i] : -INFINITY;
+          acc[kt][s][i] = d;
+          dmax[i] = max_sel(dmax[i], d);
         }
     }
   }
-  M = pair32_max(pair16_max(M));
-  // e = exp2(logit - M), kept in acc for the column max (masked keys: exp2(-inf) = 0)
-  float L = 0.f;
+  // row statistics: M = the largest logit (rounding is monotone, so it is the rounded
+  // largest dot product), then the sum of exp2(logit - M) over the row's 16 lanes
+  float M[4], Ls[4], cq[4], cc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    M[i] = __fmul_rn(row16_max_sel(dmax[i]), kLog2eOver8);  // finite: key 0 is attended
+    Ls[i] = 0.f;
+  }
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float e = exp2_fast(__fsub_rn(acc[kt][s][i], M));
-          acc[kt][s][i] = e;
-          L += e;
-        }
+        for (int i = 0; i < 4; ++i) Ls[i] += exp2_fast(__fmaf_rn(acc[kt][s][i], kLog2eOver8, -M[i]));
     }
   }
-  L = pair32_sum(pair16_sum(L));
-  const float inv = 1.0f / L;
-  if (c.g == 0 && c.q < c.n) {
-    const int64_t o = ((int64_t)c.b * p.H + c.h) * c.n + c.q;
-    p.row_max[o] = M;
-    p.row_inv_sum[o] = inv;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    cq[i] = M[i] + __builtin_amdgcn_logf(row16_sum(Ls[i]));
+    cc[i] = colmax_offset<BAND>(c, rq, i, cq[i]);
   }
+  store_row_c(p, c, cq);
 
-  // column max of the valid queries, every tile in its own LDS slot (one barrier).
-  // probability = e * (1/L), bitwise the value prob() gives in the output pass; queries
-  // past the valid length contribute 0; local window: times |S_q|
-  const float wq = query_weight<BAND>(c);
-  const float inv_q = c.q < c.len ? inv : 0.f;
+  // column max of the block's valid queries, every tile in its own LDS slot (one barrier)
 #pragma unroll
-  for (int kt = 0; kt < NT; ++kt) {
-    if (kt < c.ntl) {
-      float a[4][4];
-#pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-          a[s][i] = BAND ? __fmul_rn(__fmul_rn(acc[kt][s][i], inv), wq) : __fmul_rn(acc[kt][s][i], inv_q);
-      max_over_queries16(a);  // 16 independent reductions, interleaved
-      if (c.r16 == 0) {
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) cm[kt][c.wave][16 * s + 4 * c.g + i] = a[s][i];
-      }
-    }
-  }
+  for (int kt = 0; kt < NT; ++kt)
+    if (kt < c.ntl) tile_colmax(acc[kt], cc, cm[kt][c.wave], c);
   lds_barrier();
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
   for (int e = c.tid; e < c.ntl * kTile; e += kThreads) {
     const int kt = e / kTile, k = e % kTile;
-    const float v = __uint_as_float(max(max(__float_as_uint(cm[kt][0][k]), __float_as_uint(cm[kt][1][k])),
-                                        max(__float_as_uint(cm[kt][2][k]), __float_as_uint(cm[kt][3][k]))));
-    if (e < c.n) part[(int64_t)e * p.nparts] = v;
+    const float v = max_sel(max_sel(cm[kt][0][k], cm[kt][1][k]), max_sel(cm[kt][2][k], cm[kt][3][k]));
+    if (e < c.n) part[(int64_t)e * p.nparts] = exp2_fast(v);
   }
 }
 
-// Streaming variant: tiles double buffered, next tile prefetched; two sweeps.
+// Streaming variant: tiles double buffered, next tile prefetched; two sweeps (per-lane
+// online statistics, then the column max).
 template <int BF, bool BAND>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
@@ -477,9 +586,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   QFrag<BF> qf;
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
+  const RowQ rq = row_queries<BAND>(c);
 
-  // Sweep 1: online row max and row sum of exp over the attended keys.
-  float M = -INFINITY, L = 0.f;
+  // Sweep 1: per lane and query, the running max logit M and the sum of exp2(logit - M)
+  // over the lane's keys; the 16 lanes of a row are combined at the end.
+  float M[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, Ls[4] = {0.f, 0.f, 0.f, 0.f};
   const int nvis = tile_count(c);
   TileRegs kr;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
@@ -490,38 +601,41 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     lds_barrier();
     kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
     f32x4_t acc[4];
-    score_tile(acc, buf, qf, c.r16, c.g);
-    float mx = -INFINITY;
+    score_tile_qk(acc, buf, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+    for (int i = 0; i < 4; ++i) {
+      float d[4], dm = -INFINITY;
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float lg = key_ok<BAND>(c, kt, lim, s, i) ? logit(acc[s][i]) : -INFINITY;
-        acc[s][i] = lg;
-        mx = max_sel(mx, lg);
+      for (int s = 0; s < 4; ++s) {
+        d[s] = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[s][i] : -INFINITY;
+        dm = max_sel(dm, d[s]);
       }
-    mx = pair32_max(pair16_max(mx));
-    const float Mn = max_sel(M, mx);  // finite: key 0 of tile 0 is attended by every query
-    float sum = 0.f;
+      const float Mn = max_sel(M[i], __fmul_rn(dm, kLog2eOver8));
+      float sum = 0.f;
 #pragma unroll
-    for (int s = 0; s < 4; ++s)
+      for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(d[s], kLog2eOver8, -Mn));
+      const float old = M[i] == -INFINITY ? 0.f : __fmul_rn(Ls[i], exp2_fast(__fsub_rn(M[i], Mn)));
+      Ls[i] = Mn == -INFINITY ? 0.f : old + sum;
+      M[i] = Mn;
+    }
+  }
+  float cq[4], cc[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) sum += exp2_fast(__fsub_rn(acc[s][i], Mn));  // masked: exp2(-inf) = 0
-    sum = pair32_sum(pair16_sum(sum));
-    L = (M == -INFINITY ? 0.f : __fmul_rn(L, exp2_fast(__fsub_rn(M, Mn)))) + sum;
-    M = Mn;
+  for (int i = 0; i < 4; ++i) {
+    float Mi = M[i], Li = Ls[i];
+    row_stat_step<0xB1>(Mi, Li);
+    row_stat_step<0x4E>(Mi, Li);
+    row_stat_step<0x141>(Mi, Li);
+    row_stat_step<0x140>(Mi, Li);
+    cq[i] = Mi + __builtin_amdgcn_logf(Li);  // finite: key 0 is attended by every query
+    cc[i] = colmax_offset<BAND>(c, rq, i, cq[i]);
   }
-  const float inv = 1.0f / L;
-  if (c.g == 0 && c.q < c.n) {
-    const int64_t o = ((int64_t)c.b * p.H + c.h) * c.n + c.q;
-    p.row_max[o] = M;
-    p.row_inv_sum[o] = inv;
-  }
+  store_row_c(p, c, cq);
 
-  // Sweep 2: probabilities and the per-key column max of this block's valid queries.
-  // The t-th visited tile uses K buffer t & 1 and column-max slot t & 1; the barrier after
-  // its LDS store also orders the reads of tile t - 2's slot before this tile's writes.
+  // Sweep 2: the per-key column max of this block's valid queries. The t-th visited tile
+  // uses K buffer t & 1 and column-max slot t & 1; the barrier after its LDS store also
+  // orders the reads of tile t - 2's slot before this tile's writes.
   lds_barrier();  // sweep 1 is done with both K buffers
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
   if (BAND) {  // valid keys of the tiles outside the window get a zero partial
@@ -530,8 +644,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
       if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
     }
   }
-  const float wq = query_weight<BAND>(c);
-  const float inv_q = c.q < c.len ? inv : 0.f;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
   for (int t = 0; t < nvis; ++t) {
     const int kt = tile_at(c, t);
@@ -541,23 +653,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     lds_barrier();
     kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
     f32x4_t acc[4];
-    score_tile(acc, buf, qf, c.r16, c.g);
+    score_tile_qk(acc, buf, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const bool kvalid = key_ok<BAND>(c, kt, lim, s, i);
-        const float pr = BAND ? __fmul_rn(prob(logit(acc[s][i]), M, inv), wq) : prob(logit(acc[s][i]), M, inv_q);
-        const float a = max_over_queries(kvalid ? pr : 0.f);
-        if (c.r16 == 0) cmk[c.wave][16 * s + 4 * c.g + i] = a;
-      }
+      for (int i = 0; i < 4; ++i)
+        if (!key_ok_q<BAND>(c, rq, kt, lim, s, i)) acc[s][i] = -INFINITY;
+    tile_colmax(acc, cc, cmk[c.wave], c);
     lds_barrier();
     if (c.tid < kTile) {
-      const float v = __uint_as_float(max(max(__float_as_uint(cmk[0][c.tid]), __float_as_uint(cmk[1][c.tid])),
-                                          max(__float_as_uint(cmk[2][c.tid]), __float_as_uint(cmk[3][c.tid]))));
+      const float v = max_sel(max_sel(cmk[0][c.tid], cmk[1][c.tid]), max_sel(cmk[2][c.tid], cmk[3][c.tid]));
       const int key = kt * kTile + c.tid;
-      if (key < c.n) part[(int64_t)key * p.nparts] = v;
+      if (key < c.n) part[(int64_t)key * p.nparts] = exp2_fast(v);
     }
   }
 }
@@ -584,7 +692,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
   QFrag<BF> qf;
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
   const int64_t so = ((int64_t)c.b * p.H + c.h) * c.n + min(c.q, c.n - 1);
-  const float M = p.row_max[so], inv = p.row_inv_sum[so];
+  const float cq = p.row_c[so];
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
@@ -607,7 +715,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
       for (int s = 0; s < 4; ++s)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const float pr = prob(logit(acc[s][i]), M, inv);
+          const float pr = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq));
           acc[s][i] = key_ok<BAND>(c, kt, lim, s, i) ? pr : 0.f;
         }
       pv_tile(y, acc, Vs[kt], c.r16, c.g);
@@ -634,7 +742,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   QFrag<BF> qf;
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
   const int64_t so = ((int64_t)c.b * p.H + c.h) * c.n + min(c.q, c.n - 1);
-  const float M = p.row_max[so], inv = p.row_inv_sum[so];
+  const float cq = p.row_c[so];
 
   f32x4_t y[4];
 #pragma unroll
@@ -657,7 +765,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
     for (int s = 0; s < 4; ++s)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const float pr = prob(logit(acc[s][i]), M, inv);
+        const float pr = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq));
         acc[s][i] = key_ok<BAND>(c, kt, lim, s, i) ? pr : 0.f;
       }
     pv_tile(y, acc, vb, c.r16, c.g);

@@ -38,7 +38,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t colmax_part, row_max, row_inv, henc, list, ucount, total;
+  size_t colmax_part, row_c, henc, list, ucount, total;
   int qtiles, nparts;
 };
 
@@ -51,8 +51,7 @@ Layout layout_for(const mca_forward_desc& d) {
   L.nparts = (int)(d.heads * L.qtiles);
   size_t off = 0;
   L.colmax_part = off; off = align256(off + 4 * tokens * size_t(L.nparts));
-  L.row_max = off;     off = align256(off + 4 * tokens * size_t(d.heads));
-  L.row_inv = off;     off = align256(off + 4 * tokens * size_t(d.heads));
+  L.row_c = off;       off = align256(off + 4 * tokens * size_t(d.heads));
   L.henc = off;        off = align256(off + helem * tokens * d_out);
   L.list = off;
   off = align256(off + 8 * (tokens * size_t(mca::list_stride((int)d.d_in)) + size_t(mca::list_tail_pad((int)d.d_in))));
@@ -245,8 +244,7 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.r = r;
   char* ws = static_cast<char*>(workspace);
   p.colmax_part = reinterpret_cast<float*>(ws + L.colmax_part);
-  p.row_max = reinterpret_cast<float*>(ws + L.row_max);
-  p.row_inv_sum = reinterpret_cast<float*>(ws + L.row_inv);
+  p.row_c = reinterpret_cast<float*>(ws + L.row_c);
   p.Henc = ws + L.henc;
   p.list = reinterpret_cast<uint2*>(ws + L.list);
   p.ucount = reinterpret_cast<int32_t*>(ws + L.ucount);

@@ -57,8 +57,8 @@ struct FwdParams {
   int32_t* r;
   // workspace
   float* colmax_part;  // [B*n][nparts]: max of A over one (head, query tile) block, per key
-  float* row_max;      // [B*H*n]
-  float* row_inv_sum;  // [B*H*n]
+  float* row_c;        // [B*H*n] softmax normaliser of a query row in base-2 units:
+                       // M + log2(sum of exp2(logit - M)), M the largest logit
   void* Henc;          // [B*n*d_out] H~ in the input dtype
   uint2* list;         // [B*n][list_stride(d_in)] distinct sampled rows of a token:
                        // (row * gather_row_bytes(d_in), float32 bits of coef); the even

@@ -67,9 +67,9 @@ def test_workspace_size_formula():
     def a(v):
         return (v + 255) // 256 * 256
 
-    # colmax partials, row max, row 1/sum, H~ (bf16), sample lists (8 bytes per row slot,
+    # colmax partials, row normalisers, H~ (bf16), sample lists (8 bytes per row slot,
     # slack after the last list), list layouts
-    expect = (a(4 * tokens * parts) + 2 * a(4 * tokens * H) + a(2 * tokens * H * 64) + a(8 * (tokens * ((d + 2) // 2 * 2) + 2 * ((d + 2) // 2 * 2) + 64))
+    expect = (a(4 * tokens * parts) + a(4 * tokens * H) + a(2 * tokens * H * 64) + a(8 * (tokens * ((d + 2) // 2 * 2) + 2 * ((d + 2) // 2 * 2) + 64))
               + a(4 * tokens))
     assert got == expect
     assert mca.workspace_size(_desc(dtype_code=0)) > got  # float32 H~
