@@ -60,9 +60,12 @@ typedef enum mca_sampling {
 typedef enum mca_stage {
   MCA_STAGE_SCORES_COLMAX = 0,  /* softmax(Q K^T / 8) row statistics and column-max partials */
   MCA_STAGE_SAMPLE = 1,         /* count rule (Eq. 9), sampling weights (Eq. 4), draws, merge */
-  MCA_STAGE_GATHER = 2,         /* H~: sampled rows gather-accumulate, saturated tokens on MFMA */
+  MCA_STAGE_GATHER = 2,         /* H~: sampled rows gather-accumulate (and, for d_in <= 768 in
+                                   bfloat16, the saturated tokens on MFMA) */
   MCA_STAGE_ATTN_OUT = 3,       /* Y = A H~ (MFMA) */
-  MCA_NUM_STAGES = 4
+  MCA_STAGE_SATURATED = 4,      /* H~ = x W_v of the saturated tokens on MFMA, as a kernel of its
+                                   own (d_in > 768 or float32 inputs; runs before the gather) */
+  MCA_NUM_STAGES = 5
 } mca_stage;
 
 /*

@@ -31,8 +31,8 @@ def _sampling_code(sampling) -> int:
     if sampling not in SAMPLING:
         raise ValueError(f"sampling must be one of {sorted(SAMPLING)} (got {sampling!r})")
     return SAMPLING[sampling]
-NUM_STAGES = 4
-STAGES = ("scores_colmax", "sample", "gather", "attn_out")
+NUM_STAGES = 5
+STAGES = ("scores_colmax", "sample", "gather", "attn_out", "saturated")
 
 
 class ForwardDesc(ctypes.Structure):

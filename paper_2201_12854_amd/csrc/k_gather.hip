@@ -467,7 +467,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
       const int len = min(uc & 0xffff, stride);                                                \
       const int nepad = min(min((uc >> 16) & 0xffff, len), 2046) & ~1;                         \
       if (r >= d_in) {                                                                         \
-        satl[atomicAdd(ctr, 1)] = tid;                                                         \
+        if (!p.sat_separate) satl[atomicAdd(ctr, 1)] = tid;                                    \
       } else if (r > 0 && len > 0) {                                                           \
         key = sort_key(max(nepad, len - nepad));                                               \
         rank = atomicAdd(ctr + 2 + key, 1);                                                    \
@@ -535,6 +535,238 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
 #undef MCA_SLICE_STORE
 }
 
+// ------------------------------------------------------------------ saturated tokens
+// Exact encoding x_j W_v of the saturated tokens (r_j = d_in) as a kernel of its own, for
+// the shapes where the gather cannot hold the B operand in LDS (d_in > 768, float32, or x
+// rows not in 16-byte chunks). A block takes 64 consecutive tokens, lists its saturated
+// tokens in LDS and multiplies them with a block of columns; each of its four waves
+// computes 32 of them (two 16-row tiles). A is the x rows (k-contiguous), B the prepared
+// W_v^T in fragment order (one coalesced 1 KB block per 16-column tile and k step). Every
+// output row depends on its own x row only, so a token's H~ does not depend on where the
+// list puts it.
+//
+// k_saturated (x rows not in 16-byte chunks): 128 columns per block, 64 per wave, operands
+// straight from memory into registers, two k steps per round, the next round's loads
+// issued before this round's MFMAs.
+constexpr int kSatTokens = 64;   // tokens per block
+constexpr int kSatCols = 128;    // columns per block
+constexpr int kSatThreads = 256;
+
+template <int BF, bool VEC>
+__global__ __launch_bounds__(kSatThreads) void k_saturated(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  constexpr int E = BF ? 8 : 4;     // elements per 16 bytes
+  constexpr int KS = BF ? 32 : 16;  // k per step
+  constexpr int RD = 2;             // steps per round
+  __shared__ int satl[kSatTokens];
+  __shared__ int nsat_s;
+  const int ncb = p.d_out / kSatCols;
+  const int cb = blockIdx.x % ncb, tb = blockIdx.x / ncb;
+  const int64_t t0 = (int64_t)tb * kSatTokens;
+  const int64_t ntok = (int64_t)p.B * p.n;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g = lane >> 4;
+  const int d_in = p.d_in;
+  if (tid == 0) nsat_s = 0;
+  __syncthreads();
+  if (tid < kSatTokens && t0 + tid < ntok && p.r[t0 + tid] >= d_in) satl[atomicAdd(&nsat_s, 1)] = tid;
+  __syncthreads();
+  const int nsat = nsat_s;
+  const int wm = wave >> 1, wn = wave & 1;
+  if (32 * wm >= nsat) return;  // no token for this wave (wave-uniform)
+  const int c0 = cb * kSatCols + 64 * wn;
+  // A rows: list rows 32 wm + 16 mt + r16 (rows past the list repeat a token, not stored)
+  const T* xr[2];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+    xr[mt] = static_cast<const T*>(p.X) + (t0 + satl[min(32 * wm + 16 * mt + r16, nsat - 1)]) * d_in;
+  const int nks = p.din_pad / KS;
+  const T* wt = static_cast<const T*>(p.Wt) + ((int64_t)(c0 / 16) * nks * 64 + lane) * E;
+  f32x4_t acc[2][4];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  const int nrounds = nks / RD;  // even: nks is a multiple of 4
+  uint4 a0[RD][2], b0[RD][4], a1[RD][2], b1[RD][4];
+#define MCA_SAT_LOAD(A, Bv, RND)                                                               \
+  _Pragma("unroll") for (int u = 0; u < RD; ++u) {                                             \
+    const int ks = (RND) * RD + u;                                                             \
+    _Pragma("unroll") for (int mt = 0; mt < 2; ++mt) A[u][mt] = load_x_chunk<BF, VEC>(xr[mt], ks * KS + E * g, d_in); \
+    _Pragma("unroll") for (int nt = 0; nt < 4; ++nt)                                           \
+      Bv[u][nt] = *reinterpret_cast<const uint4*>(wt + ((int64_t)nt * nks + ks) * 64 * E);      \
+  }
+#define MCA_SAT_MFMA(A, Bv)                                                                    \
+  _Pragma("unroll") for (int u = 0; u < RD; ++u) {                                             \
+    _Pragma("unroll") for (int mt = 0; mt < 2; ++mt) {                                         \
+      _Pragma("unroll") for (int nt = 0; nt < 4; ++nt) {                                       \
+        if constexpr (BF) {                                                                    \
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, A[u][mt]), \
+                                                               __builtin_bit_cast(bf16x8_t, Bv[u][nt]), \
+                                                               acc[mt][nt], 0, 0, 0);          \
+        } else {                                                                               \
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u][mt].x), __uint_as_float(Bv[u][nt].x), acc[mt][nt], 0, 0, 0); \
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u][mt].y), __uint_as_float(Bv[u][nt].y), acc[mt][nt], 0, 0, 0); \
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u][mt].z), __uint_as_float(Bv[u][nt].z), acc[mt][nt], 0, 0, 0); \
+          acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(A[u][mt].w), __uint_as_float(Bv[u][nt].w), acc[mt][nt], 0, 0, 0); \
+        }                                                                                      \
+      }                                                                                        \
+    }                                                                                          \
+  }
+  MCA_SAT_LOAD(a0, b0, 0)
+  for (int rd = 0; rd < nrounds; rd += 2) {
+    MCA_SAT_LOAD(a1, b1, rd + 1)
+    __builtin_amdgcn_sched_barrier(0);  // the next round's loads stay ahead of these MFMAs
+    MCA_SAT_MFMA(a0, b0)
+    MCA_SAT_LOAD(a0, b0, min(rd + 2, nrounds - 1))
+    __builtin_amdgcn_sched_barrier(0);
+    MCA_SAT_MFMA(a1, b1)
+  }
+#undef MCA_SAT_LOAD
+#undef MCA_SAT_MFMA
+  // acc[mt][nt][i] = H~[list row 32 wm + 16 mt + 4 g + i][c0 + 16 nt + r16]
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 32 * wm + 16 * mt + 4 * g + i;
+      if (row < nsat) {
+        const int64_t base = (t0 + satl[row]) * p.d_out + c0 + r16;
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) store_h<BF>(p, base + 16 * nt, acc[mt][nt][i]);
+      }
+    }
+}
+
+// k_saturated_lds (16-byte x chunks): 32 NTW columns per block (256 with NTW = 8), 16 NTW
+// per wave, the operands staged through LDS by direct global-to-LDS loads (16 bytes per
+// lane, no registers) with kSatStages - 1 k steps in flight. Per k step the block stages
+// its four 16-row A tiles and 2 NTW 16-column B tiles in fragment order (1 KB each; lane
+// l's 16 bytes at 16 l), and every wave reads its two A and NTW B fragments from there. A
+// chunk past the end of a row re-reads the row's last chunk: the prepared W_v^T is zero
+// there.
+constexpr int kSatStages = 3;
+
+// s_waitcnt for at most n outstanding vector memory operations (gfx9 encoding: vmcnt in
+// bits 3:0 and 15:14; expcnt and lgkmcnt left at their maxima, i.e. not waited for).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// One direct global-to-LDS load of 16 bytes per lane: lane l's bytes land at lds + 16 l
+// (lds wave-uniform, in M0). Issued through inline assembly so that the compiler does not
+// track it: the kernel waits for these loads itself (s_waitcnt vmcnt with the count of
+// loads issued after the one it needs) and publishes them with a barrier.
+__device__ __forceinline__ void load_lds16(const void* g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// Block barrier without a memory fence: LDS written by the direct loads is published by the
+// explicit wait before it, and the compiler may not move memory operations across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int BF, int NTW>
+__global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  constexpr int E = BF ? 8 : 4;     // elements per 16 bytes
+  constexpr int KS = BF ? 32 : 16;  // k per step
+  constexpr int NB = 2 * NTW;       // B tiles per block (16 columns each)
+  constexpr int COLS = 16 * NB;     // columns per block
+  constexpr int TILES = 4 + NB;     // 1 KB tiles per step slot: A tiles 0-3, then the B tiles
+  constexpr int kLoads = 1 + NB / 4;  // direct loads per wave per step: A tile w, B tiles w NB/4 ..
+  constexpr int kSlot = TILES * 64 * 16;
+  __shared__ int satl[kSatTokens];
+  __shared__ int nsat_s;
+  __shared__ __align__(16) uint4 stage[kSatStages * TILES * 64];
+  const int ncb = p.d_out / COLS;
+  const int cb = blockIdx.x % ncb, tb = blockIdx.x / ncb;
+  const int64_t t0 = (int64_t)tb * kSatTokens;
+  const int64_t ntok = (int64_t)p.B * p.n;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int r16 = lane & 15, g = lane >> 4;
+  const int d_in = p.d_in;
+  if (tid == 0) nsat_s = 0;
+  __syncthreads();
+  if (tid < kSatTokens && t0 + tid < ntok && p.r[t0 + tid] >= d_in) satl[atomicAdd(&nsat_s, 1)] = tid;
+  __syncthreads();
+  const int nsat = nsat_s;
+  if (nsat == 0) return;  // block-uniform
+  const int nks = p.din_pad / KS;
+  // this wave's loads: A tile `wave` (list rows 16 wave + r16, chunk E g of the step) and
+  // B tiles 2 wave, 2 wave + 1 of the block's 128 columns
+  const T* xrow = static_cast<const T*>(p.X) + (t0 + satl[min(16 * wave + r16, nsat - 1)]) * d_in;
+  const int klast = d_in - E;  // last chunk of a row
+  const T* wt = static_cast<const T*>(p.Wt) + ((int64_t)(cb * COLS / 16) * nks * 64 + lane) * E;
+  const uint32_t st0 = lds_addr(stage);
+  auto issue = [&](int ks) {
+    const uint32_t slot = st0 + (uint32_t)(ks % kSatStages) * kSlot;
+    load_lds16(xrow + min(ks * KS + E * g, klast), slot + (uint32_t)wave * 1024u);
+#pragma unroll
+    for (int j = 0; j < NB / 4; ++j) {
+      const int nt = (NB / 4) * wave + j;
+      load_lds16(wt + ((int64_t)nt * nks + ks) * 64 * E, slot + (uint32_t)(4 + nt) * 1024u);
+    }
+  };
+  const int wm = wave >> 1, wn = wave & 1;
+  const bool active = 32 * wm < nsat;  // wave-uniform
+  f32x4_t acc[2][NTW];
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int nt = 0; nt < NTW; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < kSatStages - 1; ++ks) issue(min(ks, nks - 1));
+  for (int ks = 0; ks < nks; ++ks) {
+    wait_vmcnt<(kSatStages - 2) * kLoads>();  // this wave's loads of step ks have landed
+    stage_barrier();                           // everyone's; and step ks - 1's slot is free
+    issue(min(ks + kSatStages - 1, nks - 1));  // past the end: reloads of the last step into a free slot
+    if (active) {
+      const uint4* st = stage + (ks % kSatStages) * TILES * 64;
+      uint4 a[2], b[NTW];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt) a[mt] = st[(2 * wm + mt) * 64 + lane];
+#pragma unroll
+      for (int nt = 0; nt < NTW; ++nt) b[nt] = st[(4 + NTW * wn + nt) * 64 + lane];
+#pragma unroll
+      for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt) {
+          if constexpr (BF) {
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a[mt]),
+                                                                 __builtin_bit_cast(bf16x8_t, b[nt]), acc[mt][nt], 0, 0, 0);
+          } else {
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[mt].x), __uint_as_float(b[nt].x), acc[mt][nt], 0, 0, 0);
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[mt].y), __uint_as_float(b[nt].y), acc[mt][nt], 0, 0, 0);
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[mt].z), __uint_as_float(b[nt].z), acc[mt][nt], 0, 0, 0);
+            acc[mt][nt] = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[mt].w), __uint_as_float(b[nt].w), acc[mt][nt], 0, 0, 0);
+          }
+        }
+    }
+  }
+  wait_vmcnt<0>();  // the trailing reloads have landed before the wave ends
+  if (!active) return;
+  const int c0 = cb * COLS + 16 * NTW * wn;
+  // acc[mt][nt][i] = H~[list row 32 wm + 16 mt + 4 g + i][c0 + 16 nt + r16]
+#pragma unroll
+  for (int mt = 0; mt < 2; ++mt)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int row = 32 * wm + 16 * mt + 4 * g + i;
+      if (row < nsat) {
+        const int64_t base = (t0 + satl[row]) * p.d_out + c0 + r16;
+#pragma unroll
+        for (int nt = 0; nt < NTW; ++nt) store_h<BF>(p, base + 16 * nt, acc[mt][nt][i]);
+      }
+    }
+}
+
 int device_cus() {
   static int cached[64] = {0};
   int dev = 0;
@@ -577,9 +809,29 @@ int gather_blocks_per_slice(int d_in, int d_out) {
   return max(1, device_cus() / nslices);
 }
 
+hipError_t launch_saturated(const FwdParams& p, hipStream_t s) {
+  if (p.d_out % kSatCols != 0) return hipErrorInvalidValue;
+  const bool vec = p.d_in % (p.bf16 ? 8 : 4) == 0;
+  const int64_t ntok = (int64_t)p.B * p.n;
+  const dim3 grid((unsigned)(((ntok + kSatTokens - 1) / kSatTokens) * (p.d_out / kSatCols))), blk(kSatThreads);
+  if (vec) {  // 64 tokens x 256 columns per block
+    const dim3 g2((unsigned)(((ntok + kSatTokens - 1) / kSatTokens) * (p.d_out / 256)));
+    return p.bf16 ? launch_stage_kernel(k_saturated_lds<1, 8>, g2, blk, 0, s, p)
+                  : launch_stage_kernel(k_saturated_lds<0, 8>, g2, blk, 0, s, p);
+  }
+  return p.bf16 ? launch_stage_kernel(k_saturated<1, false>, grid, blk, 0, s, p)
+                : launch_stage_kernel(k_saturated<0, false>, grid, blk, 0, s, p);
+}
+
 hipError_t launch_gather(const FwdParams& p, hipStream_t s) {
   if (p.wc != gather_slice_cols(p.d_in) || p.d_out % p.wc != 0 || p.gather_bps < 1) return hipErrorInvalidValue;
   const bool vec = p.d_in % (p.bf16 ? 8 : 4) == 0;
+  if (p.sat_separate) {
+    if (p.bf16) {
+      if (p.wc == 32) return vec ? launch_wc<1, 32, true, false>(p, s) : launch_wc<1, 32, false, false>(p, s);
+      return vec ? launch_wc<1, 16, true, false>(p, s) : launch_wc<1, 16, false, false>(p, s);
+    }
+  }
   if (p.bf16) {
     if (p.wc == 32) {
       // bfloat16, d_in <= 768: the saturated tokens' B operand fits in LDS next to the slice

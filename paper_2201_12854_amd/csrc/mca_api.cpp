@@ -159,7 +159,7 @@ const char* mca_last_error(void) { return g_last_error; }
 int mca_num_stages(void) { return MCA_NUM_STAGES; }
 
 const char* mca_stage_name(int stage) {
-  static const char* names[MCA_NUM_STAGES] = {"scores_colmax", "sample", "gather", "attn_out"};
+  static const char* names[MCA_NUM_STAGES] = {"scores_colmax", "sample", "gather", "attn_out", "saturated"};
   return (stage >= 0 && stage < MCA_NUM_STAGES) ? names[stage] : "unknown";
 }
 
@@ -249,6 +249,9 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.list = reinterpret_cast<uint2*>(ws + L.list);
   p.ucount = reinterpret_cast<int32_t*>(ws + L.ucount);
   p.wc = mca::gather_slice_cols(p.d_in);
+  // saturated tokens: inside the gather (bf16, 16-byte x chunks, d_in <= 768: the slice's
+  // B operand fits in LDS next to the W_v slice), else in their own MFMA kernel
+  p.sat_separate = !(p.bf16 && p.d_in % 8 == 0 && p.din_pad <= 768);
   p.gather_bps = mca::gather_blocks_per_slice(p.d_in, p.d_out);
   p.colmax_out = desc->colmax_out;
   p.idx_out = desc->sample_idx_out;
@@ -260,6 +263,9 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   if ((st = run_stage(pr, MCA_STAGE_SCORES_COLMAX, p, [&] { return mca::launch_scores_colmax(p, s); })) != MCA_OK)
     return st;
   if ((st = run_stage(pr, MCA_STAGE_SAMPLE, p, [&] { return mca::launch_sample(p, s); })) != MCA_OK) return st;
+  if (p.sat_separate &&
+      (st = run_stage(pr, MCA_STAGE_SATURATED, p, [&] { return mca::launch_saturated(p, s); })) != MCA_OK)
+    return st;
   if ((st = run_stage(pr, MCA_STAGE_GATHER, p, [&] { return mca::launch_gather(p, s); })) != MCA_OK) return st;
   if ((st = run_stage(pr, MCA_STAGE_ATTN_OUT, p, [&] { return mca::launch_attn_out(p, s); })) != MCA_OK) return st;
   return ok();

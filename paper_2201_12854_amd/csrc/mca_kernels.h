@@ -68,6 +68,7 @@ struct FwdParams {
   int32_t* ucount;     // [B*n] list layout of a sampled token: (even part length << 16) |
                        // total length; 0 when the token has no list
   int wc;              // W_v columns per gather slice (32 or 16)
+  int sat_separate;    // saturated tokens encoded by their own kernel (the gather skips them)
   int gather_bps;      // gather blocks per slice
   // optional outputs
   float* colmax_out;
@@ -90,6 +91,8 @@ inline hipError_t launch_stage_kernel(K kernel, dim3 grid, dim3 block, size_t ld
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s);
 hipError_t launch_sample(const FwdParams& p, hipStream_t s);
 hipError_t launch_gather(const FwdParams& p, hipStream_t s);
+// The exact encoding of saturated tokens as its own MFMA kernel (when sat_separate).
+hipError_t launch_saturated(const FwdParams& p, hipStream_t s);
 // Columns per gather slice for d_in (the slice, float32, must fit the LDS).
 __host__ __device__ inline int gather_slice_cols(int d_in) { return d_in <= 1024 ? 32 : 16; }
 // Entries reserved per token in the sample list: at most d_in - 1 distinct rows plus one

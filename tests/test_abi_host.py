@@ -32,7 +32,7 @@ def test_header_enums_match_binding():
     text = open(HEADER).read()
     for name, val in [("MCA_OK", 0), ("MCA_ERR_INVALID_ARGUMENT", 1), ("MCA_ERR_UNSUPPORTED", 2),
                       ("MCA_ERR_WORKSPACE_TOO_SMALL", 3), ("MCA_ERR_HIP", 4), ("MCA_F32", 0), ("MCA_BF16", 1),
-                      ("MCA_NUM_STAGES", 4), ("MCA_SAMPLING_TOKEN", 0), ("MCA_SAMPLING_WEIGHT", 1)]:
+                      ("MCA_NUM_STAGES", 5), ("MCA_SAMPLING_TOKEN", 0), ("MCA_SAMPLING_WEIGHT", 1)]:
         assert re.search(rf"\b{name}\s*=\s*{val}\b", text), name
     # struct layout: the binding's ctypes mirror has the header's field order
     body = re.search(r"typedef struct mca_forward_desc \{(.*?)\} mca_forward_desc;", text, re.S).group(1)
@@ -46,8 +46,8 @@ def test_status_strings_and_stages():
     for code, name in [(0, "MCA_OK"), (1, "MCA_ERR_INVALID_ARGUMENT"), (2, "MCA_ERR_UNSUPPORTED"),
                        (3, "MCA_ERR_WORKSPACE_TOO_SMALL"), (4, "MCA_ERR_HIP")]:
         assert mca.status_string(code) == name
-    assert lib.mca_num_stages() == 4
-    assert [lib.mca_stage_name(i).decode() for i in range(4)] == list(binding.STAGES)
+    assert lib.mca_num_stages() == 5
+    assert [lib.mca_stage_name(i).decode() for i in range(5)] == list(binding.STAGES)
     assert lib.mca_stage_name(99).decode() == "unknown"
 
 
