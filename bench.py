@@ -78,7 +78,7 @@ def stage_work(L, r, idx, elem):
     n_zero = B * n - n_sampled - n_sat
     qk_flops = 2.0 * H * 64 * float(np.sum(n * lens))  # per pass over all (query, valid key) pairs
     w = {}
-    w["scores_colmax"] = dict(bytes=2.0 * B * n * d_out * s_in + 8.0 * B * H * n + 4.0 * B * n * nparts,
+    w["scores_colmax"] = dict(bytes=2.0 * B * n * d_out * s_in + 4.0 * B * H * n + 4.0 * B * n * nparts,
                               flops=2 * qk_flops)
     # partials, x rows of valid tokens, rho, r, the lists (8 bytes per distinct row), zero rows
     w["sample"] = dict(bytes=4.0 * B * n * nparts + n_valid * d_in * s_in + 4.0 * d_in + 4.0 * B * n
@@ -93,7 +93,10 @@ def stage_work(L, r, idx, elem):
                        bytes_every_draw=8.0 * distinct + draws * d_out * s_in + n_sampled * d_out * s_h + sat_bytes,
                        mfma_flops=2.0 * n_sat * d_in * d_out)
     w["attn_out"] = dict(bytes=2.0 * B * n * d_out * s_in + B * n * d_out * s_h + 4.0 * B * n * d_out
-                         + 8.0 * B * H * n, flops=2 * qk_flops)
+                         + 4.0 * B * H * n, flops=2 * qk_flops)
+    # the separate saturated kernel (shapes whose B operand does not fit next to the slice);
+    # at this shape the gather encodes the saturated tokens and this stage does not run
+    w["saturated"] = dict(bytes=sat_bytes, flops=2.0 * n_sat * d_in * d_out)
     stats = dict(sampled_tokens=n_sampled, saturated_tokens=n_sat, draws=draws, distinct_rows=distinct)
     return w, stats
 
@@ -253,6 +256,54 @@ def window_extras(mca, wl, dev, alpha, seed, steps, warmup):
     return out
 
 
+def dense_stage_extras(mca, wl, dev, alpha, seed, steps):
+    """MFMA rates of the dense stages where they carry the work: BERT-large with sharpened
+    logits (every token saturates, so the value encoding is the exact X W_v GEMM) and the
+    4096-token sequences. Algorithmic FLOPs over the valid keys and queries: the score pass
+    2 H sum(len^2) 64 (one Q K^T), the output pass twice that (Q K^T and A H~), the
+    saturated encoding 2 d_in d_out per saturated token; against the bf16 dense peak."""
+    import torch
+
+    out = {}
+    for name in ("bert_large_sharp_bf16", "long_seq_bf16"):
+        L = wl.WORKLOADS[name]()
+        t = {k: torch.from_numpy(getattr(L, k)).to(dev).to(torch.bfloat16).contiguous()
+             for k in ("Q", "K", "X", "Wv")}
+        lens = torch.from_numpy(L.lens.astype(np.int32)).to(dev)
+        prep = mca.prepare_weights(t["Wv"])
+        prof = mca.Profiler()
+        plan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, alpha, seed, heads=L.heads, seq_lens=lens,
+                               profiler=prof)
+        for _ in range(3):
+            plan.run()
+        torch.cuda.synchronize()
+        prof.collect()
+        for _ in range(steps):
+            plan.run()
+        torch.cuda.synchronize()
+        st = {k: (v[0] / max(v[1], 1)) * 1e3 for k, v in prof.collect().items()}
+        prof.close()
+        r = plan.r.cpu().numpy()
+        nsat = int((r == L.d_in).sum())
+        qk = 2.0 * L.heads * float(np.sum(L.lens.astype(np.float64) ** 2)) * 64
+        res = {"batch": L.batch, "seq": L.seq, "d": L.d_in, "heads": L.heads, "stage_us": st,
+               "ms_per_step": sum(st.values()) * 1e-3, "saturated_tokens": nsat}
+
+        def rate(flops, us):
+            if not us:
+                return None
+            tf = flops / (us * 1e-6) / 1e12
+            return {"TFLOP/s": tf, "mfma_frac": tf / MFMA_BF16_PEAK_TFLOPS}
+
+        res["scores_colmax"] = rate(qk, st["scores_colmax"])
+        res["attn_out"] = rate(2 * qk, st["attn_out"])
+        if st.get("saturated"):
+            res["saturated"] = rate(2.0 * nsat * L.d_in * L.d_out, st["saturated"])
+        log(f"{name}: " + ", ".join(f"{k}={v:.1f} us" for k, v in st.items()))
+        out[name] = res
+    return out
+
+
 def cpu_baseline(L, alpha, seed, seconds):
     """The CPU oracle (fp64 numpy), as it stands, on the same layer."""
     import oracle
@@ -398,6 +449,8 @@ def main():
         ms6, _ = time_loop(p6.run, args.steps, args.warmup)
         record["sampling_eq6"] = {"ms_per_step": ms6, "tokens_per_s": L.tokens / (ms6 * 1e-3)}
         log(f"mca forward, Eq. 6 sampling: {ms6 * 1e3:.1f} us/step")
+        # dense stages at the MFMA-bound shapes
+        record["dense_stages"] = dense_stage_extras(mca, wl, dev, args.alpha, args.seed, 20)
         # local-window attention (Longformer stand-ins), fewer steps
         record["local_window"] = window_extras(mca, wl, dev, args.alpha, args.seed, max(1, args.steps // 4),
                                                max(1, args.warmup // 4))
