@@ -13,8 +13,9 @@ Prints one JSON line (stdout). Also reported: per-stage kernel times from HIP ev
 recorded around each launch on the library's stream, the roofline of the dominant
 kernel, the same layer computed exactly (dense) with torch on the same GPU, the
 realised FLOP reduction, the loose/tight error-bound settings, the paper's Eq. 6
-probability, the local-window (Longformer) stand-ins against full attention and the
-exact windowed layer, and the CPU oracle timed on this host.
+probability, the dense stages at the BERT-large and 4096-token shapes, the error growth
+over a 12-layer stack, the local-window (Longformer) stand-ins against full attention and
+the exact windowed layer, and the CPU oracle timed on this host.
 """
 from __future__ import annotations
 
@@ -304,6 +305,33 @@ def dense_stage_extras(mca, wl, dev, alpha, seed, steps):
     return out
 
 
+def depth_extras(dev):
+    """Error growth with depth: a 12-layer stack of MCA attention layers (BERT-base width,
+    synthetic N(0, 0.02^2) weights, layer-norm after the residual) against the same stack in
+    regular mode (exact X W_v), relative Frobenius error of every layer's output averaged
+    over 4 seeds, in bfloat16 and float32."""
+    import torch
+
+    from paper_2201_12854_amd.stack import SyntheticEncoder, depth_error
+
+    B, n, d, H, layers = 8, 128, 768, 12, 12
+    x32 = np.random.default_rng(11).standard_normal((B, n, d)).astype(np.float32)
+    lens = torch.full((B,), n, dtype=torch.int32, device=dev)
+    out = {"batch": B, "seq": n, "d": d, "heads": H, "layers": layers}
+    for dtype in ("bf16", "f32"):
+        enc = SyntheticEncoder(layers, d, H, dtype, seed=21, device=dev)
+        x = torch.from_numpy(x32).to(dev).to(enc.dtype).contiguous()
+        res = {}
+        for alpha in (0.2, 0.4, 1.0):
+            errs = depth_error(enc, x, lens, alpha, range(1, 5))
+            res[str(alpha)] = {"rel_error_by_layer": [float(e) for e in errs], "after_6": float(errs[5]),
+                               "after_12": float(errs[11])}
+        out[dtype] = res
+        log(f"depth ({dtype}): relative error after 1 / 6 / 12 layers at alpha 0.4: "
+            + " / ".join(f"{res['0.4']['rel_error_by_layer'][i]:.4f}" for i in (0, 5, 11)))
+    return out
+
+
 def cpu_baseline(L, alpha, seed, seconds):
     """The CPU oracle (fp64 numpy), as it stands, on the same layer."""
     import oracle
@@ -451,6 +479,8 @@ def main():
         log(f"mca forward, Eq. 6 sampling: {ms6 * 1e3:.1f} us/step")
         # dense stages at the MFMA-bound shapes
         record["dense_stages"] = dense_stage_extras(mca, wl, dev, args.alpha, args.seed, 20)
+        # error growth over a 12-layer stack
+        record["depth"] = depth_extras(dev)
         # local-window attention (Longformer stand-ins), fewer steps
         record["local_window"] = window_extras(mca, wl, dev, args.alpha, args.seed, max(1, args.steps // 4),
                                                max(1, args.warmup // 4))

@@ -341,3 +341,31 @@ def test_window_eq6(dev):
     L = wl.make_layer(2, 300, 128, 4, "bf16", data_seed=8, lens=np.array([300, 201]), token_scale_sigma=0.5,
                       window=64)
     _full_check(L, dev, 0.4, seed=1, sampling="weight")
+
+
+# ------------------------------------------------------------------ stacked layers
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_stack_layers_match_oracle(dev, dtype):
+    # every layer of a 3-layer stack with synthetic weights, on the hidden states the stack
+    # itself produced (post layer-norm), against the oracle
+    import torch
+
+    from paper_2201_12854_amd.stack import SyntheticEncoder
+
+    enc = SyntheticEncoder(3, 256, 4, dtype, seed=7)
+    tdt = torch.float32 if dtype == "f32" else torch.bfloat16
+    rng = np.random.default_rng(3)
+    x = torch.from_numpy(rng.standard_normal((2, 48, 256)).astype(np.float32)).to(dev).to(tdt).contiguous()
+    lens_np = np.array([48, 30], np.int32)
+    lens = torch.from_numpy(lens_np).to(dev)
+    outs = enc.forward(x, lens, 0.4, 5, keep=True)
+    torch.cuda.synchronize()
+    for l in range(3):
+        h = x if l == 0 else outs[l - 1]
+        q, k = enc.layer_inputs(h, l)
+        arr = [t.float().cpu().numpy() for t in (q, k, h, enc.layers[l].Wv)]
+        L = wl.Layer(f"stack_layer{l}", dtype, *arr, lens_np, 4, 0.4, 5 + l)
+        _full_check(L, dev, 0.4, seed=5 + l)
+    # the exact stack (every count at d_in) equals the regular-mode layers: no samples drawn
+    ex = enc.forward(x, lens, 0.4, 5, exact=True)
+    assert torch.isfinite(ex.float()).all()
