@@ -13,7 +13,9 @@ Mechanism" (AAAI-22), step by step, in the paper's notation:
       Mechanisms", the definition of A before Eq. 1)
   O3  m_j = max A[:, j]  (largest attention key j receives,   (Sec. "Determining Sample
       over valid queries and all heads)                         Size from Attention", Eq. 8)
-  O4  sqrt(r_j) = n * m_j / alpha                              (Eq. 9)
+  O4  sqrt(r_j) = n * m_j / alpha                              (Eq. 9); m_j may instead be
+      the mean or the median of A[:, j] (the more aggressive rules
+      named after Eq. 8; no bound is proved for them)
   O5  p_ji proportional to |x_ji| * ||W[i]||                   (Eq. 4, the DKM-optimal
                                                                  probability, per token)
       or, in the paper's own input-independent mode,
@@ -186,6 +188,32 @@ def column_max(Q, K, lens, heads, window: int = 0) -> np.ndarray:
     return m
 
 
+IMPORTANCE_MAX = "max"        # Eq. 8-9: the largest attention a key receives
+IMPORTANCE_MEAN = "mean"      # the mean over valid queries and heads (a more aggressive rule)
+IMPORTANCE_MEDIAN = "median"  # the median over valid queries and heads
+
+
+def column_importance(Q, K, lens, heads, rule: str = IMPORTANCE_MAX) -> np.ndarray:
+    """The per-key statistic that sets the count under full attention: the max of
+    A_h[b, i, j] over heads h and valid queries i (Eq. 8-9), or, as the more aggressive
+    schemes the paper names after Eq. 8, their mean or median (over the H * len values;
+    for an even count the median is the mean of the two middle values). 0 for padded
+    keys."""
+    if rule == IMPORTANCE_MAX:
+        return column_max(Q, K, lens, heads)
+    if rule not in (IMPORTANCE_MEAN, IMPORTANCE_MEDIAN):
+        raise ValueError(f"unknown importance rule {rule!r}")
+    B, n = Q.shape[0], Q.shape[1]
+    m = np.zeros((B, n), dtype=np.float64)
+    for b in range(B):
+        L = int(lens[b])
+        vals = np.stack([attention_probs(Q[b, :, head_slice(h)], K[b, :, head_slice(h)], L)[:L, :L]
+                         for h in range(heads)])  # [H, queries, keys]
+        per_key = vals.transpose(2, 0, 1).reshape(L, heads * L)
+        m[b, :L] = per_key.mean(axis=1) if rule == IMPORTANCE_MEAN else np.median(per_key, axis=1)
+    return m
+
+
 # --------------------------------------------------------------------------- O4
 def sample_counts(m: np.ndarray, lens, alpha: float, d_in: int, window: int = 0) -> np.ndarray:
     """Eq. 9: sqrt(r_j) = n * m_j / alpha with n the valid length of the sequence;
@@ -293,7 +321,7 @@ def encode_token(x, W, rho, r: int, seed: int, b: int, j: int, *, sampling=SAMPL
 # --------------------------------------------------------------------------- forward
 def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_override=None,
                 rho=None, y_rows=None, want_samples=False, want_exact=False, sampling=SAMPLING_TOKEN,
-                window: int = 0):
+                window: int = 0, importance: str = IMPORTANCE_MAX):
     """Full MCA forward (O1-O9) for right-padded sequences.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W: [d_in, heads*64] (all float32
@@ -305,16 +333,21 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
     samples (per token: indices, coefficients) and the exact Y* of Eq. 1.
     ``sampling`` selects the probability: SAMPLING_TOKEN (Eq. 4, per token) or
     SAMPLING_WEIGHT (Eq. 6, one table per weight matrix). ``window`` > 0 selects
-    local-window attention with a global first token (see ``attended``).
+    local-window attention with a global first token (see ``attended``). ``importance``
+    selects the per-key statistic of the count rule (``column_importance``; full
+    attention only for the mean and median).
     """
     if window < 0 or window % 2:
         raise ValueError("window must be 0 (full attention) or a positive even number of keys")
+    if importance != IMPORTANCE_MAX and window:
+        raise ValueError("the mean and median rules are defined for full attention")
     B, n, d_in = X.shape
     d_out = W.shape[1]
     lens = np.asarray(lens)
     if rho is None:
         rho = row_norms(W)
-    m = column_max(Q, K, lens, heads, window)
+    m = column_max(Q, K, lens, heads, window) if importance == IMPORTANCE_MAX else \
+        column_importance(Q, K, lens, heads, importance)
     if r_override is None:
         r = sample_counts(m, lens, alpha, d_in, window)
     else:
