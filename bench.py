@@ -13,7 +13,7 @@ Prints one JSON line (stdout). Also reported: per-stage kernel times from HIP ev
 recorded around each launch on the library's stream, the roofline of the dominant
 kernel, the same layer computed exactly (dense) with torch on the same GPU, the
 realised FLOP reduction, the loose/tight error-bound settings, the paper's Eq. 6
-probability, the dense stages at the BERT-large and 4096-token shapes, the error growth
+probability, the mean and median importance rules, the dense stages at the BERT-large and 4096-token shapes, the error growth
 over a 12-layer stack, the local-window (Longformer) stand-ins against full attention and
 the exact windowed layer, and the CPU oracle timed on this host.
 """
@@ -477,6 +477,19 @@ def main():
         ms6, _ = time_loop(p6.run, args.steps, args.warmup)
         record["sampling_eq6"] = {"ms_per_step": ms6, "tokens_per_s": L.tokens / (ms6 * 1e-3)}
         log(f"mca forward, Eq. 6 sampling: {ms6 * 1e3:.1f} us/step")
+        # the mean and median importance rules (same workload and alpha)
+        rules = {}
+        for rule in ("mean", "median"):
+            pr = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
+                                 seq_lens=lens, importance=rule)
+            ms_r, _ = time_loop(pr.run, args.steps, args.warmup)
+            torch.cuda.synchronize()
+            rr = pr.r.cpu().numpy()
+            rules[rule] = {"ms_per_step": ms_r, "tokens_per_s": L.tokens / (ms_r * 1e-3),
+                           "mean_r": float(rr[rr > 0].mean()), "saturated_frac": float((rr == L.d_in).mean()),
+                           "reduction_vs_dense_xw": float(L.tokens * L.d_in) / float(rr.sum())}
+            log(f"mca forward, {rule} rule: {ms_r * 1e3:.1f} us/step, mean r {rules[rule]['mean_r']:.1f}")
+        record["importance_rules"] = rules
         # dense stages at the MFMA-bound shapes
         record["dense_stages"] = dense_stage_extras(mca, wl, dev, args.alpha, args.seed, 20)
         # error growth over a 12-layer stack

@@ -57,6 +57,13 @@ typedef enum mca_sampling {
 } mca_sampling;
 
 /* Stages of the forward pass, in launch order (profiler slots). */
+typedef enum mca_importance {
+  MCA_IMPORTANCE_MAX = 0,     /* m_j = max over valid queries and heads of A[:, j] (Eq. 8-9) */
+  MCA_IMPORTANCE_MEAN = 1,    /* their mean */
+  MCA_IMPORTANCE_MEDIAN = 2   /* their median (the mean of the two middle values for an even
+                                 count); needs 4 B n H n bytes more workspace */
+} mca_importance;
+
 typedef enum mca_stage {
   MCA_STAGE_SCORES_COLMAX = 0,  /* softmax(Q K^T / 8) row statistics and column-max partials */
   MCA_STAGE_SAMPLE = 1,         /* count rule (Eq. 9), sampling weights (Eq. 4), draws, merge */
@@ -115,6 +122,10 @@ typedef struct mca_forward_desc {
      rule then uses each query's key count |S_i| in place of n:
      m_j = max over heads and valid queries i of |S_i| A[i, j], t = m_j / alpha. */
   int64_t window;
+  /* mca_importance: the per-key statistic m_j of the count rule under full attention
+     (window = 0). MCA_IMPORTANCE_MAX is Eq. 8-9; the mean and the median are the more
+     aggressive schemes the paper names after Eq. 8 (no error bound is proved for them). */
+  int32_t importance;
 } mca_forward_desc;
 
 /*
@@ -178,7 +189,8 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  * `workspace` must hold at least mca_workspace_size bytes; its contents on entry do not
  * matter and are overwritten.
  * Errors: MCA_ERR_INVALID_ARGUMENT (null required pointer, size < 1, non-finite or
- * non-positive alpha, unknown sampling mode, odd or negative window, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
+ * non-positive alpha, unknown sampling mode, odd or negative window, unknown importance rule or
+ * a mean/median rule with a window, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
  * != 64, d_out not a multiple of 256 or > 2048, d_in > 2048), MCA_ERR_WORKSPACE_TOO_SMALL,
  * MCA_ERR_HIP.
  */

@@ -25,6 +25,14 @@ MCA_BF16 = 1
 MCA_SAMPLING_TOKEN = 0   # Eq. 4 per token
 MCA_SAMPLING_WEIGHT = 1  # Eq. 6, input independent
 SAMPLING = {"token": MCA_SAMPLING_TOKEN, "weight": MCA_SAMPLING_WEIGHT}
+MCA_IMPORTANCE_MAX, MCA_IMPORTANCE_MEAN, MCA_IMPORTANCE_MEDIAN = 0, 1, 2
+IMPORTANCE = {"max": MCA_IMPORTANCE_MAX, "mean": MCA_IMPORTANCE_MEAN, "median": MCA_IMPORTANCE_MEDIAN}
+
+
+def _importance_code(rule) -> int:
+    if rule not in IMPORTANCE:
+        raise ValueError(f"importance must be one of {sorted(IMPORTANCE)} (got {rule!r})")
+    return IMPORTANCE[rule]
 
 
 def _sampling_code(sampling) -> int:
@@ -54,6 +62,7 @@ class ForwardDesc(ctypes.Structure):
         ("encoded_out", ctypes.c_void_p),
         ("profiler", ctypes.c_void_p),
         ("window", ctypes.c_int64),
+        ("importance", ctypes.c_int32),
     ]
 
 
@@ -132,7 +141,7 @@ def _stream_handle(device) -> int:
 
 def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None, r_in=None,
               colmax_out=None, sample_idx_out=None, sample_coef_out=None, encoded_out=None,
-              profiler=None, sampling=0, window=0) -> ForwardDesc:
+              profiler=None, sampling=0, window=0, importance=0) -> ForwardDesc:
     d = ForwardDesc()
     d.batch, d.seq, d.heads, d.d_head, d.d_in = batch, seq, heads, 64, d_in
     d.dtype, d.sampling = dtype_code, sampling
@@ -142,6 +151,7 @@ def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None
     d.sample_coef_out, d.encoded_out = _ptr(sample_coef_out), _ptr(encoded_out)
     d.profiler = None if profiler is None else profiler.handle
     d.window = int(window)
+    d.importance = int(importance)
     return d
 
 
@@ -192,7 +202,7 @@ class ForwardResult:
 def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int,
                       seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
                       workspace=None, out=None, profiler=None, sampling: str = "token",
-                      window: int = 0) -> ForwardResult:
+                      window: int = 0, importance: str = "max") -> ForwardResult:
     """One MCA forward pass through libmca on the current HIP stream.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
@@ -203,7 +213,8 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     ``out`` may pass preallocated (Y, r). ``sampling``: "token" (Eq. 4, per token) or
     "weight" (Eq. 6, the paper's input-independent probability). ``window``: 0 for full
     attention, or an even local window (keys within window / 2 of each query, plus a
-    global first token).
+    global first token). ``importance``: "max" (Eq. 8-9), "mean" or "median", the per-key
+    statistic of the count rule (full attention).
     """
     import torch
 
@@ -234,7 +245,8 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     desc = make_desc(B, n, heads, d_in, dt, alpha, seed, seq_lens=seq_lens, r_in=r_in,
                      colmax_out=res.colmax, sample_idx_out=res.sample_idx,
                      sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler,
-                     sampling=_sampling_code(sampling), window=window)
+                     sampling=_sampling_code(sampling), window=window,
+                     importance=_importance_code(importance))
     ws_bytes = workspace_size(desc)
     if workspace is None or workspace.numel() < ws_bytes:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
@@ -283,7 +295,7 @@ class ForwardPlan:
     stream), so that ``run()`` is a single C call: for timing loops and serving."""
 
     def __init__(self, Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
-                 r_in=None, profiler=None, sampling: str = "token", window: int = 0):
+                 r_in=None, profiler=None, sampling: str = "token", window: int = 0, importance: str = "max"):
         import torch
 
         lib = load_library()
@@ -292,7 +304,8 @@ class ForwardPlan:
         dev = X.device
         self._keep = (Q, K, X, W_v, prepared, seq_lens, r_in)
         self.desc = make_desc(B, n, heads, d_in, _dtype_code(X), alpha, seed, seq_lens=seq_lens, r_in=r_in,
-                              profiler=profiler, sampling=_sampling_code(sampling), window=window)
+                              profiler=profiler, sampling=_sampling_code(sampling), window=window,
+                              importance=_importance_code(importance))
         ws = workspace_size(self.desc)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
         self.Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)

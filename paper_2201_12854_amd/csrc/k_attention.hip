@@ -469,21 +469,48 @@ __device__ __forceinline__ void row_stat_step(float& M, float& L) {
   M = Mn;
 }
 
-// Column max of one tile: t = dot a log2(e) - cc[i], the max over the lane's four queries,
-// then over the four lane rows; lane row 0 leaves the wave's value of key 16 s + r16 in
-// cmw[16 s + r16].
-__device__ __forceinline__ void tile_colmax(const f32x4_t acc[4], const float cc[4], float* cmw, const BlockCtx& c) {
+// Column statistic of one tile, t = dot a log2(e) - cc[i]: the max of t over the lane's four
+// queries, then over the four lane rows (max rule; the block's partial is exp2 of the max),
+// or the sum of exp2(t) = A (mean rule); lane row 0 leaves the wave's value of key
+// 16 s + r16 in cmw[16 s + r16].
+__device__ __forceinline__ void tile_colmax(const f32x4_t acc[4], const float cc[4], float* cmw, const BlockCtx& c,
+                                            bool sum) {
   float v[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    float t = -INFINITY;
+    if (sum) {
+      float t = 0.f;
 #pragma unroll
-    for (int i = 0; i < 4; ++i) t = max_sel(t, __fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
-    v[s] = pair32_max(pair16_max(t));
+      for (int i = 0; i < 4; ++i) t += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
+      v[s] = pair32_sum(pair16_sum(t));
+    } else {
+      float t = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) t = max_sel(t, __fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
+      v[s] = pair32_max(pair16_max(t));
+    }
   }
   if (c.g == 0) {
 #pragma unroll
     for (int s = 0; s < 4; ++s) cmw[16 * s + c.r16] = v[s];
+  }
+}
+
+// Median rule: the probabilities of one tile, A = exp2(dot a log2(e) - c), into the per-key
+// array acol[b n + key][h][query].
+__device__ __forceinline__ void store_probs(const FwdParams& p, const BlockCtx& c, const f32x4_t acc[4], int kt,
+                                            const float cq[4]) {
+  float* ac = p.acol + (int64_t)c.b * c.n * p.H * c.n;
+  const int qw = c.qt * kTile + c.wave * 16 + 4 * c.g;
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    const int key = kt * kTile + 16 * s + c.r16;
+    if (key < c.n) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (qw + i < c.n)
+          ac[((int64_t)key * p.H + c.h) * c.n + qw + i] = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq[i]));
+    }
   }
 }
 
@@ -560,16 +587,23 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   }
   store_row_c(p, c, cq);
 
-  // column max of the block's valid queries, every tile in its own LDS slot (one barrier)
+  // column max (or, mean rule, column sum) of the block's valid queries, every tile in its
+  // own LDS slot (one barrier); median rule: every probability to acol as well
+  const bool sum = p.importance == 1;
 #pragma unroll
-  for (int kt = 0; kt < NT; ++kt)
-    if (kt < c.ntl) tile_colmax(acc[kt], cc, cm[kt][c.wave], c);
+  for (int kt = 0; kt < NT; ++kt) {
+    if (kt < c.ntl) {
+      tile_colmax(acc[kt], cc, cm[kt][c.wave], c, sum);
+      if (p.acol) store_probs(p, c, acc[kt], kt, cq);
+    }
+  }
   lds_barrier();
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
   for (int e = c.tid; e < c.ntl * kTile; e += kThreads) {
     const int kt = e / kTile, k = e % kTile;
-    const float v = max_sel(max_sel(cm[kt][0][k], cm[kt][1][k]), max_sel(cm[kt][2][k], cm[kt][3][k]));
-    if (e < c.n) part[(int64_t)e * p.nparts] = exp2_fast(v);
+    const float v = sum ? (cm[kt][0][k] + cm[kt][1][k]) + (cm[kt][2][k] + cm[kt][3][k])
+                        : exp2_fast(max_sel(max_sel(cm[kt][0][k], cm[kt][1][k]), max_sel(cm[kt][2][k], cm[kt][3][k])));
+    if (e < c.n) part[(int64_t)e * p.nparts] = v;
   }
 }
 
@@ -644,6 +678,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
       if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
     }
   }
+  const bool sum = p.importance == 1;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
   for (int t = 0; t < nvis; ++t) {
     const int kt = tile_at(c, t);
@@ -660,12 +695,14 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
       for (int i = 0; i < 4; ++i)
         if (!key_ok_q<BAND>(c, rq, kt, lim, s, i)) acc[s][i] = -INFINITY;
-    tile_colmax(acc, cc, cmk[c.wave], c);
+    tile_colmax(acc, cc, cmk[c.wave], c, sum);
+    if (p.acol) store_probs(p, c, acc, kt, cq);
     lds_barrier();
     if (c.tid < kTile) {
-      const float v = max_sel(max_sel(cmk[0][c.tid], cmk[1][c.tid]), max_sel(cmk[2][c.tid], cmk[3][c.tid]));
+      const float v = sum ? (cmk[0][c.tid] + cmk[1][c.tid]) + (cmk[2][c.tid] + cmk[3][c.tid])
+                          : exp2_fast(max_sel(max_sel(cmk[0][c.tid], cmk[1][c.tid]), max_sel(cmk[2][c.tid], cmk[3][c.tid])));
       const int key = kt * kTile + c.tid;
-      if (key < c.n) part[(int64_t)key * p.nparts] = exp2_fast(v);
+      if (key < c.n) part[(int64_t)key * p.nparts] = v;
     }
   }
 }

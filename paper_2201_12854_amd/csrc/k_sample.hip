@@ -56,6 +56,114 @@ __device__ __forceinline__ void write_zero4(const FwdParams& p, int64_t off) {
   if (p.enc_out) *reinterpret_cast<float4*>(p.enc_out + off) = make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
+// Sum over the 64 lanes in a fixed order (DPP within rows of 16, then the four rows).
+__device__ __forceinline__ float wave_sum(float v) {
+  v += dpp_f32<0xB1>(v);
+  v += dpp_f32<0x4E>(v);
+  v += dpp_f32<0x141>(v);
+  v += dpp_f32<0x140>(v);
+  const float a = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 0));
+  const float b = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 16));
+  const float c = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 32));
+  const float d = __builtin_bit_cast(float, __builtin_amdgcn_readlane(__builtin_bit_cast(int, v), 48));
+  return (a + b) + (c + d);
+}
+
+// Median of the N = H len values v[h n + i], h < H, i < len (all non-negative floats, so
+// their bit patterns order like the values): the value of rank (N - 1) / 2 (counting from
+// 0) by a radix select over 8-bit digits, most significant first (each pass counts the
+// values that match the digits found so far in a 256-bin histogram in the wave's LDS
+// region; the bin holding the rank gives the next digit), then, for even N, the next value
+// up from one more pass (the count of values <= it and the smallest value above it). Up to
+// 2048 values are kept in registers (32 per lane); longer columns are read again per pass.
+constexpr int kSelRegs = 32;
+
+struct ColumnValues {
+  const float* v;
+  int n, len, N;
+  float reg[kSelRegs];
+  bool cached;
+  __device__ __forceinline__ uint32_t at(int u, int lane) const {  // value u * 64 + lane (< N)
+    if (cached) return __float_as_uint(reg[u]);
+    const int idx = u * kWave + lane, h = idx / len;
+    return __float_as_uint(v[(int64_t)h * n + idx - h * len]);
+  }
+};
+
+__device__ uint32_t column_select(const ColumnValues& cv, uint32_t k, uint32_t* hist, int lane) {
+  const int rounds = (cv.N + kWave - 1) / kWave;
+  uint32_t prefix = 0u, pmask = 0u;
+  for (int shift = 24; shift >= 0; shift -= 8) {
+    for (int bb = lane; bb < 256; bb += kWave) hist[bb] = 0u;
+    wave_lds_sync();
+    for (int u = 0; u < rounds; ++u) {
+      if (u * kWave + lane < cv.N) {
+        const uint32_t x = cv.at(u, lane);
+        if ((x & pmask) == prefix) atomicAdd(hist + ((x >> shift) & 255u), 1u);
+      }
+    }
+    wave_lds_sync();
+    const uint4 hc = *reinterpret_cast<const uint4*>(hist + 4 * lane);
+    const uint32_t sum = hc.x + hc.y + hc.z + hc.w;
+    const uint32_t incl = wave_inclusive_scan<uint32_t>(sum), excl = incl - sum;
+    uint32_t d = 4u * lane, below = excl;  // the digit and the count below it, if k is in this lane's bins
+    if (k >= below + hc.x) {
+      below += hc.x;
+      ++d;
+      if (k >= below + hc.y) {
+        below += hc.y;
+        ++d;
+        if (k >= below + hc.z) {
+          below += hc.z;
+          ++d;
+        }
+      }
+    }
+    const uint64_t own = __ballot(excl <= k && k < incl);  // exactly one lane
+    const int src = __ffsll((unsigned long long)own) - 1;
+    k -= (uint32_t)__shfl((int)below, src);
+    prefix |= (uint32_t)__shfl((int)d, src) << shift;
+    pmask |= 255u << shift;
+    wave_lds_sync();  // every lane has read the histogram before the next pass clears it
+  }
+  return prefix;
+}
+
+__device__ float column_median(const float* v, int H, int n, int len, uint32_t* hist, int lane) {
+  ColumnValues cv;
+  cv.v = v;
+  cv.n = n;
+  cv.len = len;
+  cv.N = H * len;
+  cv.cached = cv.N <= kSelRegs * kWave;
+  if (cv.cached) {
+#pragma unroll
+    for (int u = 0; u < kSelRegs; ++u) {
+      const int idx = u * kWave + lane, h = idx / len;
+      cv.reg[u] = idx < cv.N ? v[(int64_t)h * n + idx - h * len] : 0.f;
+    }
+  }
+  const uint32_t N = (uint32_t)cv.N;
+  const uint32_t lo = column_select(cv, (N - 1) / 2, hist, lane);
+  if (N % 2) return __uint_as_float(lo);
+  // rank N / 2: lo again if more than N / 2 values are <= lo, else the smallest value above
+  uint32_t le = 0u, above = 0xffffffffu;
+  const int rounds = (cv.N + kWave - 1) / kWave;
+  for (int u = 0; u < rounds; ++u) {
+    if (u * kWave + lane < cv.N) {
+      const uint32_t x = cv.at(u, lane);
+      le += x <= lo ? 1u : 0u;
+      if (x > lo) above = min(above, x);
+    }
+  }
+  for (int o = 32; o >= 1; o >>= 1) {  // wave sums and minima
+    le += (uint32_t)__shfl_xor((int)le, o);
+    above = min(above, (uint32_t)__shfl_xor((int)above, o));
+  }
+  const uint32_t hi = le > N / 2 ? lo : above;
+  return (float)(0.5 * ((double)__uint_as_float(lo) + (double)__uint_as_float(hi)));
+}
+
 // Per-wave results of phase 1, shared with the block for the pooled draws.
 struct TokInfo {
   int r[kMaxWaves];     // draws of the wave's token (0: no draws)
@@ -73,8 +181,10 @@ static_assert(sizeof(TokInfo) <= kHeader, "header");
 //          float32 [d_in].
 __host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
 __host__ __device__ inline int sample_shared_bytes(int d_in, bool table) { return table ? round16(8 * d_in) : 0; }
+// (at least 1 KB: the median rule's histogram uses the region before phase 1 fills it)
 __host__ __device__ inline int sample_region_bytes(int d_in, bool table) {
-  return table ? 2 * round16(4 * d_in) : round16(8 * d_in) + round16(4 * d_in);
+  const int b = table ? 2 * round16(4 * d_in) : round16(8 * d_in) + round16(4 * d_in);
+  return b > 1024 ? b : 1024;
 }
 __host__ __device__ inline int sample_lds_bytes(int d_in, bool table, int nw) {
   return kHeader + sample_shared_bytes(d_in, table) + nw * sample_region_bytes(d_in, table);
@@ -206,7 +316,8 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   const int rin = p.r_in ? p.r_in[tk] : 0;
   const float* part = p.colmax_part + tk * p.nparts;
   float m = 0.f;
-  for (int t = lane; t < p.nparts; t += kWave) m = fmaxf(m, part[t]);
+  const bool mean_rule = p.importance == 1;
+  for (int t = lane; t < p.nparts; t += kWave) m = mean_rule ? m + part[t] : fmaxf(m, part[t]);
   const int per = (d_in + kWave - 1) / kWave;
   const int i0 = min(lane * per, d_in);
   const int nrows = min(per, d_in - i0);
@@ -247,7 +358,14 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
       }
     }
   }
-  m = wave_max(m);
+  if (mean_rule) {  // the partials are column sums: the mean over H len values
+    m = (float)((double)wave_sum(m) / ((double)p.H * (double)len));
+  } else {
+    m = wave_max(m);
+  }
+  if (p.importance == 2 && j < len)  // median of the H len probabilities of key j
+    m = column_median(p.acol + tk * (int64_t)p.H * n, p.H, n, len,
+                      reinterpret_cast<uint32_t*>(smem + region_off(d_in, TABLE, wave)), lane);
   if constexpr (TABLE) __syncthreads();  // the shared table is in LDS
 
   // 1a. sample count (Eq. 9)

@@ -38,7 +38,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 size_t align256(size_t v) { return (v + 255) & ~size_t(255); }
 
 struct Layout {
-  size_t colmax_part, row_c, henc, list, ucount, total;
+  size_t colmax_part, row_c, henc, list, ucount, acol, total;
   int qtiles, nparts;
 };
 
@@ -56,6 +56,8 @@ Layout layout_for(const mca_forward_desc& d) {
   L.list = off;
   off = align256(off + 8 * (tokens * size_t(mca::list_stride((int)d.d_in)) + size_t(mca::list_tail_pad((int)d.d_in))));
   L.ucount = off;      off = align256(off + 4 * tokens);
+  L.acol = off;        // median rule: every attention probability, per key
+  if (d.importance == MCA_IMPORTANCE_MEDIAN) off = align256(off + 4 * tokens * size_t(d.heads) * size_t(d.seq));
   L.total = off;
   return L;
 }
@@ -71,6 +73,10 @@ mca_status check_desc(const mca_forward_desc* d) {
   if (d->window < 0 || d->window % 2 != 0 || d->window > (int64_t(1) << 25))
     return fail(MCA_ERR_INVALID_ARGUMENT, "window must be 0 or an even number of keys in 2..2^25 (got %lld)",
                 (long long)d->window);
+  if (d->importance < MCA_IMPORTANCE_MAX || d->importance > MCA_IMPORTANCE_MEDIAN)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "importance %d is not an mca_importance", d->importance);
+  if (d->importance != MCA_IMPORTANCE_MAX && d->window != 0)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "the mean and median rules are defined for full attention (window 0)");
   if (!std::isfinite(d->alpha) || !(d->alpha > 0.0))
     return fail(MCA_ERR_INVALID_ARGUMENT, "alpha must be finite and > 0 (got %g)", d->alpha);
   if (d->seq > (int64_t(1) << 24) || d->batch > (int64_t(1) << 24) || d->heads > 1024 ||
@@ -224,6 +230,7 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.bf16 = desc->dtype == MCA_BF16;
   p.weight_sampling = desc->sampling == MCA_SAMPLING_WEIGHT;
   p.band_half = (int)(desc->window / 2);
+  p.importance = desc->importance;
   p.qtiles = L.qtiles;
   p.nparts = L.nparts;
   p.din_pad = (int)mca::prepared_din_pad(desc->d_in);
@@ -245,6 +252,7 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   char* ws = static_cast<char*>(workspace);
   p.colmax_part = reinterpret_cast<float*>(ws + L.colmax_part);
   p.row_c = reinterpret_cast<float*>(ws + L.row_c);
+  p.acol = desc->importance == MCA_IMPORTANCE_MEDIAN ? reinterpret_cast<float*>(ws + L.acol) : nullptr;
   p.Henc = ws + L.henc;
   p.list = reinterpret_cast<uint2*>(ws + L.list);
   p.ucount = reinterpret_cast<int32_t*>(ws + L.ucount);

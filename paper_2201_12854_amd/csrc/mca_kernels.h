@@ -39,6 +39,7 @@ struct FwdParams {
   int weight_sampling;  // 0: Eq. 4, p_ji ~ |x_ji| rho_i; 1: Eq. 6, p_i ~ rho_i^2
   int band_half;        // local window: query q attends keys within band_half of q and the
                         // first token attends and is attended by all (0: full attention)
+  int importance;       // per-key statistic of the count rule: 0 max, 1 mean, 2 median
   int qtiles;   // query tiles per sequence = ceil(n / kQueryTile)
   int nparts;   // column-max partials per token = H * qtiles
   int din_pad;  // row length of W_v^T
@@ -57,6 +58,7 @@ struct FwdParams {
   int32_t* r;
   // workspace
   float* colmax_part;  // [B*n][nparts]: max of A over one (head, query tile) block, per key
+  float* acol;         // median rule: [B*n][H][n] A[h][query][key] per key (else null)
   float* row_c;        // [B*H*n] softmax normaliser of a query row in base-2 units:
                        // M + log2(sum of exp2(logit - M)), M the largest logit
   void* Henc;          // [B*n*d_out] H~ in the input dtype

@@ -73,6 +73,15 @@ def test_workspace_size_formula():
               + a(4 * tokens))
     assert got == expect
     assert mca.workspace_size(_desc(dtype_code=0)) > got  # float32 H~
+    # median rule: every probability per key, 4 B n H n more
+    d = _desc()
+    d.importance = binding.MCA_IMPORTANCE_MEDIAN
+    assert mca.workspace_size(d) == expect + a(4 * tokens * H * n)
+    d.importance = binding.MCA_IMPORTANCE_MEAN
+    assert mca.workspace_size(d) == expect
+    d.window = 64  # a window only with the max rule
+    with pytest.raises(binding.MCAError):
+        mca.workspace_size(d)
 
 
 def test_prepared_size_formula():
@@ -102,6 +111,8 @@ def test_prepared_size_formula():
     ("window", -2, binding.MCA_ERR_INVALID_ARGUMENT),
     ("window", 3, binding.MCA_ERR_INVALID_ARGUMENT),
     ("window", 1 << 26, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("importance", 3, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("importance", -1, binding.MCA_ERR_INVALID_ARGUMENT),
 ])
 def test_desc_validation(field, value, status):
     d = _desc()

@@ -30,14 +30,14 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token"):
+def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", importance="max"):
     """Oracle vs GPU on every stage; returns (#ambiguous tokens, #sampled tokens)."""
     print(f"[case] {L.name} dtype={L.dtype} B={L.batch} n={L.seq} d_in={L.d_in} H={L.heads} "
-          f"alpha={alpha} seed={seed} sampling={sampling} window={L.window}", flush=True)
+          f"alpha={alpha} seed={seed} sampling={sampling} window={L.window} importance={importance}", flush=True)
     ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed, want_samples=True, sampling=sampling,
-                             window=L.window)
+                             window=L.window, importance=importance)
     t = to_device(L, dev)
-    g = run_gpu(L, dev, alpha, seed, tensors=t, sampling=sampling)
+    g = run_gpu(L, dev, alpha, seed, tensors=t, sampling=sampling, importance=importance)
     assert np.array_equal(g["rho"], ref["rho"])
     valid = np.arange(L.seq)[None, :] < L.lens[:, None]
     m_ref = ref["m"]
@@ -52,7 +52,8 @@ def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token"):
     if check_e2e_y and not amb.any():
         assert row_rel_err(g["Y"], ref["Y"], L.lens) <= TOL_Y[L.dtype]
     # counts fixed to the oracle's: indices, coefficients, H~ and Y
-    g2 = run_gpu(L, dev, alpha, seed, r_in=ref["r"], export_samples=True, tensors=t, sampling=sampling)
+    g2 = run_gpu(L, dev, alpha, seed, r_in=ref["r"], export_samples=True, tensors=t, sampling=sampling,
+                 importance=importance)
     assert np.array_equal(g2["r"], ref["r"])
     n_tok = compare_samples(g2, ref, L)
     assert row_rel_err(g2["H"], ref["Htilde"], L.lens) <= TOL_H
@@ -369,3 +370,26 @@ def test_stack_layers_match_oracle(dev, dtype):
     # the exact stack (every count at d_in) equals the regular-mode layers: no samples drawn
     ex = enc.forward(x, lens, 0.4, 5, exact=True)
     assert torch.isfinite(ex.float()).all()
+
+
+# ------------------------------------------------------------------ mean / median rules
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("rule", ["mean", "median"])
+def test_importance_rules_small_ragged(dev, dtype, rule):
+    # resident kernels; 4 heads x lengths 40 and 23 (H len even and odd for the median)
+    L = wl.make_layer(2, 40, 96, 4, dtype, data_seed=5, lens=np.array([40, 23]), q_scale=3.0,
+                      token_scale_sigma=0.5)
+    for alpha in (0.2, 0.05):
+        _full_check(L, dev, alpha, seed=11, importance=rule)
+
+
+@pytest.mark.parametrize("rule", ["mean", "median"])
+def test_importance_rules_streaming(dev, rule):
+    L = wl.make_layer(2, 300, 128, 4, "bf16", data_seed=6, lens=np.array([300, 181]), q_scale=2.0,
+                      token_scale_sigma=0.5)
+    _full_check(L, dev, 0.1, seed=3, importance=rule)
+
+
+@pytest.mark.parametrize("rule", ["mean", "median"])
+def test_importance_rules_bert_base(dev, rule):
+    _full_check(wl.bert_base_bf16(), dev, 0.2, seed=0, importance=rule)
