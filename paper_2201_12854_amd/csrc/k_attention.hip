@@ -305,6 +305,16 @@ __device__ __forceinline__ bool key_ok(const BlockCtx& c, int kt, int lim, int s
   }
 }
 
+// The same for the output pass's probabilities (S^T layout): masked keys get 0.
+template <bool BAND>
+__device__ __forceinline__ void mask_tile(f32x4_t acc[4], const BlockCtx& c, int kt, int lim) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (!key_ok<BAND>(c, kt, lim, s, i)) acc[s][i] = 0.f;
+}
+
 // Weight of the lane's query in the column max: 1 (full attention) or |S_q| (local
 // window); 0 for padded queries.
 template <bool BAND>
@@ -405,6 +415,18 @@ __device__ __forceinline__ bool key_ok_q(const BlockCtx& c, const RowQ& rq, int 
   } else {
     return lim >= kTile || 16 * s + c.r16 < lim;
   }
+}
+
+// Masks the scores of a tile the lane's queries do not all attend (a partial last tile, a
+// local window): called only for such tiles, so that full tiles pay no per-key test.
+template <bool BAND>
+__device__ __forceinline__ void mask_tile_q(f32x4_t acc[4], const BlockCtx& c, const RowQ& rq, int kt, int lim,
+                                            float fill) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s)
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      if (!key_ok_q<BAND>(c, rq, kt, lim, s, i)) acc[s][i] = fill;
 }
 
 // Offset of the column-max argument of query i: c (full attention) or c - log2 |S_q|
@@ -556,7 +578,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
+        for (int i = 0; i < 4; ++i) {  // a select per key: cheaper here than a branch per tile
           const float d = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[kt][s][i] : -INFINITY;
           acc[kt][s][i] = d;
           dmax[i] = max_sel(dmax[i], d);
@@ -637,12 +659,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     f32x4_t acc[4];
     score_tile_qk(acc, buf, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
+    if (BAND || lim < kTile) mask_tile_q<BAND>(acc, c, rq, kt, lim, -INFINITY);  // tile-uniform
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       float d[4], dm = -INFINITY;
 #pragma unroll
       for (int s = 0; s < 4; ++s) {
-        d[s] = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[s][i] : -INFINITY;
+        d[s] = acc[s][i];
         dm = max_sel(dm, d[s]);
       }
       const float Mn = max_sel(M[i], __fmul_rn(dm, kLog2eOver8));
@@ -690,11 +713,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     f32x4_t acc[4];
     score_tile_qk(acc, buf, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
-#pragma unroll
-    for (int s = 0; s < 4; ++s)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (!key_ok_q<BAND>(c, rq, kt, lim, s, i)) acc[s][i] = -INFINITY;
+    if (BAND || lim < kTile) mask_tile_q<BAND>(acc, c, rq, kt, lim, -INFINITY);  // tile-uniform
     tile_colmax(acc, cc, cmk[c.wave], c, sum);
     if (p.acol) store_probs(p, c, acc, kt, cq);
     lds_barrier();
@@ -751,10 +770,8 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float pr = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq));
-          acc[s][i] = key_ok<BAND>(c, kt, lim, s, i) ? pr : 0.f;
-        }
+        for (int i = 0; i < 4; ++i) acc[s][i] = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq));
+      if (BAND || lim < kTile) mask_tile<BAND>(acc, c, kt, lim);  // tile-uniform
       pv_tile(y, acc, Vs[kt], c.r16, c.g);
     }
   }
@@ -801,10 +818,8 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
 #pragma unroll
     for (int s = 0; s < 4; ++s)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float pr = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq));
-        acc[s][i] = key_ok<BAND>(c, kt, lim, s, i) ? pr : 0.f;
-      }
+      for (int i = 0; i < 4; ++i) acc[s][i] = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq));
+    if (BAND || lim < kTile) mask_tile<BAND>(acc, c, kt, lim);  // tile-uniform
     pv_tile(y, acc, vb, c.r16, c.g);
   }
   store_y(p, c, y);
