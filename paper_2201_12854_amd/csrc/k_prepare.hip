@@ -14,29 +14,41 @@ namespace {
 template <int BF> struct Elem { using T = float; };
 template <> struct Elem<1> { using T = uint16_t; };
 
-// rho_i = float32(sqrt(sum_c W[i, c]^2)), float64 running sum in column order. One wave
-// per 64 rows; 64x64 tiles go through LDS so global reads are coalesced.
+// rho_i = float32(sqrt(sum_c W[i, c]^2)), float64 running sum in column order. A block of
+// four waves per 64 rows: the waves load 64 x 64 tiles together (coalesced, the next tile
+// in registers while the current one is summed) and wave 0 runs the 64 row sums, one row
+// per lane, in column order.
 template <int BF>
-__global__ __launch_bounds__(64) void k_rownorm(const void* Wp, int d_in, int d_out, float* rownorm) {
+__global__ __launch_bounds__(256) void k_rownorm(const void* Wp, int d_in, int d_out, float* rownorm) {
   using T = typename Elem<BF>::T;
   __shared__ double tile[64][65];
   const T* W = static_cast<const T*>(Wp);
-  const int r0 = blockIdx.x * 64, lane = threadIdx.x;
+  const int r0 = blockIdx.x * 64, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  double nxt[16];
+  auto load = [&](int c0) {
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int row = r0 + 16 * wave + j, c = c0 + lane;
+      nxt[j] = (row < d_in && c < d_out) ? (double)load_f32(W, (int64_t)row * d_out + c) : 0.0;
+    }
+  };
   double s = 0.0;
+  load(0);
   for (int c0 = 0; c0 < d_out; c0 += 64) {
-    for (int rr = 0; rr < 64; ++rr) {
-      const int row = r0 + rr, c = c0 + lane;
-      tile[rr][lane] = (row < d_in && c < d_out) ? (double)load_f32(W, (int64_t)row * d_out + c) : 0.0;
+#pragma unroll
+    for (int j = 0; j < 16; ++j) tile[16 * wave + j][lane] = nxt[j];
+    __syncthreads();
+    if (c0 + 64 < d_out) load(c0 + 64);  // in flight during the sums
+    if (wave == 0) {
+      const int cend = min(64, d_out - c0);
+      for (int cc = 0; cc < cend; ++cc) {
+        const double v = tile[lane][cc];
+        s = __dadd_rn(s, __dmul_rn(v, v));  // v*v is exact in float64
+      }
     }
-    lds_barrier();
-    const int cend = min(64, d_out - c0);
-    for (int cc = 0; cc < cend; ++cc) {
-      const double v = tile[lane][cc];
-      s = __dadd_rn(s, __dmul_rn(v, v));  // v*v is exact in float64
-    }
-    lds_barrier();
+    __syncthreads();
   }
-  if (r0 + lane < d_in) rownorm[r0 + lane] = (float)sqrt(s);
+  if (wave == 0 && r0 + lane < d_in) rownorm[r0 + lane] = (float)sqrt(s);
 }
 
 // W_v^T in MFMA fragment order (layout in mca_kernels.h): one thread per 16-byte chunk;
@@ -115,10 +127,10 @@ hipError_t launch_prepare(const void* W, int bf16, int d_in, int d_out, void* pr
   const dim3 g1((d_in + 63) / 64);
   const dim3 g2((unsigned)((nchunks + 255) / 256));
   if (bf16) {
-    hipLaunchKernelGGL(k_rownorm<1>, g1, dim3(64), 0, s, W, d_in, d_out, rownorm);
+    hipLaunchKernelGGL(k_rownorm<1>, g1, dim3(256), 0, s, W, d_in, d_out, rownorm);
     hipLaunchKernelGGL(k_fragment_wt<1>, g2, dim3(256), 0, s, W, d_in, d_out, nks, nchunks, Wt);
   } else {
-    hipLaunchKernelGGL(k_rownorm<0>, g1, dim3(64), 0, s, W, d_in, d_out, rownorm);
+    hipLaunchKernelGGL(k_rownorm<0>, g1, dim3(256), 0, s, W, d_in, d_out, rownorm);
     hipLaunchKernelGGL(k_fragment_wt<0>, g2, dim3(256), 0, s, W, d_in, d_out, nks, nchunks, Wt);
   }
   if (d_in > 2048) return hipErrorInvalidValue;
