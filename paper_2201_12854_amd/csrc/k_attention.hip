@@ -1,26 +1,28 @@
 // Attention stages of the MCA forward pass on gfx950:
 //   scores + row softmax statistics + column max   (softmax(a Q K^T), a = 1/8, and the
-//                                                    per-block part of max A[:, j], Eq. 8/9)
+//                                                    per-block part of max A[:, j], Eq. 8/9;
+//                                                    or of the column sum (mean rule), or
+//                                                    every probability (median rule))
 //   Y = A H~                                        ("Y = AH", Sec. "Self-Attention
 //                                                    Mechanisms"; Eq. 5 outer sum)
-// Both kernels rebuild the score tiles from Q and K with one shared routine and the same
-// row statistics, so the attention probabilities that set the sample counts are bitwise
-// the ones multiplied into H~. A is never written to memory.
+// Both kernels compute a probability the same way, A = exp2(fma(q . k, log2(e)/8, -c))
+// with the row normaliser c written by the score pass. A is never written to memory
+// (except under the median rule).
 //
 // Tiling: one block = 4 waves = 64 queries of one (batch row, head); a wave owns 16
-// queries. Keys come in tiles of 64 staged in LDS. Scores are computed transposed,
-// S^T = K Q^T, with 16x16 MFMA tiles (bf16 16x16x32 or fp32 16x16x4), so after the score
-// MFMA lane l holds the scores of query (l % 16) for keys 16 s + 4 (l / 16) + i
-// (s, i = 0..3): exactly the A-operand layout of the P V MFMA, with no data movement
-// between the two products.
+// queries. Keys come in tiles of 64 staged in LDS; 16x16 MFMA tiles (bf16 16x16x32 or
+// fp32 16x16x4). The score pass computes S = Q K^T (its layout and reductions are
+// described with the kernels). The output pass computes S^T = K Q^T, so lane l holds the
+// scores of query (l % 16) for keys 16 s + 4 (l / 16) + i (s, i = 0..3): exactly the
+// A-operand layout of the P V MFMA, with no data movement between the two products.
 //
 // Two variants of each kernel:
 //   resident (padded length <= 64 NT keys): every K (and H~) tile of the sequence is
 //     loaded at once behind one barrier and all scores stay in registers, so the
 //     statistics and the column max come from a single pass;
 //   streaming (longer sequences): tiles are double buffered in LDS with the next tile
-//     prefetched into registers; the score pass sweeps twice (online statistics, then
-//     probabilities).
+//     prefetched into registers; the score pass sweeps twice (online statistics, then the
+//     column statistic).
 // Local-window attention (Sec. "Longformer": a window of w keys around each token and a
 // global first token): query q attends key k < len when |q - k| <= w / 2, or q = 0, or
 // k = 0; the other scores are masked like padded keys. The column max is then taken of

@@ -4,7 +4,9 @@
 //   sampled token (0 < r_j < d_in): H~[j] = sum over its distinct sampled rows i of
 //     coef_i W_v[i, :] (Eq. 2 with duplicates merged; Eq. 5 inner sum), float32
 //     accumulation;
-//   saturated token (r_j = d_in): H~[j] = x_j W_v exactly, on MFMA (16 tokens per tile).
+//   saturated token (r_j = d_in): H~[j] = x_j W_v exactly, on MFMA (16 tokens per tile),
+//     here when the slice's B operand fits in LDS next to it (bfloat16, d_in <= 768),
+//     otherwise in the kernels of the saturated-token section below (their own launch).
 //
 // The slice W_v[:, c0 .. c0 + WC) is converted to float32 once and kept in LDS for the
 // whole block (768 x 32 floats = 96 KB: the 160 KB LDS of a gfx950 CU holds it), so the
