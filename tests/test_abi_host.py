@@ -173,3 +173,11 @@ def test_binding_fails_loudly_without_library(tmp_path):
             binding.load_library(str(tmp_path / "missing.so"))
         finally:
             binding._lib = binding._lib_saved
+
+
+def test_binding_rejects_unknown_rule_names():
+    with pytest.raises(ValueError):
+        binding._importance_code("mode")
+    with pytest.raises(ValueError):
+        binding._sampling_code("rows")
+    assert [binding._importance_code(r) for r in ("max", "mean", "median")] == [0, 1, 2]

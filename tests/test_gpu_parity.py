@@ -393,3 +393,12 @@ def test_importance_rules_streaming(dev, rule):
 @pytest.mark.parametrize("rule", ["mean", "median"])
 def test_importance_rules_bert_base(dev, rule):
     _full_check(wl.bert_base_bf16(), dev, 0.2, seed=0, importance=rule)
+
+
+@pytest.mark.parametrize("rule", ["mean", "median"])
+def test_importance_rules_single_token_row_and_eq6(dev, rule):
+    # a row of one valid token (H len = H values), fp32, and the Eq. 6 probability
+    L = wl.make_layer(3, 24, 64, 4, "f32", data_seed=9, lens=np.array([24, 1, 13]), q_scale=2.0,
+                      token_scale_sigma=0.5)
+    _full_check(L, dev, 0.1, seed=2, importance=rule)
+    _full_check(L, dev, 0.1, seed=2, importance=rule, sampling="weight")
