@@ -490,6 +490,14 @@ def main():
                            "reduction_vs_dense_xw": float(L.tokens * L.d_in) / float(rr.sum())}
             log(f"mca forward, {rule} rule: {ms_r * 1e3:.1f} us/step, mean r {rules[rule]['mean_r']:.1f}")
         record["importance_rules"] = rules
+        # the paper's regular mode through the same kernels: every count at d_in, so every
+        # token is encoded exactly on MFMA (the exact layer, computed by this library)
+        r_full = torch.full((L.batch, L.seq), L.d_in, dtype=torch.int32, device=dev)
+        pe = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
+                             seq_lens=lens, r_in=r_full)
+        ms_e, _ = time_loop(pe.run, args.steps, args.warmup)
+        record["regular_mode"] = {"ms_per_step": ms_e, "tokens_per_s": L.tokens / (ms_e * 1e-3)}
+        log(f"regular mode (exact, same kernels): {ms_e * 1e3:.1f} us/step")
         # dense stages at the MFMA-bound shapes
         record["dense_stages"] = dense_stage_extras(mca, wl, dev, args.alpha, args.seed, 20)
         # error growth over a 12-layer stack
