@@ -498,6 +498,23 @@ def main():
         ms_e, _ = time_loop(pe.run, args.steps, args.warmup)
         record["regular_mode"] = {"ms_per_step": ms_e, "tokens_per_s": L.tokens / (ms_e * 1e-3)}
         log(f"regular mode (exact, same kernels): {ms_e * 1e3:.1f} us/step")
+        # tokens whose count reaches k encoded exactly on MFMA as well (the estimate of the
+        # others unchanged): where that pays on this chip
+        hyb = {}
+        for k in (32, 64, 128, 256):
+            ph = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, args.alpha, args.seed, heads=L.heads,
+                                 seq_lens=lens, exact_from=k)
+            ms_h, _ = time_loop(ph.run, args.steps, args.warmup)
+            torch.cuda.synchronize()
+            rh = ph.r.cpu().numpy()
+            exact = (rh >= k) | (rh >= L.d_in)
+            sampled_r = rh[(rh > 0) & ~exact]
+            macs = float(exact.sum()) * L.d_in + float(sampled_r.sum())  # X W_v rows: exact d_in, sampled r_j
+            hyb[str(k)] = {"ms_per_step": ms_h, "tokens_per_s": L.tokens / (ms_h * 1e-3),
+                           "exact_tokens_frac": float(exact.mean()),
+                           "reduction_vs_dense_xw": float(L.tokens * L.d_in) / macs}
+            log(f"exact from r >= {k}: {ms_h * 1e3:.1f} us/step, {100 * exact.mean():.0f}% of tokens exact")
+        record["exact_from"] = hyb
         # dense stages at the MFMA-bound shapes
         record["dense_stages"] = dense_stage_extras(mca, wl, dev, args.alpha, args.seed, 20)
         # error growth over a 12-layer stack

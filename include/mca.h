@@ -126,6 +126,10 @@ typedef struct mca_forward_desc {
      (window = 0). MCA_IMPORTANCE_MAX is Eq. 8-9; the mean and the median are the more
      aggressive schemes the paper names after Eq. 8 (no error bound is proved for them). */
   int32_t importance;
+  /* 0: tokens are encoded exactly (x_j W_v on MFMA) only when saturated (r_j = d_in).
+     k > 0: also every token with r_j >= k, as its exact value costs less on the matrix
+     cores than a long sampled list on the vector units (r_j is still reported). */
+  int32_t exact_from;
 } mca_forward_desc;
 
 /*
@@ -190,7 +194,7 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  * matter and are overwritten.
  * Errors: MCA_ERR_INVALID_ARGUMENT (null required pointer, size < 1, non-finite or
  * non-positive alpha, unknown sampling mode, odd or negative window, unknown importance rule or
- * a mean/median rule with a window, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
+ * a mean/median rule with a window, negative exact_from, misaligned pointer), MCA_ERR_UNSUPPORTED (d_head
  * != 64, d_out not a multiple of 256 or > 2048, d_in > 2048), MCA_ERR_WORKSPACE_TOO_SMALL,
  * MCA_ERR_HIP.
  */

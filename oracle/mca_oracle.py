@@ -296,13 +296,15 @@ def estimate_from_indices(x: np.ndarray, W: np.ndarray, w, T: int, idx, r: int) 
     return out
 
 
-def encode_token(x, W, rho, r: int, seed: int, b: int, j: int, *, sampling=SAMPLING_TOKEN, table=None):
+def encode_token(x, W, rho, r: int, seed: int, b: int, j: int, *, sampling=SAMPLING_TOKEN, table=None,
+                 exact_from: int = 0):
     """H~[j] for one token. Returns (H~[j], indices, coefficients). In Eq. 6 mode
-    ``table`` is weight_fixed_point(rho) (computed here when not given)."""
+    ``table`` is weight_fixed_point(rho) (computed here when not given). ``exact_from``
+    > 0 encodes every token with r >= exact_from exactly as well (no draws)."""
     d_in = W.shape[0]
     if r <= 0:
         return np.zeros(W.shape[1]), [], np.zeros(0)
-    if r >= d_in:  # O8: saturated, exact encoding
+    if r >= d_in or (exact_from > 0 and r >= exact_from):  # O8: saturated, exact encoding
         return np.asarray(x, np.float64) @ np.asarray(W, np.float64), [], np.zeros(0)
     if sampling == SAMPLING_WEIGHT:
         fp = table if table is not None else weight_fixed_point(rho)
@@ -321,7 +323,7 @@ def encode_token(x, W, rho, r: int, seed: int, b: int, j: int, *, sampling=SAMPL
 # --------------------------------------------------------------------------- forward
 def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_override=None,
                 rho=None, y_rows=None, want_samples=False, want_exact=False, sampling=SAMPLING_TOKEN,
-                window: int = 0, importance: str = IMPORTANCE_MAX):
+                window: int = 0, importance: str = IMPORTANCE_MAX, exact_from: int = 0):
     """Full MCA forward (O1-O9) for right-padded sequences.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W: [d_in, heads*64] (all float32
@@ -335,12 +337,16 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
     SAMPLING_WEIGHT (Eq. 6, one table per weight matrix). ``window`` > 0 selects
     local-window attention with a global first token (see ``attended``). ``importance``
     selects the per-key statistic of the count rule (``column_importance``; full
-    attention only for the mean and median).
+    attention only for the mean and median). ``exact_from`` > 0: tokens whose count
+    reaches it are encoded exactly, like saturated ones (their counts are still reported;
+    0 keeps exact encoding for r = d_in only, the paper's case).
     """
     if window < 0 or window % 2:
         raise ValueError("window must be 0 (full attention) or a positive even number of keys")
     if importance != IMPORTANCE_MAX and window:
         raise ValueError("the mean and median rules are defined for full attention")
+    if exact_from < 0:
+        raise ValueError("exact_from must be >= 0")
     B, n, d_in = X.shape
     d_out = W.shape[1]
     lens = np.asarray(lens)
@@ -362,7 +368,8 @@ def mca_forward(Q, K, X, W, lens, heads: int, alpha: float, seed: int, *, r_over
     samples = {}
     for b in range(B):
         for j in range(n):
-            H, idx, coef = encode_token(X[b, j], W, rho, int(r[b, j]), seed, b, j, sampling=sampling, table=table)
+            H, idx, coef = encode_token(X[b, j], W, rho, int(r[b, j]), seed, b, j, sampling=sampling, table=table,
+                                        exact_from=exact_from)
             Ht[b, j] = H
             if want_samples:
                 samples[(b, j)] = (idx, coef)

@@ -63,6 +63,7 @@ class ForwardDesc(ctypes.Structure):
         ("profiler", ctypes.c_void_p),
         ("window", ctypes.c_int64),
         ("importance", ctypes.c_int32),
+        ("exact_from", ctypes.c_int32),
     ]
 
 
@@ -141,7 +142,7 @@ def _stream_handle(device) -> int:
 
 def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None, r_in=None,
               colmax_out=None, sample_idx_out=None, sample_coef_out=None, encoded_out=None,
-              profiler=None, sampling=0, window=0, importance=0) -> ForwardDesc:
+              profiler=None, sampling=0, window=0, importance=0, exact_from=0) -> ForwardDesc:
     d = ForwardDesc()
     d.batch, d.seq, d.heads, d.d_head, d.d_in = batch, seq, heads, 64, d_in
     d.dtype, d.sampling = dtype_code, sampling
@@ -152,6 +153,7 @@ def make_desc(batch, seq, heads, d_in, dtype_code, alpha, seed, *, seq_lens=None
     d.profiler = None if profiler is None else profiler.handle
     d.window = int(window)
     d.importance = int(importance)
+    d.exact_from = int(exact_from)
     return d
 
 
@@ -202,7 +204,7 @@ class ForwardResult:
 def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int,
                       seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
                       workspace=None, out=None, profiler=None, sampling: str = "token",
-                      window: int = 0, importance: str = "max") -> ForwardResult:
+                      window: int = 0, importance: str = "max", exact_from: int = 0) -> ForwardResult:
     """One MCA forward pass through libmca on the current HIP stream.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
@@ -214,7 +216,8 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     "weight" (Eq. 6, the paper's input-independent probability). ``window``: 0 for full
     attention, or an even local window (keys within window / 2 of each query, plus a
     global first token). ``importance``: "max" (Eq. 8-9), "mean" or "median", the per-key
-    statistic of the count rule (full attention).
+    statistic of the count rule (full attention). ``exact_from`` > 0: tokens with
+    r_j >= exact_from are encoded exactly on MFMA too.
     """
     import torch
 
@@ -246,7 +249,7 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
                      colmax_out=res.colmax, sample_idx_out=res.sample_idx,
                      sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler,
                      sampling=_sampling_code(sampling), window=window,
-                     importance=_importance_code(importance))
+                     importance=_importance_code(importance), exact_from=exact_from)
     ws_bytes = workspace_size(desc)
     if workspace is None or workspace.numel() < ws_bytes:
         workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
@@ -295,7 +298,8 @@ class ForwardPlan:
     stream), so that ``run()`` is a single C call: for timing loops and serving."""
 
     def __init__(self, Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int, seq_lens=None,
-                 r_in=None, profiler=None, sampling: str = "token", window: int = 0, importance: str = "max"):
+                 r_in=None, profiler=None, sampling: str = "token", window: int = 0, importance: str = "max",
+                 exact_from: int = 0):
         import torch
 
         lib = load_library()
@@ -305,7 +309,7 @@ class ForwardPlan:
         self._keep = (Q, K, X, W_v, prepared, seq_lens, r_in)
         self.desc = make_desc(B, n, heads, d_in, _dtype_code(X), alpha, seed, seq_lens=seq_lens, r_in=r_in,
                               profiler=profiler, sampling=_sampling_code(sampling), window=window,
-                              importance=_importance_code(importance))
+                              importance=_importance_code(importance), exact_from=exact_from)
         ws = workspace_size(self.desc)
         self.workspace = torch.empty(max(ws, 1), dtype=torch.uint8, device=dev)
         self.Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)

@@ -468,7 +468,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
       const int r = (RV), uc = (UV);                                                           \
       const int len = min(uc & 0xffff, stride);                                                \
       const int nepad = min(min((uc >> 16) & 0xffff, len), 2046) & ~1;                         \
-      if (r >= d_in) {                                                                         \
+      if (exact_token(r, d_in, p.exact_from)) {                                                \
         if (!p.sat_separate) satl[atomicAdd(ctr, 1)] = tid;                                    \
       } else if (r > 0 && len > 0) {                                                           \
         key = sort_key(max(nepad, len - nepad));                                               \
@@ -571,7 +571,8 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated(FwdParams p) {
   const int d_in = p.d_in;
   if (tid == 0) nsat_s = 0;
   __syncthreads();
-  if (tid < kSatTokens && t0 + tid < ntok && p.r[t0 + tid] >= d_in) satl[atomicAdd(&nsat_s, 1)] = tid;
+  if (tid < kSatTokens && t0 + tid < ntok && exact_token(p.r[t0 + tid], d_in, p.exact_from))
+    satl[atomicAdd(&nsat_s, 1)] = tid;
   __syncthreads();
   const int nsat = nsat_s;
   const int wm = wave >> 1, wn = wave & 1;
@@ -696,7 +697,8 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
   const int d_in = p.d_in;
   if (tid == 0) nsat_s = 0;
   __syncthreads();
-  if (tid < kSatTokens && t0 + tid < ntok && p.r[t0 + tid] >= d_in) satl[atomicAdd(&nsat_s, 1)] = tid;
+  if (tid < kSatTokens && t0 + tid < ntok && exact_token(p.r[t0 + tid], d_in, p.exact_from))
+    satl[atomicAdd(&nsat_s, 1)] = tid;
   __syncthreads();
   const int nsat = nsat_s;
   if (nsat == 0) return;  // block-uniform

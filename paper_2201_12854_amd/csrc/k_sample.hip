@@ -399,7 +399,7 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   } else {
     const float vmax = wave_max(lmax);
     none = !(vmax > 0.f) || !(vmax <= 3.40282347e38f);
-    if (!none && r > 0 && r < d_in) {
+    if (!none && r > 0 && !exact_token(r, d_in, p.exact_from)) {
       int e;
       (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
       const int shift = 32 - e;
@@ -431,10 +431,11 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
       }
     }
   }
-  const bool sampled = live && r > 0 && r < d_in && !none;
+  const bool exact = exact_token(r, d_in, p.exact_from);  // encoded on MFMA by the gather or its own kernel
+  const bool sampled = live && r > 0 && !exact && !none;
   if (live && !sampled) {
     if (lane == 0) p.ucount[tok] = 0;
-    if (r < d_in)
+    if (!exact)
       for (int c = 4 * lane; c < p.d_out; c += 4 * kWave) write_zero4<BF>(p, tok * p.d_out + c);
   }
   if (sampled) {

@@ -75,6 +75,7 @@ mca_status check_desc(const mca_forward_desc* d) {
                 (long long)d->window);
   if (d->importance < MCA_IMPORTANCE_MAX || d->importance > MCA_IMPORTANCE_MEDIAN)
     return fail(MCA_ERR_INVALID_ARGUMENT, "importance %d is not an mca_importance", d->importance);
+  if (d->exact_from < 0) return fail(MCA_ERR_INVALID_ARGUMENT, "exact_from must be >= 0 (got %d)", d->exact_from);
   if (d->importance != MCA_IMPORTANCE_MAX && d->window != 0)
     return fail(MCA_ERR_INVALID_ARGUMENT, "the mean and median rules are defined for full attention (window 0)");
   if (!std::isfinite(d->alpha) || !(d->alpha > 0.0))
@@ -231,6 +232,7 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   p.weight_sampling = desc->sampling == MCA_SAMPLING_WEIGHT;
   p.band_half = (int)(desc->window / 2);
   p.importance = desc->importance;
+  p.exact_from = desc->exact_from;
   p.qtiles = L.qtiles;
   p.nparts = L.nparts;
   p.din_pad = (int)mca::prepared_din_pad(desc->d_in);

@@ -40,6 +40,7 @@ struct FwdParams {
   int band_half;        // local window: query q attends keys within band_half of q and the
                         // first token attends and is attended by all (0: full attention)
   int importance;       // per-key statistic of the count rule: 0 max, 1 mean, 2 median
+  int exact_from;       // > 0: tokens with r >= exact_from are encoded exactly too
   int qtiles;   // query tiles per sequence = ceil(n / kQueryTile)
   int nparts;   // column-max partials per token = H * qtiles
   int din_pad;  // row length of W_v^T
@@ -88,6 +89,12 @@ inline hipError_t launch_stage_kernel(K kernel, dim3 grid, dim3 block, size_t ld
   if (p.ev_start) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, p.ev_start, p.ev_stop, 0u, p);
   else hipLaunchKernelGGL(kernel, grid, block, lds, s, p);
   return hipGetLastError();
+}
+
+// A token encoded exactly (x_j W_v on MFMA) rather than sampled: saturated (r = d_in), or
+// r >= exact_from when that is set.
+__host__ __device__ inline bool exact_token(int r, int d_in, int exact_from) {
+  return r >= d_in || (exact_from > 0 && r >= exact_from);
 }
 
 hipError_t launch_scores_colmax(const FwdParams& p, hipStream_t s);

@@ -33,7 +33,7 @@ def to_device(L, dev):
 
 
 def run_gpu(L, dev, alpha, seed, *, r_in=None, export=True, export_samples=False, tensors=None, prep=None,
-            sampling="token", window=None, importance="max"):
+            sampling="token", window=None, importance="max", exact_from=0):
     import torch
 
     import paper_2201_12854_amd as mca
@@ -45,7 +45,7 @@ def run_gpu(L, dev, alpha, seed, *, r_in=None, export=True, export_samples=False
     out = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], prep, alpha, seed, heads=L.heads,
                                 seq_lens=t["lens"], r_in=rin, export=export, export_samples=export_samples,
                                 sampling=sampling, window=L.window if window is None else window,
-                                importance=importance)
+                                importance=importance, exact_from=exact_from)
     torch.cuda.synchronize()
     res = {"Y": out.Y.cpu().numpy(), "r": out.r.cpu().numpy(), "rho": mca.rownorm(prep, L.d_in).cpu().numpy()}
     if export:

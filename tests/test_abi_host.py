@@ -113,6 +113,7 @@ def test_prepared_size_formula():
     ("window", 1 << 26, binding.MCA_ERR_INVALID_ARGUMENT),
     ("importance", 3, binding.MCA_ERR_INVALID_ARGUMENT),
     ("importance", -1, binding.MCA_ERR_INVALID_ARGUMENT),
+    ("exact_from", -1, binding.MCA_ERR_INVALID_ARGUMENT),
 ])
 def test_desc_validation(field, value, status):
     d = _desc()

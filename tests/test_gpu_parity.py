@@ -30,14 +30,15 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", importance="max"):
+def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", importance="max", exact_from=0):
     """Oracle vs GPU on every stage; returns (#ambiguous tokens, #sampled tokens)."""
     print(f"[case] {L.name} dtype={L.dtype} B={L.batch} n={L.seq} d_in={L.d_in} H={L.heads} "
-          f"alpha={alpha} seed={seed} sampling={sampling} window={L.window} importance={importance}", flush=True)
+          f"alpha={alpha} seed={seed} sampling={sampling} window={L.window} importance={importance} "
+          f"exact_from={exact_from}", flush=True)
     ref = oracle.mca_forward(L.Q, L.K, L.X, L.Wv, L.lens, L.heads, alpha, seed, want_samples=True, sampling=sampling,
-                             window=L.window, importance=importance)
+                             window=L.window, importance=importance, exact_from=exact_from)
     t = to_device(L, dev)
-    g = run_gpu(L, dev, alpha, seed, tensors=t, sampling=sampling, importance=importance)
+    g = run_gpu(L, dev, alpha, seed, tensors=t, sampling=sampling, importance=importance, exact_from=exact_from)
     assert np.array_equal(g["rho"], ref["rho"])
     valid = np.arange(L.seq)[None, :] < L.lens[:, None]
     m_ref = ref["m"]
@@ -53,7 +54,7 @@ def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", impo
         assert row_rel_err(g["Y"], ref["Y"], L.lens) <= TOL_Y[L.dtype]
     # counts fixed to the oracle's: indices, coefficients, H~ and Y
     g2 = run_gpu(L, dev, alpha, seed, r_in=ref["r"], export_samples=True, tensors=t, sampling=sampling,
-                 importance=importance)
+                 importance=importance, exact_from=exact_from)
     assert np.array_equal(g2["r"], ref["r"])
     n_tok = compare_samples(g2, ref, L)
     assert row_rel_err(g2["H"], ref["Htilde"], L.lens) <= TOL_H
@@ -402,3 +403,20 @@ def test_importance_rules_single_token_row_and_eq6(dev, rule):
                       token_scale_sigma=0.5)
     _full_check(L, dev, 0.1, seed=2, importance=rule)
     _full_check(L, dev, 0.1, seed=2, importance=rule, sampling="weight")
+
+
+# ------------------------------------------------------------------ exact encoding from a count
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("exact_from", [1, 20, 64])
+def test_exact_from_small_ragged(dev, dtype, exact_from):
+    # tokens with r >= exact_from take the exact MFMA path (in the gather for bf16, d_in
+    # <= 768; in its own kernel for float32), the rest are sampled
+    L = wl.make_layer(2, 40, 96, 4, dtype, data_seed=5, lens=np.array([40, 23]), q_scale=3.0,
+                      token_scale_sigma=0.5)
+    _full_check(L, dev, 0.4, seed=11, exact_from=exact_from)
+
+
+def test_exact_from_bert_base_and_large(dev):
+    _full_check(wl.bert_base_bf16(), dev, 0.4, seed=0, exact_from=128)
+    _full_check(wl.make_layer(2, 300, 1024, 4, "bf16", data_seed=12, lens=np.array([300, 140]),
+                              token_scale_sigma=0.5), dev, 0.2, seed=4, exact_from=96)
