@@ -317,49 +317,6 @@ __device__ __forceinline__ void mask_tile(f32x4_t acc[4], const BlockCtx& c, int
       if (!key_ok<BAND>(c, kt, lim, s, i)) acc[s][i] = 0.f;
 }
 
-// Weight of the lane's query in the column max: 1 (full attention) or |S_q| (local
-// window); 0 for padded queries.
-template <bool BAND>
-__device__ __forceinline__ float query_weight(const BlockCtx& c) {
-  if (c.q >= c.len) return 0.f;
-  if constexpr (BAND) {
-    return (float)(c.kspan + 1 + (c.klo > 0 ? 1 : 0));  // the window, and key 0 if outside it
-  } else {
-    return 1.f;
-  }
-}
-
-// Max over the wave's 16 queries (the 16 lanes of a row, same l / 16) of a probability.
-// Probabilities are non-negative, so their bit patterns order like the values: an
-// unsigned max with DPP operands (one instruction per step).
-__device__ __forceinline__ float max_over_queries(float a) {
-  uint32_t v = __float_as_uint(a);
-  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0xB1, 0xF, 0xF, true));   // lane ^ 1
-  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x4E, 0xF, 0xF, true));   // lane ^ 2
-  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x141, 0xF, 0xF, true));  // half-row mirror
-  v = max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, 0x140, 0xF, 0xF, true));  // row mirror
-  return __uint_as_float(v);
-}
-
-// The same for a 4 x 4 block of values, step by step over all 16 so that the dependent
-// DPP operations of one value are separated by the others (no hazard waits).
-template <int CTRL>
-__device__ __forceinline__ void max_step16(uint32_t (&v)[16]) {
-#pragma unroll
-  for (int j = 0; j < 16; ++j) v[j] = max(v[j], (uint32_t)__builtin_amdgcn_mov_dpp((int)v[j], CTRL, 0xF, 0xF, true));
-}
-__device__ __forceinline__ void max_over_queries16(float (&a)[4][4]) {
-  uint32_t v[16];
-#pragma unroll
-  for (int j = 0; j < 16; ++j) v[j] = __float_as_uint(a[j >> 2][j & 3]);
-  max_step16<0xB1>(v);
-  max_step16<0x4E>(v);
-  max_step16<0x141>(v);
-  max_step16<0x140>(v);
-#pragma unroll
-  for (int j = 0; j < 16; ++j) a[j >> 2][j & 3] = __uint_as_float(v[j]);
-}
-
 // Writes Y rows of the wave's queries: y[cc][i] = Y[query 4 g + i][column 16 cc + l % 16].
 __device__ __forceinline__ void store_y(const FwdParams& p, const BlockCtx& c, const f32x4_t y[4]) {
 #pragma unroll
