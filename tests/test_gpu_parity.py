@@ -420,3 +420,36 @@ def test_exact_from_bert_base_and_large(dev):
     _full_check(wl.bert_base_bf16(), dev, 0.4, seed=0, exact_from=128)
     _full_check(wl.make_layer(2, 300, 1024, 4, "bf16", data_seed=12, lens=np.array([300, 140]),
                               token_scale_sigma=0.5), dev, 0.2, seed=4, exact_from=96)
+
+
+def test_forward_replays_from_a_captured_graph(dev):
+    # the forward pass launches only kernels (no memset, no allocation), so a stream capture
+    # replays it: three replays with eager work between them give the eager results bitwise
+    import torch
+
+    import paper_2201_12854_amd as mca
+
+    L = wl.make_layer(4, 96, 256, 4, "bf16", data_seed=21, lens=np.array([96, 50, 1, 77]), q_scale=2.0,
+                      token_scale_sigma=0.5)
+    t = to_device(L, dev)
+    prep = mca.prepare_weights(t["Wv"])
+    s = torch.cuda.Stream()
+    with torch.cuda.stream(s):
+        plan = mca.ForwardPlan(t["Q"], t["K"], t["X"], t["Wv"], prep, 0.4, 3, heads=L.heads, seq_lens=t["lens"])
+        plan.run()
+    torch.cuda.synchronize()
+    Y0, r0 = plan.Y.clone(), plan.r.clone()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g, stream=s):
+        plan.run()
+    for k in range(3):
+        plan.Y.fill_(float("nan"))
+        plan.r.fill_(-1)
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert torch.equal(plan.r, r0) and torch.equal(plan.Y, Y0), k
+        with torch.cuda.stream(s):  # eager work between the replays
+            plan.run()
+        torch.cuda.synchronize()
+        assert torch.equal(plan.Y, Y0)
