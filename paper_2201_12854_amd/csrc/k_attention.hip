@@ -588,6 +588,98 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   }
 }
 
+// Streamed-resident variant (up to NT visited tiles, padded length <= 64 NT): K tiles are
+// streamed through two LDS buffers as in the streaming variant, but every score stays in
+// registers, so a single sweep over K gives the statistics and the column statistic (the
+// streaming variant computes every score twice and keeps online statistics).
+template <int BF, int NT, bool BAND>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_scores_rs(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  constexpr int S = stride_of<BF>();
+  __shared__ __align__(16) T Ks[2][kTile * S];
+  __shared__ float cm[NT][4][kTile];
+  const BlockCtx c = block_ctx(p);
+  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const int nvis = tile_count(c);  // <= NT (the launch checks the padded length)
+  TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  QFrag<BF> qf;
+  load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
+  const RowQ rq = row_queries<BAND>(c);
+
+  // scores in registers (masked keys -inf), the lane's max dot product per query; the t-th
+  // visited tile goes through K buffer t & 1 (the barrier after its store also orders the
+  // reads of tile t - 2, consumed by that tile's MFMAs, before it)
+  f32x4_t acc[NT][4];
+  float dmax[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t < nvis) {
+      const int kt = tile_at(c, t);
+      T* buf = Ks[t & 1];
+      tile_store<BF>(kr, buf, c.tid);
+      lds_barrier();
+      kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
+      score_tile_qk(acc[t], buf, qf, c.r16, c.g);
+      const int lim = c.len - kt * kTile;
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const float d = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[t][s][i] : -INFINITY;
+          acc[t][s][i] = d;
+          dmax[i] = max_sel(dmax[i], d);
+        }
+    }
+  }
+  // row statistics as in the resident variant
+  float M[4], Ls[4], cq[4], cc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    M[i] = __fmul_rn(row16_max_sel(dmax[i]), kLog2eOver8);  // finite: key 0 is attended
+    Ls[i] = 0.f;
+  }
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t < nvis) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) Ls[i] += exp2_fast(__fmaf_rn(acc[t][s][i], kLog2eOver8, -M[i]));
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    cq[i] = M[i] + __builtin_amdgcn_logf(row16_sum(Ls[i]));
+    cc[i] = colmax_offset<BAND>(c, rq, i, cq[i]);
+  }
+  store_row_c(p, c, cq);
+
+  float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
+  if (BAND) {  // valid keys of the tiles outside the window get a zero partial
+    for (int key = kTile + c.tid; key < c.len; key += kThreads) {
+      const int kt = key / kTile;
+      if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
+    }
+  }
+  const bool sum = p.importance == 1;
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t < nvis) {
+      tile_colmax(acc[t], cc, cm[t][c.wave], c, sum);
+      if (p.acol) store_probs(p, c, acc[t], tile_at(c, t), cq);
+    }
+  }
+  lds_barrier();
+  for (int e = c.tid; e < nvis * kTile; e += kThreads) {
+    const int t = e / kTile, k = e % kTile;
+    const float v = sum ? (cm[t][0][k] + cm[t][1][k]) + (cm[t][2][k] + cm[t][3][k])
+                        : exp2_fast(max_sel(max_sel(cm[t][0][k], cm[t][1][k]), max_sel(cm[t][2][k], cm[t][3][k])));
+    const int key = tile_at(c, t) * kTile + k;
+    if (key < c.n) part[(int64_t)key * p.nparts] = v;
+  }
+}
+
 // Streaming variant: tiles double buffered, next tile prefetched; two sweeps (per-lane
 // online statistics, then the column max).
 template <int BF, bool BAND>
@@ -939,10 +1031,12 @@ hipError_t launch_scores_band(const FwdParams& p, hipStream_t s) {
     if (nt <= 1) return launch_stage_kernel((k_scores_res<1, 1, BAND>), grid, blk, 0, s, p);
     else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2, BAND>), grid, blk, 0, s, p);
     else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 8) return launch_stage_kernel((k_scores_rs<1, 8, BAND>), grid, blk, 0, s, p);
     else return launch_stage_kernel((k_scores_stream<1, BAND>), grid, blk, 0, s, p);
   } else {
     if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1, BAND>), grid, blk, 0, s, p);
     else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2, BAND>), grid, blk, 0, s, p);
+    else if (nt <= 8) return launch_stage_kernel((k_scores_rs<0, 8, BAND>), grid, blk, 0, s, p);
     else return launch_stage_kernel((k_scores_stream<0, BAND>), grid, blk, 0, s, p);
   }
 }
