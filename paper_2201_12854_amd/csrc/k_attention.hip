@@ -174,19 +174,30 @@ __device__ __forceinline__ void score_tile(f32x4_t acc[4], const float* Ks, cons
 constexpr float kLog2eOver8 = (float)(1.4426950408889634 / 8.0);
 __device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }  // exp2(-inf) = 0
 
-// max(a, b) of floats by compare and select (no NaN canonicalisation of the operands).
-__device__ __forceinline__ float max_sel(float a, float b) { return a > b ? a : b; }
+// max of floats on the VALU max instructions, without the operand canonicalisation the
+// compiler adds around fmaxf: v_max_f32 and the three-input v_max3_f32. The operands are
+// scores, statistics and probabilities (finite or -inf), whose maximum is exact.
+__device__ __forceinline__ float vmax(float a, float b) {
+  float r;
+  asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ float vmax3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
 
 // Combination with lane ^ 16 and lane ^ 32 (the four 16-lane rows hold one query's partial
 // results for different keys) by the gfx950 lane swaps: swapping a value with itself gives
 // each lane the pair {own, partner}, in some order, in registers.
 __device__ __forceinline__ float pair16_max(float v) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return max_sel(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float pair32_max(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return max_sel(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
 }
 __device__ __forceinline__ float pair16_sum(float v) {
   const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -429,7 +440,7 @@ __device__ __forceinline__ void score_tile_qk(f32x4_t acc[4], const float* Ks, c
 
 // Reductions over the 16 lanes of a lane row (DPP butterflies; every lane gets the result).
 template <int CTRL>
-__device__ __forceinline__ float row_max_step(float v) { return max_sel(v, dpp_f32<CTRL>(v)); }
+__device__ __forceinline__ float row_max_step(float v) { return vmax(v, dpp_f32<CTRL>(v)); }
 __device__ __forceinline__ float row16_max_sel(float v) {
   return row_max_step<0x140>(row_max_step<0x141>(row_max_step<0x4E>(row_max_step<0xB1>(v))));
 }
@@ -443,7 +454,7 @@ __device__ __forceinline__ float row16_sum(float v) {
 template <int CTRL>
 __device__ __forceinline__ void row_stat_step(float& M, float& L) {
   const float m2 = dpp_f32<CTRL>(M), l2 = dpp_f32<CTRL>(L);
-  const float Mn = max_sel(M, m2);
+  const float Mn = vmax(M, m2);
   const float a = M == -INFINITY ? 0.f : __fmul_rn(L, exp2_fast(__fsub_rn(M, Mn)));
   const float b = m2 == -INFINITY ? 0.f : __fmul_rn(l2, exp2_fast(__fsub_rn(m2, Mn)));
   L = a + b;
@@ -465,10 +476,10 @@ __device__ __forceinline__ void tile_colmax(const f32x4_t acc[4], const float cc
       for (int i = 0; i < 4; ++i) t += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
       v[s] = pair32_sum(pair16_sum(t));
     } else {
-      float t = -INFINITY;
+      float t[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) t = max_sel(t, __fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
-      v[s] = pair32_max(pair16_max(t));
+      for (int i = 0; i < 4; ++i) t[i] = __fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]);
+      v[s] = pair32_max(pair16_max(vmax(vmax3(t[0], t[1], t[2]), t[3])));
     }
   }
   if (c.g == 0) {
@@ -537,11 +548,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {  // a select per key: cheaper here than a branch per tile
-          const float d = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[kt][s][i] : -INFINITY;
-          acc[kt][s][i] = d;
-          dmax[i] = max_sel(dmax[i], d);
-        }
+        for (int i = 0; i < 4; ++i)  // a select per key: cheaper here than a branch per tile
+          acc[kt][s][i] = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[kt][s][i] : -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        dmax[i] = vmax3(vmax3(dmax[i], acc[kt][0][i], acc[kt][1][i]), acc[kt][2][i], acc[kt][3][i]);
     }
   }
   // row statistics: M = the largest logit (rounding is monotone, so it is the rounded
@@ -583,7 +594,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   for (int e = c.tid; e < c.ntl * kTile; e += kThreads) {
     const int kt = e / kTile, k = e % kTile;
     const float v = sum ? (cm[kt][0][k] + cm[kt][1][k]) + (cm[kt][2][k] + cm[kt][3][k])
-                        : exp2_fast(max_sel(max_sel(cm[kt][0][k], cm[kt][1][k]), max_sel(cm[kt][2][k], cm[kt][3][k])));
+                        : exp2_fast(vmax(vmax3(cm[kt][0][k], cm[kt][1][k], cm[kt][2][k]), cm[kt][3][k]));
     if (e < c.n) part[(int64_t)e * p.nparts] = v;
   }
 }
@@ -622,14 +633,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
       score_tile_qk(acc[t], buf, qf, c.r16, c.g);
       const int lim = c.len - kt * kTile;
+      if (BAND || lim < kTile) mask_tile_q<BAND>(acc[t], c, rq, kt, lim, -INFINITY);  // tile-uniform
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const float d = key_ok_q<BAND>(c, rq, kt, lim, s, i) ? acc[t][s][i] : -INFINITY;
-          acc[t][s][i] = d;
-          dmax[i] = max_sel(dmax[i], d);
-        }
+      for (int i = 0; i < 4; ++i)
+        dmax[i] = vmax3(vmax3(dmax[i], acc[t][0][i], acc[t][1][i]), acc[t][2][i], acc[t][3][i]);
     }
   }
   // row statistics as in the resident variant
@@ -674,7 +681,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   for (int e = c.tid; e < nvis * kTile; e += kThreads) {
     const int t = e / kTile, k = e % kTile;
     const float v = sum ? (cm[t][0][k] + cm[t][1][k]) + (cm[t][2][k] + cm[t][3][k])
-                        : exp2_fast(max_sel(max_sel(cm[t][0][k], cm[t][1][k]), max_sel(cm[t][2][k], cm[t][3][k])));
+                        : exp2_fast(vmax(vmax3(cm[t][0][k], cm[t][1][k], cm[t][2][k]), cm[t][3][k]));
     const int key = tile_at(c, t) * kTile + k;
     if (key < c.n) part[(int64_t)key * p.nparts] = v;
   }
@@ -713,13 +720,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     if (BAND || lim < kTile) mask_tile_q<BAND>(acc, c, rq, kt, lim, -INFINITY);  // tile-uniform
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float d[4], dm = -INFINITY;
+      float d[4];
 #pragma unroll
-      for (int s = 0; s < 4; ++s) {
-        d[s] = acc[s][i];
-        dm = max_sel(dm, d[s]);
-      }
-      const float Mn = max_sel(M[i], __fmul_rn(dm, kLog2eOver8));
+      for (int s = 0; s < 4; ++s) d[s] = acc[s][i];
+      const float dm = vmax(vmax3(d[0], d[1], d[2]), d[3]);
+      const float Mn = vmax(M[i], __fmul_rn(dm, kLog2eOver8));
       float sum = 0.f;
 #pragma unroll
       for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(d[s], kLog2eOver8, -Mn));
@@ -770,7 +775,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     lds_barrier();
     if (c.tid < kTile) {
       const float v = sum ? (cmk[0][c.tid] + cmk[1][c.tid]) + (cmk[2][c.tid] + cmk[3][c.tid])
-                          : exp2_fast(max_sel(max_sel(cmk[0][c.tid], cmk[1][c.tid]), max_sel(cmk[2][c.tid], cmk[3][c.tid])));
+                          : exp2_fast(vmax(vmax3(cmk[0][c.tid], cmk[1][c.tid], cmk[2][c.tid]), cmk[3][c.tid]));
       const int key = kt * kTile + c.tid;
       if (key < c.n) part[(int64_t)key * p.nparts] = v;
     }
