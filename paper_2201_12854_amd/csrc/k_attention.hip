@@ -449,8 +449,9 @@ __device__ __forceinline__ float row_sum_step(float v) { return v + dpp_f32<CTRL
 __device__ __forceinline__ float row16_sum(float v) {
   return row_sum_step<0x140>(row_sum_step<0x141>(row_sum_step<0x4E>(row_sum_step<0xB1>(v))));
 }
-// (max, sum of exp2(logit - max)) pairs of the 16 lanes of a row combined, rescaled to the
-// common max; a lane with no attended key so far holds (-inf, 0).
+// (reference, sum of exp2(logit - reference)) pairs of the 16 lanes of a row combined,
+// rescaled to the larger reference; a lane with no attended key holds (-inf or a reference
+// below every logit, 0).
 template <int CTRL>
 __device__ __forceinline__ void row_stat_step(float& M, float& L) {
   const float m2 = dpp_f32<CTRL>(M), l2 = dpp_f32<CTRL>(L);
@@ -702,9 +703,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
   const RowQ rq = row_queries<BAND>(c);
 
-  // Sweep 1: per lane and query, the running max logit M and the sum of exp2(logit - M)
-  // over the lane's keys; the 16 lanes of a row are combined at the end.
-  float M[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY}, Ls[4] = {0.f, 0.f, 0.f, 0.f};
+  // Sweep 1: per lane and query, a reference logit M and the sum of exp2(logit - M) over
+  // the lane's keys; the 16 lanes of a row are combined at the end. M is raised to the
+  // running max only when a tile holds a logit more than kRescale above it (after the
+  // first tiles, rarely): otherwise the terms, all below 2^kRescale, are added without
+  // rescaling. The branch is wave-uniform.
+  constexpr float kNoMax = -1e30f;  // below every logit: no attended key seen yet
+  constexpr float kRescale = 16.f;
+  constexpr float kInvScale = (float)(8.0 / 1.4426950408889634);  // 1 / (log2(e) / 8)
+  float M[4], Ls[4], thr[4];  // thr: the largest dot product M admits, (M + kRescale) / (log2(e) / 8)
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    M[i] = kNoMax;
+    Ls[i] = 0.f;
+    thr[i] = kNoMax;
+  }
   const int nvis = tile_count(c);
   TileRegs kr;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
@@ -718,19 +731,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
     score_tile_qk(acc, buf, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
     if (BAND || lim < kTile) mask_tile_q<BAND>(acc, c, rq, kt, lim, -INFINITY);  // tile-uniform
+    float dm[4];
+    bool raise = false;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      float d[4];
+      dm[i] = vmax(vmax3(acc[0][i], acc[1][i], acc[2][i]), acc[3][i]);
+      raise |= dm[i] > thr[i];
+    }
+    if (__any(raise)) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) d[s] = acc[s][i];
-      const float dm = vmax(vmax3(d[0], d[1], d[2]), d[3]);
-      const float Mn = vmax(M[i], __fmul_rn(dm, kLog2eOver8));
-      float sum = 0.f;
+      for (int i = 0; i < 4; ++i) {
+        const float Mn = vmax(M[i], __fmul_rn(dm[i], kLog2eOver8));
+        float sum = 0.f;
 #pragma unroll
-      for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(d[s], kLog2eOver8, -Mn));
-      const float old = M[i] == -INFINITY ? 0.f : __fmul_rn(Ls[i], exp2_fast(__fsub_rn(M[i], Mn)));
-      Ls[i] = Mn == -INFINITY ? 0.f : old + sum;
-      M[i] = Mn;
+        for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -Mn));
+        Ls[i] = __fmul_rn(Ls[i], exp2_fast(__fsub_rn(M[i], Mn))) + sum;
+        M[i] = Mn;
+        thr[i] = __fmul_rn(Mn + kRescale, kInvScale);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        float sum = 0.f;
+#pragma unroll
+        for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -M[i]));
+        Ls[i] += sum;
+      }
     }
   }
   float cq[4], cc[4];
