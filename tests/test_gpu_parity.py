@@ -331,6 +331,26 @@ def test_window_streaming_ragged(dev, dtype, window, lens):
     assert n_tok > 0
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("n,lens,window", [(300, (300, 181), 0), (600, (600, 531), 0), (600, (600, 77), 128)])
+def test_score_pass_variants_ragged(dev, dtype, n, lens, window):
+    # n = 300: the one-sweep score pass that keeps every score in registers (up to 8 key
+    # tiles); n = 600: the two-sweep streaming score pass (its online row sum and its
+    # column max), with full attention and with a window; ragged rows
+    L = wl.make_layer(2, n, 128, 4, dtype, data_seed=9, lens=np.array(lens), q_scale=2.5,
+                      token_scale_sigma=0.5, window=window)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=5)
+    assert n_tok > 0
+
+
+@pytest.mark.parametrize("rule", ["mean", "median"])
+def test_importance_rules_long_rows(dev, rule):
+    # mean and median rules through the two-sweep streaming score pass (n = 600)
+    L = wl.make_layer(2, 600, 128, 4, "bf16", data_seed=10, lens=np.array([600, 413]), q_scale=2.0,
+                      token_scale_sigma=0.5)
+    _full_check(L, dev, 0.1, seed=2, importance=rule)
+
+
 @pytest.mark.parametrize("name", ["longformer_aapd_bf16", "longformer_imdb_bf16", "longformer_hnd_bf16"])
 def test_longformer_workloads(dev, name):
     # the document-classification stand-ins at full width, on two batch rows each
