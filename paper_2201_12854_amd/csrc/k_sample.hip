@@ -566,9 +566,13 @@ hipError_t launch_nw(const FwdParams& p, hipStream_t s) {
 template <int BF, int PER, bool TABLE>
 hipError_t launch_per(const FwdParams& p, hipStream_t s) {
   constexpr int kLds = 160 * 1024;
-  if (sample_lds_bytes(p.d_in, TABLE, 16) <= kLds) return launch_nw<BF, PER, TABLE, 16>(p, s);
-  if (sample_lds_bytes(p.d_in, TABLE, 8) <= kLds) return launch_nw<BF, PER, TABLE, 8>(p, s);
+  // four tokens per block: several blocks per CU, so that one block's first loads overlap
+  // another's draws (measured faster than 16 or 8 tokens per block, which balance the
+  // pooled draws over more tokens, at the BERT-base, BERT-large, long-sequence and
+  // local-window shapes)
   if (sample_lds_bytes(p.d_in, TABLE, 4) <= kLds) return launch_nw<BF, PER, TABLE, 4>(p, s);
+  if (sample_lds_bytes(p.d_in, TABLE, 2) <= kLds) return launch_nw<BF, PER, TABLE, 2>(p, s);
+  if (sample_lds_bytes(p.d_in, TABLE, 1) <= kLds) return launch_nw<BF, PER, TABLE, 1>(p, s);
   return hipErrorInvalidValue;
 }
 
