@@ -181,7 +181,7 @@ def dense_baseline(t, L, steps, warmup):
 
             ms2, _ = time_loop(sdpa_path, steps, warmup)
             out["sdpa_ms"] = ms2
-        except Exception as e:  # backend unavailable on this build: keep the bmm path
+        except Exception as e:  # backend unavailable in the installed PyTorch: keep the bmm path
             out["sdpa_error"] = str(e)[:200]
     out["ms"] = min(v for k, v in out.items() if k.endswith("_ms"))
     out["tokens_per_s"] = float(L.tokens) / (out["ms"] * 1e-3)
