@@ -36,7 +36,7 @@ namespace {
 template <int BF> struct Elem { using T = float; };
 template <> struct Elem<1> { using T = uint16_t; };
 
-constexpr int kMaxWaves = 16;  // tokens (waves) per block: 16, 8 or 4, as the LDS allows
+constexpr int kMaxWaves = 4;  // tokens (waves) per block: 4, 2 or 1, as the LDS allows
 
 
 // Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
@@ -284,6 +284,7 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
 // leaves before them.
 template <int BF, int PER, bool TABLE, int NW>
 __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
+  static_assert(NW >= 1 && NW <= kMaxWaves, "tokens per block");
   using T = typename Elem<BF>::T;
   extern __shared__ __align__(16) unsigned char smem[];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
