@@ -10,7 +10,7 @@
 // (except under the median rule).
 //
 // Tiling: one block = 4 waves = 64 queries of one (batch row, head); a wave owns 16
-// queries (the streaming output pass: 128 queries, 32 per wave). Keys come in tiles of 64 staged in LDS; 16x16 MFMA tiles (bf16 16x16x32 or
+// queries (the streaming kernels: 128 queries, 32 per wave). Keys come in tiles of 64 staged in LDS; 16x16 MFMA tiles (bf16 16x16x32 or
 // fp32 16x16x4). The score pass computes S = Q K^T (its layout and reductions are
 // described with the kernels). The output pass computes S^T = K Q^T, so lane l holds the
 // scores of query (l % 16) for keys 16 s + 4 (l / 16) + i (s, i = 0..3): exactly the
@@ -492,9 +492,8 @@ __device__ __forceinline__ void tile_colmax(const f32x4_t acc[4], const float cc
 // Median rule: the probabilities of one tile, A = exp2(dot a log2(e) - c), into the per-key
 // array acol[b n + key][h][query].
 __device__ __forceinline__ void store_probs(const FwdParams& p, const BlockCtx& c, const f32x4_t acc[4], int kt,
-                                            const float cq[4]) {
+                                            const float cq[4], int qw) {
   float* ac = p.acol + (int64_t)c.b * c.n * p.H * c.n;
-  const int qw = c.qt * kTile + c.wave * 16 + 4 * c.g;
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
     const int key = kt * kTile + 16 * s + c.r16;
@@ -587,7 +586,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
       tile_colmax(acc[kt], cc, cm[kt][c.wave], c, sum);
-      if (p.acol) store_probs(p, c, acc[kt], kt, cq);
+      if (p.acol) store_probs(p, c, acc[kt], kt, cq, c.qt * kTile + c.wave * 16 + 4 * c.g);
     }
   }
   lds_barrier();
@@ -675,7 +674,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   for (int t = 0; t < NT; ++t) {
     if (t < nvis) {
       tile_colmax(acc[t], cc, cm[t][c.wave], c, sum);
-      if (p.acol) store_probs(p, c, acc[t], tile_at(c, t), cq);
+      if (p.acol) store_probs(p, c, acc[t], tile_at(c, t), cq, c.qt * kTile + c.wave * 16 + 4 * c.g);
     }
   }
   lds_barrier();
@@ -685,126 +684,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                         : exp2_fast(vmax(vmax3(cm[t][0][k], cm[t][1][k], cm[t][2][k]), cm[t][3][k]));
     const int key = tile_at(c, t) * kTile + k;
     if (key < c.n) part[(int64_t)key * p.nparts] = v;
-  }
-}
-
-// Streaming variant: tiles double buffered, next tile prefetched; two sweeps (per-lane
-// online statistics, then the column max).
-template <int BF, bool BAND>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_stream(FwdParams p) {
-  using T = typename Elem<BF>::T;
-  constexpr int S = stride_of<BF>();
-  __shared__ __align__(16) T Ks[2][kTile * S];
-  __shared__ float cm[2][4][kTile];
-  const BlockCtx c = block_ctx(p);
-  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
-  const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
-  QFrag<BF> qf;
-  load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
-  const RowQ rq = row_queries<BAND>(c);
-
-  // Sweep 1: per lane and query, a reference logit M and the sum of exp2(logit - M) over
-  // the lane's keys; the 16 lanes of a row are combined at the end. M is raised to the
-  // running max only when a tile holds a logit more than kRescale above it (after the
-  // first tiles, rarely): otherwise the terms, all below 2^kRescale, are added without
-  // rescaling. The branch is wave-uniform.
-  constexpr float kNoMax = -1e30f;  // below every logit: no attended key seen yet
-  constexpr float kRescale = 16.f;
-  constexpr float kInvScale = (float)(8.0 / 1.4426950408889634);  // 1 / (log2(e) / 8)
-  float M[4], Ls[4], thr[4];  // thr: the largest dot product M admits, (M + kRescale) / (log2(e) / 8)
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    M[i] = kNoMax;
-    Ls[i] = 0.f;
-    thr[i] = kNoMax;
-  }
-  const int nvis = tile_count(c);
-  TileRegs kr;
-  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  for (int t = 0; t < nvis; ++t) {
-    const int kt = tile_at(c, t);
-    T* buf = Ks[t & 1];
-    tile_store<BF>(kr, buf, c.tid);
-    lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
-    f32x4_t acc[4];
-    score_tile_qk(acc, buf, qf, c.r16, c.g);
-    const int lim = c.len - kt * kTile;
-    if (BAND || lim < kTile) mask_tile_q<BAND>(acc, c, rq, kt, lim, -INFINITY);  // tile-uniform
-    float dm[4];
-    bool raise = false;
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      dm[i] = vmax(vmax3(acc[0][i], acc[1][i], acc[2][i]), acc[3][i]);
-      raise |= dm[i] > thr[i];
-    }
-    if (__any(raise)) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float Mn = vmax(M[i], __fmul_rn(dm[i], kLog2eOver8));
-        float sum = 0.f;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -Mn));
-        Ls[i] = __fmul_rn(Ls[i], exp2_fast(__fsub_rn(M[i], Mn))) + sum;
-        M[i] = Mn;
-        thr[i] = __fmul_rn(Mn + kRescale, kInvScale);
-      }
-    } else {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        float sum = 0.f;
-#pragma unroll
-        for (int s = 0; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -M[i]));
-        Ls[i] += sum;
-      }
-    }
-  }
-  float cq[4], cc[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float Mi = M[i], Li = Ls[i];
-    row_stat_step<0xB1>(Mi, Li);
-    row_stat_step<0x4E>(Mi, Li);
-    row_stat_step<0x141>(Mi, Li);
-    row_stat_step<0x140>(Mi, Li);
-    cq[i] = Mi + __builtin_amdgcn_logf(Li);  // finite: key 0 is attended by every query
-    cc[i] = colmax_offset<BAND>(c, rq, i, cq[i]);
-  }
-  store_row_c(p, c, cq);
-
-  // Sweep 2: the per-key column max of this block's valid queries. The t-th visited tile
-  // uses K buffer t & 1 and column-max slot t & 1; the barrier after its LDS store also
-  // orders the reads of tile t - 2's slot before this tile's writes.
-  lds_barrier();  // sweep 1 is done with both K buffers
-  float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
-  if (BAND) {  // valid keys of the tiles outside the window get a zero partial
-    for (int key = kTile + c.tid; key < c.len; key += kThreads) {
-      const int kt = key / kTile;
-      if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
-    }
-  }
-  const bool sum = p.importance == 1;
-  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  for (int t = 0; t < nvis; ++t) {
-    const int kt = tile_at(c, t);
-    T* buf = Ks[t & 1];
-    float (*cmk)[kTile] = cm[t & 1];
-    tile_store<BF>(kr, buf, c.tid);
-    lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
-    f32x4_t acc[4];
-    score_tile_qk(acc, buf, qf, c.r16, c.g);
-    const int lim = c.len - kt * kTile;
-    if (BAND || lim < kTile) mask_tile_q<BAND>(acc, c, rq, kt, lim, -INFINITY);  // tile-uniform
-    tile_colmax(acc, cc, cmk[c.wave], c, sum);
-    if (p.acol) store_probs(p, c, acc, kt, cq);
-    lds_barrier();
-    if (c.tid < kTile) {
-      const float v = sum ? (cmk[0][c.tid] + cmk[1][c.tid]) + (cmk[2][c.tid] + cmk[3][c.tid])
-                          : exp2_fast(vmax(vmax3(cmk[0][c.tid], cmk[1][c.tid], cmk[2][c.tid]), cmk[3][c.tid]));
-      const int key = kt * kTile + c.tid;
-      if (key < c.n) part[(int64_t)key * p.nparts] = v;
-    }
   }
 }
 
@@ -1053,6 +932,225 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
     }
 }
 
+// ------------------------------------------------------------------ score pass, streaming
+// Streaming score pass (rows longer than 8 key tiles): 128 queries per block, two 16-query
+// tiles per wave, so that every K fragment read from LDS feeds two MFMAs and the per-tile
+// work (tile loads and stores, barriers, lane swaps, partial stores) serves twice the
+// queries. Two sweeps over the visited tiles: per-lane statistics, then the column
+// statistic, one partial per (key, head, 128-query tile).
+
+// S = Q K^T of two 16-query tiles: acc[m][s][i] = dot(query 16 m + 4 g + i, key 16 s + r16).
+__device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const uint16_t* Ks, const QFrag<1> q[2], int r16,
+                                               int g) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    acc[0][s] = acc[1][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int ks = 0; ks < 2; ++ks) {
+      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 * ks + 8 * g);
+      acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[0].v[ks], b, acc[0][s], 0, 0, 0);
+      acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[1].v[ks], b, acc[1][s], 0, 0, 0);
+    }
+  }
+}
+
+__device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const float* Ks, const QFrag<0> q[2], int r16,
+                                               int g) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    acc[0][s] = acc[1][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    const float* krow = Ks + (16 * s + r16) * kStrideF + 16 * g;
+#pragma unroll
+    for (int t = 0; t < 16; ++t) {
+      const float b = krow[t];
+      acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[0].v[t], b, acc[0][s], 0, 0, 0);
+      acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(q[1].v[t], b, acc[1][s], 0, 0, 0);
+    }
+  }
+}
+
+template <int BF, bool BAND>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_scores_stream(FwdParams p) {
+  using T = typename Elem<BF>::T;
+  constexpr int S = stride_of<BF>();
+  __shared__ __align__(16) T Ks[2][kTile * S];
+  __shared__ float cm[2][4][kTile];
+  const BlockCtx c = block_ctx2(p);
+  const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
+  const int qw = c.qt * kTile2 + c.wave * 32;  // the wave's first query
+  QFrag<BF> qf[2];
+#pragma unroll
+  for (int m = 0; m < 2; ++m) load_qfrag(qf[m], Qb + (int64_t)min(qw + 16 * m + c.r16, c.n - 1) * c.d_out, c.g);
+  // the lane's eight queries qw + 16 m + 4 g + i in slot 4 m + i; under a local window each
+  // attends keys klo .. klo + kspan and key 0
+  int klo[8], kspan[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    klo[k] = 0;
+    kspan[k] = 0;
+    if constexpr (BAND) query_window(c, qw + 16 * (k >> 2) + 4 * c.g + (k & 3), klo[k], kspan[k]);
+  }
+  // masked keys of a tile the lane's queries do not all attend (called for such tiles only)
+  auto mask = [&](f32x4_t acc[2][4], int kt, int lim) {
+#pragma unroll
+    for (int m = 0; m < 2; ++m)
+#pragma unroll
+      for (int s = 0; s < 4; ++s)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          bool ok;
+          if constexpr (BAND) {
+            const int key = kt * kTile + 16 * s + c.r16;
+            ok = (unsigned)(key - klo[4 * m + i]) <= (unsigned)kspan[4 * m + i] || key == 0;
+          } else {
+            ok = 16 * s + c.r16 < lim;
+          }
+          if (!ok) acc[m][s][i] = -INFINITY;
+        }
+  };
+
+  // Sweep 1: per lane and query, a reference logit M and the sum of exp2(logit - M) over
+  // the lane's keys; the 16 lanes of a row are combined at the end. M is raised to the
+  // running max only when a tile holds a logit more than kRescale above it (after the
+  // first tiles, rarely): otherwise the terms, all below 2^kRescale, are added without
+  // rescaling. The branch is wave-uniform.
+  constexpr float kNoMax = -1e30f;  // below every logit: no attended key seen yet
+  constexpr float kRescale = 16.f;
+  constexpr float kInvScale = (float)(8.0 / 1.4426950408889634);  // 1 / (log2(e) / 8)
+  float M[8], Ls[8], thr[8];  // thr: the largest dot product M admits, (M + kRescale) / (log2(e) / 8)
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    M[k] = kNoMax;
+    Ls[k] = 0.f;
+    thr[k] = kNoMax;
+  }
+  const int nvis = tile_count(c);
+  TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  for (int t = 0; t < nvis; ++t) {
+    const int kt = tile_at(c, t);
+    T* buf = Ks[t & 1];
+    tile_store<BF>(kr, buf, c.tid);
+    lds_barrier();
+    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
+    f32x4_t acc[2][4];
+    score_tile_qk2(acc, buf, qf, c.r16, c.g);
+    const int lim = c.len - kt * kTile;
+    if (BAND || lim < kTile) mask(acc, kt, lim);  // tile-uniform
+    float dm[8];
+    bool raise = false;
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int m = k >> 2, i = k & 3;
+      dm[k] = vmax(vmax3(acc[m][0][i], acc[m][1][i], acc[m][2][i]), acc[m][3][i]);
+      raise |= dm[k] > thr[k];
+    }
+    if (__any(raise)) {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int m = k >> 2, i = k & 3;
+        const float Mn = vmax(M[k], __fmul_rn(dm[k], kLog2eOver8));
+        float sum = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -Mn));
+#pragma unroll
+        for (int s = 1; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -Mn));
+        Ls[k] = __fmul_rn(Ls[k], exp2_fast(__fsub_rn(M[k], Mn))) + sum;
+        M[k] = Mn;
+        thr[k] = __fmul_rn(Mn + kRescale, kInvScale);
+      }
+    } else {
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        const int m = k >> 2, i = k & 3;
+        float sum = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -M[k]));
+#pragma unroll
+        for (int s = 1; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
+        Ls[k] += sum;
+      }
+    }
+  }
+  float cq[8], cc[8];
+#pragma unroll
+  for (int k = 0; k < 8; ++k) {
+    float Mi = M[k], Li = Ls[k];
+    row_stat_step<0xB1>(Mi, Li);
+    row_stat_step<0x4E>(Mi, Li);
+    row_stat_step<0x141>(Mi, Li);
+    row_stat_step<0x140>(Mi, Li);
+    cq[k] = Mi + __builtin_amdgcn_logf(Li);  // finite: key 0 is attended by every query
+    // the column statistic's offset: c, or c - log2 |S_q| under a window; +inf for
+    // padded queries (excluded)
+    const int q = qw + 16 * (k >> 2) + 4 * c.g + (k & 3);
+    float off = cq[k];
+    if constexpr (BAND) off = cq[k] - __builtin_amdgcn_logf((float)(kspan[k] + 1 + (klo[k] > 0 ? 1 : 0)));
+    cc[k] = q >= c.len ? INFINITY : off;
+  }
+  {  // c of query qw + 16 m + 4 g + i from lane r16 = 4 m + i of each lane row
+    float v = cq[0];
+#pragma unroll
+    for (int k = 1; k < 8; ++k) v = c.r16 == k ? cq[k] : v;
+    const int q = qw + 16 * (c.r16 >> 2) + 4 * c.g + (c.r16 & 3);
+    if (c.r16 < 8 && q < c.n) p.row_c[((int64_t)c.b * p.H + c.h) * c.n + q] = v;
+  }
+
+  // Sweep 2: the per-key column statistic of this block's valid queries. The t-th visited
+  // tile uses K buffer t & 1 and column slot t & 1; the barrier after its LDS store also
+  // orders the reads of tile t - 2's slot before this tile's writes.
+  lds_barrier();  // sweep 1 is done with both K buffers
+  float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
+  if (BAND) {  // valid keys of the tiles outside the window get a zero partial
+    for (int key = kTile + c.tid; key < c.len; key += kThreads) {
+      const int kt = key / kTile;
+      if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
+    }
+  }
+  const bool sum = p.importance == 1;
+  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  for (int t = 0; t < nvis; ++t) {
+    const int kt = tile_at(c, t);
+    T* buf = Ks[t & 1];
+    float (*cmk)[kTile] = cm[t & 1];
+    tile_store<BF>(kr, buf, c.tid);
+    lds_barrier();
+    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
+    f32x4_t acc[2][4];
+    score_tile_qk2(acc, buf, qf, c.r16, c.g);
+    const int lim = c.len - kt * kTile;
+    if (BAND || lim < kTile) mask(acc, kt, lim);  // tile-uniform
+    // t = dot a log2(e) - cc over the lane's eight queries: max (or sum of exp2) per key,
+    // then over the four lane rows; lane row 0 leaves the wave's value in LDS
+    float v[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      float x[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) x[k] = __fmaf_rn(acc[k >> 2][s][k & 3], kLog2eOver8, -cc[k]);
+      if (sum) {
+        float e = exp2_fast(x[0]);
+#pragma unroll
+        for (int k = 1; k < 8; ++k) e += exp2_fast(x[k]);
+        v[s] = pair32_sum(pair16_sum(e));
+      } else {
+        v[s] = pair32_max(pair16_max(vmax3(vmax3(x[0], x[1], x[2]), vmax3(x[3], x[4], x[5]), vmax(x[6], x[7]))));
+      }
+    }
+    if (c.g == 0) {
+#pragma unroll
+      for (int s = 0; s < 4; ++s) cmk[c.wave][16 * s + c.r16] = v[s];
+    }
+    if (p.acol) {
+#pragma unroll
+      for (int m = 0; m < 2; ++m) store_probs(p, c, acc[m], kt, cq + 4 * m, qw + 16 * m + 4 * c.g);
+    }
+    lds_barrier();
+    if (c.tid < kTile) {
+      const float w = sum ? (cmk[0][c.tid] + cmk[1][c.tid]) + (cmk[2][c.tid] + cmk[3][c.tid])
+                          : exp2_fast(vmax(vmax3(cmk[0][c.tid], cmk[1][c.tid], cmk[2][c.tid]), cmk[3][c.tid]));
+      const int key = kt * kTile + c.tid;
+      if (key < c.n) part[(int64_t)key * p.nparts] = w;
+    }
+  }
+}
+
 // Resident variants for padded lengths up to 256 keys (bf16) or 128 keys (fp32).
 template <bool BAND>
 hipError_t launch_scores_band(const FwdParams& p, hipStream_t s) {
@@ -1063,12 +1161,12 @@ hipError_t launch_scores_band(const FwdParams& p, hipStream_t s) {
     else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2, BAND>), grid, blk, 0, s, p);
     else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4, BAND>), grid, blk, 0, s, p);
     else if (nt <= 8) return launch_stage_kernel((k_scores_rs<1, 8, BAND>), grid, blk, 0, s, p);
-    else return launch_stage_kernel((k_scores_stream<1, BAND>), grid, blk, 0, s, p);
+    else return launch_stage_kernel((k_scores_stream<1, BAND>), dim3((unsigned)(p.qtiles * p.H * p.B)), blk, 0, s, p);
   } else {
     if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1, BAND>), grid, blk, 0, s, p);
     else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2, BAND>), grid, blk, 0, s, p);
     else if (nt <= 8) return launch_stage_kernel((k_scores_rs<0, 8, BAND>), grid, blk, 0, s, p);
-    else return launch_stage_kernel((k_scores_stream<0, BAND>), grid, blk, 0, s, p);
+    else return launch_stage_kernel((k_scores_stream<0, BAND>), dim3((unsigned)(p.qtiles * p.H * p.B)), blk, 0, s, p);
   }
 }
 

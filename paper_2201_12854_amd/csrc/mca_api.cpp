@@ -47,7 +47,8 @@ Layout layout_for(const mca_forward_desc& d) {
   const size_t d_out = size_t(d.heads) * 64;
   const size_t helem = d.dtype == MCA_BF16 ? 2 : 4;
   Layout L;
-  L.qtiles = (int)((d.seq + mca::kQueryTile - 1) / mca::kQueryTile);
+  const int qt = mca::score_query_tile((int)d.seq);
+  L.qtiles = (int)((d.seq + qt - 1) / qt);
   L.nparts = (int)(d.heads * L.qtiles);
   size_t off = 0;
   L.colmax_part = off; off = align256(off + 4 * tokens * size_t(L.nparts));

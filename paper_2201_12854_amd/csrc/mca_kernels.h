@@ -8,7 +8,11 @@
 
 namespace mca {
 
-constexpr int kQueryTile = 64;  // queries per attention block
+constexpr int kQueryTile = 64;  // queries per attention block (the streaming kernels: 128)
+
+// Queries per column-max partial: the query tile of the score pass, 128 for rows longer
+// than 8 key tiles (its streaming kernel), else 64.
+__host__ __device__ inline int score_query_tile(int n) { return (n + 63) / 64 > 8 ? 128 : 64; }
 
 
 // Prepared weights: rownorm float32 [d_in] at offset 0, then, at prepared_wt_offset(d_in),
@@ -41,7 +45,7 @@ struct FwdParams {
                         // first token attends and is attended by all (0: full attention)
   int importance;       // per-key statistic of the count rule: 0 max, 1 mean, 2 median
   int exact_from;       // > 0: tokens with r >= exact_from are encoded exactly too
-  int qtiles;   // query tiles per sequence = ceil(n / kQueryTile)
+  int qtiles;   // query tiles per sequence = ceil(n / score_query_tile(n))
   int nparts;   // column-max partials per token = H * qtiles
   int din_pad;  // row length of W_v^T
   double alpha;

@@ -84,6 +84,23 @@ def test_workspace_size_formula():
         mca.workspace_size(d)
 
 
+
+def test_workspace_partials_per_query_tile():
+    # one column-max partial per (head, query tile): tiles of 64 queries up to 8 key tiles
+    # (n <= 512), of 128 queries beyond (the streaming score pass)
+    def a(v):
+        return (v + 255) // 256 * 256
+
+    def parts_bytes(n):
+        base = mca.workspace_size(_desc(batch=1, seq=n, heads=4, d_in=256))
+        return base
+    for n, qt in ((512, 64), (513, 128), (600, 128), (4096, 128)):
+        H, tokens, d = 4, n, 256
+        parts = H * ((n + qt - 1) // qt)
+        expect = (a(4 * tokens * parts) + a(4 * tokens * H) + a(2 * tokens * H * 64)
+                  + a(8 * (tokens * ((d + 2) // 2 * 2) + 2 * ((d + 2) // 2 * 2) + 64)) + a(4 * tokens))
+        assert parts_bytes(n) == expect, n
+
 def test_prepared_size_formula():
     for dt, esz in ((0, 4), (1, 2)):
         for d_in, d_out in ((768, 768), (45, 256), (1, 64)):
