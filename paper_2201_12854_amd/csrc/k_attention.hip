@@ -740,14 +740,16 @@ __global__ __launch_bounds__(kThreads) void k_attn_res(FwdParams p) {
 }
 
 // ------------------------------------------------------------------ Y = A H~, streaming
-// The streaming output pass takes 128 queries per block, two 16-query tiles per wave: each
-// K and H~ fragment read from LDS feeds two MFMAs (with one query tile per wave the pass
-// is bound by LDS reads; two cut its time by about a sixth at 4096 keys).
-constexpr int kTile2 = 128;
+// The streaming output pass takes MT 16-query tiles per wave (64 MT queries per block):
+// each K and H~ fragment read from LDS feeds MT MFMAs. With one query tile per wave the
+// pass is bound by LDS reads; two cut its time by about a sixth at 4096 keys; three or
+// four measured slower (fewer waves fit beside their accumulators), so MT = 2.
 
-__device__ __forceinline__ BlockCtx block_ctx2(const FwdParams& p) {
+// Block context for blocks of QB queries (QB / 4 per wave); as block_ctx otherwise.
+template <int QB>
+__device__ __forceinline__ BlockCtx block_ctx_q(const FwdParams& p) {
   BlockCtx c;
-  const int bid = blockIdx.x, Q = (p.n + kTile2 - 1) / kTile2, P = p.H * p.B;
+  const int bid = blockIdx.x, Q = (p.n + QB - 1) / QB, P = p.H * p.B;
   int pair;
   if (P % 8 == 0) {  // the query tiles of a (batch row, head) on one XCD, as in block_ctx
     const int G = 8 * Q, w = bid % G;
@@ -767,17 +769,17 @@ __device__ __forceinline__ BlockCtx block_ctx2(const FwdParams& p) {
   c.n = p.n;
   c.d_out = p.d_out;
   c.len = valid_len(p, c.b);
-  c.q = c.qt * kTile2 + c.wave * 32 + c.r16;  // query tile 0 of the wave; tile 1 is q + 16
+  c.q = c.qt * QB + c.wave * (QB / 4) + c.r16;  // query tile 0 of the wave; tile m is q + 16 m
   c.ntl = (c.len + kTile - 1) / kTile;
   c.half = p.band_half;
   c.tlo = 1;
   c.thi = c.ntl - 1;
   c.klo = 0;
   c.kspan = 0;
-  if (c.half > 0 && c.qt > 0) {  // the window of queries q0 .. q0 + 127
-    const int q0 = c.qt * kTile2;
+  if (c.half > 0 && c.qt > 0) {  // the window of queries q0 .. q0 + QB - 1
+    const int q0 = c.qt * QB;
     c.tlo = max(1, max(q0 - c.half, 0) / kTile);
-    c.thi = min(c.ntl - 1, (q0 + kTile2 - 1 + c.half) / kTile);
+    c.thi = min(c.ntl - 1, (q0 + QB - 1 + c.half) / kTile);
   }
   return c;
 }
@@ -791,41 +793,49 @@ __device__ __forceinline__ void query_window(const BlockCtx& c, int q, int& klo,
   kspan = hi - lo;
 }
 
-// S^T = K Q^T for two 16-query tiles sharing each K fragment read.
-__device__ __forceinline__ void score_tile2(f32x4_t acc[2][4], const uint16_t* Ks, const QFrag<1> q[2], int r16,
-                                            int g) {
+// S^T = K Q^T for MT 16-query tiles sharing each K fragment read.
+template <int MT>
+__device__ __forceinline__ void score_tile_m(f32x4_t acc[MT][4], const uint16_t* Ks, const QFrag<1> q[MT], int r16,
+                                             int g) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    acc[0][s] = acc[1][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
       const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 * ks + 8 * g);
-      acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, q[0].v[ks], acc[0][s], 0, 0, 0);
-      acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, q[1].v[ks], acc[1][s], 0, 0, 0);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, q[m].v[ks], acc[m][s], 0, 0, 0);
     }
   }
 }
 
-__device__ __forceinline__ void score_tile2(f32x4_t acc[2][4], const float* Ks, const QFrag<0> q[2], int r16, int g) {
+template <int MT>
+__device__ __forceinline__ void score_tile_m(f32x4_t acc[MT][4], const float* Ks, const QFrag<0> q[MT], int r16,
+                                             int g) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    acc[0][s] = acc[1][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int m = 0; m < MT; ++m) acc[m][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     const float* krow = Ks + (16 * s + r16) * kStrideF + 16 * g;
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
-      acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(krow[t], q[0].v[t], acc[0][s], 0, 0, 0);
-      acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(krow[t], q[1].v[t], acc[1][s], 0, 0, 0);
+      const float a = krow[t];
+#pragma unroll
+      for (int m = 0; m < MT; ++m) acc[m][s] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, q[m].v[t], acc[m][s], 0, 0, 0);
     }
   }
 }
 
-// P V for two query tiles sharing each H~ fragment read.
-__device__ __forceinline__ void pv_tile2(f32x4_t y[2][4], const f32x4_t acc[2][4], const uint16_t* Vs, int r16, int g) {
+// P V for MT query tiles sharing each H~ fragment read.
+template <int MT>
+__device__ __forceinline__ void pv_tile_m(f32x4_t y[MT][4], const f32x4_t acc[MT][4], const uint16_t* Vs, int r16,
+                                          int g) {
 #pragma unroll
   for (int pp = 0; pp < 2; ++pp) {
-    bf16x8_t a[2];
+    bf16x8_t a[MT];
 #pragma unroll
-    for (int m = 0; m < 2; ++m)
+    for (int m = 0; m < MT; ++m)
       a[m] = __builtin_bit_cast(bf16x8_t, make_uint4(pack_bf16x2(acc[m][2 * pp][0], acc[m][2 * pp][1]),
                                                      pack_bf16x2(acc[m][2 * pp][2], acc[m][2 * pp][3]),
                                                      pack_bf16x2(acc[m][2 * pp + 1][0], acc[m][2 * pp + 1][1]),
@@ -836,13 +846,15 @@ __device__ __forceinline__ void pv_tile2(f32x4_t y[2][4], const f32x4_t acc[2][4
       const uint2 lo = lds_read_tr16(vrow);
       const uint2 hi = lds_read_tr16(vrow + 16 * kStrideBf);
       const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
-      y[0][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[0], bv, y[0][c], 0, 0, 0);
-      y[1][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[1], bv, y[1][c], 0, 0, 0);
+#pragma unroll
+      for (int m = 0; m < MT; ++m) y[m][c] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[m], bv, y[m][c], 0, 0, 0);
     }
   }
 }
 
-__device__ __forceinline__ void pv_tile2(f32x4_t y[2][4], const f32x4_t acc[2][4], const float* Vs, int r16, int g) {
+template <int MT>
+__device__ __forceinline__ void pv_tile_m(f32x4_t y[MT][4], const f32x4_t acc[MT][4], const float* Vs, int r16,
+                                          int g) {
 #pragma unroll
   for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -851,19 +863,20 @@ __device__ __forceinline__ void pv_tile2(f32x4_t y[2][4], const f32x4_t acc[2][4
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
         const float v = vrow[16 * c];
-        y[0][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[0][s][i], v, y[0][c], 0, 0, 0);
-        y[1][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[1][s][i], v, y[1][c], 0, 0, 0);
+#pragma unroll
+        for (int m = 0; m < MT; ++m) y[m][c] = __builtin_amdgcn_mfma_f32_16x16x4f32(acc[m][s][i], v, y[m][c], 0, 0, 0);
       }
     }
 }
 
-template <int BF, bool BAND>
+template <int BF, bool BAND, int MT>
 __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
+  constexpr int QB = 64 * MT;  // queries per block
   __shared__ __align__(16) T Ks[2][kTile * S];
   __shared__ __align__(16) T Vs[2][kTile * S];
-  BlockCtx c = block_ctx2(p);
+  BlockCtx c = block_ctx_q<QB>(p);
   const int64_t off = (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Qb = static_cast<const T*>(p.Q) + off;
   const T* Kb = static_cast<const T*>(p.K) + off;
@@ -872,11 +885,11 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   TileRegs kr, vr;
   kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
   vr = tile_load<BF>(Vb, c.d_out, 0, c.n, c.tid);
-  QFrag<BF> qf[2];
-  float cq[2];
-  int klo[2], kspan[2];
+  QFrag<BF> qf[MT];
+  float cq[MT];
+  int klo[MT], kspan[MT];
 #pragma unroll
-  for (int m = 0; m < 2; ++m) {
+  for (int m = 0; m < MT; ++m) {
     const int q = c.q + 16 * m;
     load_qfrag(qf[m], Qb + (int64_t)min(q, c.n - 1) * c.d_out, c.g);
     cq[m] = p.row_c[((int64_t)c.b * p.H + c.h) * c.n + min(q, c.n - 1)];
@@ -885,9 +898,9 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
     if (BAND) query_window(c, q, klo[m], kspan[m]);
   }
 
-  f32x4_t y[2][4];
+  f32x4_t y[MT][4];
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int cc = 0; cc < 4; ++cc) y[m][cc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const int nvis = tile_count(c);
@@ -901,11 +914,11 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
     const int next = tile_at(c, min(t + 1, nvis - 1)) * kTile;
     kr = tile_load<BF>(Kb, c.d_out, next, c.n, c.tid);
     vr = tile_load<BF>(Vb, c.d_out, next, c.n, c.tid);
-    f32x4_t acc[2][4];
-    score_tile2(acc, kb, qf, c.r16, c.g);
+    f32x4_t acc[MT][4];
+    score_tile_m<MT>(acc, kb, qf, c.r16, c.g);
     const int lim = c.len - kt * kTile;
 #pragma unroll
-    for (int m = 0; m < 2; ++m) {
+    for (int m = 0; m < MT; ++m) {
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
@@ -916,14 +929,14 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
         mask_tile<BAND>(acc[m], c, kt, lim);
       }
     }
-    pv_tile2(y, acc, vb, c.r16, c.g);
+    pv_tile_m<MT>(y, acc, vb, c.r16, c.g);
   }
   // y[m][cc][i] = Y[query c.q - r16 + 16 m + 4 g + i][column 16 cc + r16]
 #pragma unroll
-  for (int m = 0; m < 2; ++m)
+  for (int m = 0; m < MT; ++m)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = c.qt * kTile2 + c.wave * 32 + 16 * m + 4 * c.g + i;
+      const int row = c.qt * QB + c.wave * (QB / 4) + 16 * m + 4 * c.g + i;
       if (row < c.n) {
         float* yrow = p.Y + ((int64_t)c.b * c.n + row) * c.d_out + c.h * kDHead + c.r16;
 #pragma unroll
@@ -975,10 +988,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[2][kTile * S];
   __shared__ float cm[2][4][kTile];
-  const BlockCtx c = block_ctx2(p);
+  const BlockCtx c = block_ctx_q<128>(p);
   const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
-  const int qw = c.qt * kTile2 + c.wave * 32;  // the wave's first query
+  const int qw = c.qt * 128 + c.wave * 32;  // the wave's first query
   QFrag<BF> qf[2];
 #pragma unroll
   for (int m = 0; m < 2; ++m) load_qfrag(qf[m], Qb + (int64_t)min(qw + 16 * m + c.r16, c.n - 1) * c.d_out, c.g);
@@ -1178,12 +1191,12 @@ hipError_t launch_attn_band(const FwdParams& p, hipStream_t s) {
     if (nt <= 1) return launch_stage_kernel((k_attn_res<1, 1, BAND>), grid, blk, 0, s, p);
     else if (nt <= 2) return launch_stage_kernel((k_attn_res<1, 2, BAND>), grid, blk, 0, s, p);
     else if (nt <= 4) return launch_stage_kernel((k_attn_res<1, 4, BAND>), grid, blk, 0, s, p);
-    else return launch_stage_kernel((k_attn_stream<1, BAND>), dim3((unsigned)(((p.n + 127) / 128) * p.H * p.B)),
+    else return launch_stage_kernel((k_attn_stream<1, BAND, 2>), dim3((unsigned)(((p.n + 127) / 128) * p.H * p.B)),
                                     blk, 0, s, p);
   } else {
     if (nt <= 1) return launch_stage_kernel((k_attn_res<0, 1, BAND>), grid, blk, 0, s, p);
     else if (nt <= 2) return launch_stage_kernel((k_attn_res<0, 2, BAND>), grid, blk, 0, s, p);
-    else return launch_stage_kernel((k_attn_stream<0, BAND>), dim3((unsigned)(((p.n + 127) / 128) * p.H * p.B)),
+    else return launch_stage_kernel((k_attn_stream<0, BAND, 2>), dim3((unsigned)(((p.n + 127) / 128) * p.H * p.B)),
                                     blk, 0, s, p);
   }
 }
