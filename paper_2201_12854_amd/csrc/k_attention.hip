@@ -9,20 +9,23 @@
 // with the row normaliser c written by the score pass. A is never written to memory
 // (except under the median rule).
 //
-// Tiling: one block = 4 waves = 64 queries of one (batch row, head); a wave owns 16
-// queries (the streaming kernels: 128 queries, 32 per wave). Keys come in tiles of 64 staged in LDS; 16x16 MFMA tiles (bf16 16x16x32 or
-// fp32 16x16x4). The score pass computes S = Q K^T (its layout and reductions are
-// described with the kernels). The output pass computes S^T = K Q^T, so lane l holds the
-// scores of query (l % 16) for keys 16 s + 4 (l / 16) + i (s, i = 0..3): exactly the
-// A-operand layout of the P V MFMA, with no data movement between the two products.
+// Tiling: one block = 4 waves = 64 queries of one (batch row, head), a wave owning 16
+// queries (the streaming kernels: 128 queries, 32 per wave in two 16-query tiles). Keys
+// come in tiles of 64 staged in LDS; 16x16 MFMA tiles (bf16 16x16x32 or fp32 16x16x4).
+// The score pass computes S = Q K^T (its layout and reductions are described with the
+// kernels). The output pass computes S^T = K Q^T, so lane l holds the scores of query
+// (l % 16) for keys 16 s + 4 (l / 16) + i (s, i = 0..3): exactly the A-operand layout of
+// the P V MFMA, with no data movement between the two products.
 //
-// Two variants of each kernel:
-//   resident (padded length <= 64 NT keys): every K (and H~) tile of the sequence is
-//     loaded at once behind one barrier and all scores stay in registers, so the
-//     statistics and the column max come from a single pass;
+// Variants by padded length:
+//   resident (up to 64 NT keys, NT <= 4 for bf16, 2 for fp32): every K (and H~) tile of
+//     the sequence is loaded at once behind one barrier and all scores stay in registers,
+//     so the statistics and the column max come from a single pass;
+//   score pass up to 8 key tiles: K tiles streamed through two LDS buffers, every score
+//     kept in registers, still a single pass;
 //   streaming (longer sequences): tiles are double buffered in LDS with the next tile
-//     prefetched into registers; the score pass sweeps twice (online statistics, then the
-//     column statistic).
+//     prefetched into registers; the score pass sweeps twice (per-lane statistics, then
+//     the column statistic).
 // Local-window attention (Sec. "Longformer": a window of w keys around each token and a
 // global first token): query q attends key k < len when |q - k| <= w / 2, or q = 0, or
 // k = 0; the other scores are masked like padded keys. The column max is then taken of
