@@ -260,14 +260,6 @@ __host__ __device__ inline size_t gather_lds_bytes(int d_in, int wc, bool ldsb) 
          + kNumCtr * 4;                      // counters
 }
 
-// Orders LDS accesses of different lanes of one wavefront: the hardware executes a wave's
-// LDS instructions in issue order, so only compiler reordering has to be prevented.
-__device__ __forceinline__ void wave_lds_sync() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
-}
-
 // LDS reads by 32-bit LDS address (offset into the workgroup's LDS).
 typedef __attribute__((address_space(3))) const float4 lds_float4;
 __device__ __forceinline__ float4 lds_read4(uint32_t addr) {
