@@ -1,5 +1,5 @@
 """Shared helpers of the GPU parity tests: run a synthetic layer through libmca and
-through the CPU oracle, and compare them.
+compare its results with the CPU oracle's.
 
 Tolerances (per valid query row i, relative to the row's largest magnitude):
   float32 layers: ||Y_i - Y_i^ref||_inf <= 1e-5 ||Y_i^ref||_inf
@@ -15,8 +15,6 @@ from __future__ import annotations
 import math
 
 import numpy as np
-
-import oracle
 
 TOL_Y = {"f32": 1e-5, "bf16": 2e-2}
 TOL_H = 1e-5
