@@ -364,6 +364,9 @@ def main():
     ap.add_argument("--cpu-seconds", type=float, default=10.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true", help="skip dense baseline and other alphas")
+    ap.add_argument("--dense-stages-only", type=int, default=0, metavar="STEPS",
+                    help="only time the dense stages at the BERT-large and 4096-token shapes over STEPS "
+                         "passes each and print their JSON (for counter collection; not the bench line)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain copy of MIB MiB (for scaling rocprofv3 byte counters)")
     args = ap.parse_args()
@@ -380,6 +383,9 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a HIP device")
     dev = torch.device("cuda:0")
+    if args.dense_stages_only:
+        print(json.dumps(dense_stage_extras(mca, wl, dev, args.alpha, args.seed, args.dense_stages_only)), flush=True)
+        return
     L = wl.bert_base_bf16()
     elem = 2
     t = {k: torch.from_numpy(getattr(L, k)).to(dev).to(torch.bfloat16).contiguous() for k in ("Q", "K", "X", "Wv")}
