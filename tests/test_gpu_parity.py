@@ -343,6 +343,19 @@ def test_score_pass_variants_ragged(dev, dtype, n, lens, window):
     assert n_tok > 0
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_streaming_score_pass_raised_reference(dev, dtype):
+    # a few shared keys with a logit bump of 20 (about 29 in log2 units) at random places
+    # in rows of 700 keys: when a query meets one after its first tiles, the streaming
+    # score pass must raise its reference logit and rescale its running sum. (A bump of 30
+    # puts the column max's float32 relative error at 1.2e-5 in every version of the score
+    # pass: t = dot log2(e)/8 - c is rounded at |c| near 43, and m = 2^t.)
+    L = wl.make_layer(2, 700, 128, 4, dtype, data_seed=12, lens=np.array([700, 555]), salient_keys=6,
+                      salient_bump=20.0, token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=4)
+    assert n_tok > 0
+
+
 @pytest.mark.parametrize("rule", ["mean", "median"])
 def test_importance_rules_long_rows(dev, rule):
     # mean and median rules through the two-sweep streaming score pass (n = 600)
