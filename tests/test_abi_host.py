@@ -199,3 +199,15 @@ def test_binding_rejects_unknown_rule_names():
     with pytest.raises(ValueError):
         binding._sampling_code("rows")
     assert [binding._importance_code(r) for r in ("max", "mean", "median")] == [0, 1, 2]
+
+
+def test_build_flags():
+    # every HIP source is compiled for gfx950 without packed-fp32 code generation and with
+    # MFMA results in ordinary VGPRs
+    from paper_2201_12854_amd import build_lib
+
+    flags = build_lib.CXXFLAGS
+    assert "--offload-arch=gfx950" in flags
+    i = flags.index("-packed-fp32-ops")
+    assert flags[i - 3:i] == ["-Xclang", "-target-feature", "-Xclang"]
+    assert "-amdgpu-mfma-vgpr-form" in flags
