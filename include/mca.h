@@ -134,8 +134,9 @@ typedef struct mca_forward_desc {
 
 /*
  * Prepared weights: the per-row statistic of the value projection, computed once per
- * weight matrix and cached (Sec. "Formulation of Sampling Probability": it can be
- * embedded in the model or cached), plus a copy of W_v laid out for the exact MFMA path.
+ * weight matrix and kept (Sec. "Formulation of Sampling Probability": it depends on W_v
+ * only, so it need not be recomputed per input), plus a copy of W_v laid out for the
+ * exact MFMA path.
  * Layout of the `prepared` buffer (device, caller-owned):
  *   offset 0:                        rownorm float32 [d_in]
  *                                    rownorm[i] = float32(sqrt(sum_c W_v[i, c]^2)), squares

@@ -8,7 +8,8 @@ It follows Kim & Ko, "Fast Monte-Carlo Approximation of the Attention
 Mechanism" (AAAI-22), step by step, in the paper's notation:
 
   O1  rho_i = ||W[i]||_2, cached once per weight matrix      (Sec. "Formulation of
-      Sampling Probability": the per-row statistic is "embedded in the model or cached")
+      Sampling Probability": the per-row statistic depends on W only, so it is
+      computed once and stored with the model)
   O2  A_h = softmax(a Q_h K_h^T), a = 1/sqrt(d_head)          (Sec. "Self-Attention
       Mechanisms", the definition of A before Eq. 1)
   O3  m_j = max A[:, j]  (largest attention key j receives,   (Sec. "Determining Sample
@@ -427,9 +428,3 @@ def estimator_variance(x, W, w, T: int, r: int) -> float:
     first = sum(x64[i] ** 2 * float(W64[i] @ W64[i]) * T / w[i] for i in keep)
     mean = sum((x64[i] * W64[i] for i in keep), np.zeros(W64.shape[1]))
     return (first - float(mean @ mean)) / r
-
-
-def realised_reduction(r, lens, d_in: int) -> float:
-    """Dense X W_v multiply-adds over sampled ones: sum_b len_b * d_in / sum_j r_j."""
-    total = float(np.sum(r))
-    return float(np.sum(lens)) * d_in / total if total > 0 else float("inf")

@@ -28,6 +28,8 @@
 // similar length, longest first, so that the lanes of a wave and the waves of a block
 // finish close together. No global atomics; outputs do not depend on which wave computes
 // them.
+#include <atomic>
+
 #include "mca_device.h"
 #include "mca_kernels.h"
 
@@ -763,16 +765,18 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
     }
 }
 
+// Per-device host caches below are atomics: concurrent host threads may fill them at once
+// (each writes the same value), and a reader sees either 0 (not yet known) or that value.
 int device_cus() {
-  static int cached[64] = {0};
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (!cached[dev]) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_acquire);
+  if (!n) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_release);
   }
-  return cached[dev];
+  return n;
 }
 
 template <int BF, int WC, bool VEC, bool LDSB>
@@ -781,16 +785,17 @@ hipError_t launch_wc(const FwdParams& p, hipStream_t s) {
   if (lds > 160 * 1024) return hipErrorInvalidValue;  // gfx950: 160 KB of LDS per workgroup
   if (LDSB && p.din_pad > 32 * kLdsbSteps) return hipErrorInvalidValue;
   // the largest slice of the variant plus the lists; allowed once per device
-  static int allowed[64] = {0};
+  static std::atomic<int> allowed[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return hipErrorInvalidDevice;
-  if (!allowed[dev]) {
+  if (!allowed[dev].load(std::memory_order_acquire)) {
+    // idempotent: threads racing here all set the same attribute before any of them launches
     const int dmax = LDSB ? 32 * kLdsbSteps : (WC == 32 ? 1024 : 2048);
     const hipError_t e = hipFuncSetAttribute((const void*)k_gather<BF, WC, VEC, LDSB>,
                                              hipFuncAttributeMaxDynamicSharedMemorySize,
                                              (int)gather_lds_bytes(dmax, WC, LDSB));
     if (e != hipSuccess) return e;
-    allowed[dev] = 1;
+    allowed[dev].store(1, std::memory_order_release);
   }
   const int nslices = p.d_out / WC;
   return launch_stage_kernel(k_gather<BF, WC, VEC, LDSB>, dim3((unsigned)(nslices * p.gather_bps)), dim3(kThreads),

@@ -381,7 +381,8 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
     // query's key count |S_q| (the per-row n of Eq. 9), so t = m / alpha
     const double t = (p.band_half > 0 ? (double)m : (double)len * (double)m) / p.alpha;
     const double tt = t * t;
-    r = (tt >= (double)d_in) ? d_in : max((int)ceil(tt), 1);
+    // a t^2 that is not below d_in (a NaN too: non-finite scores) saturates the token
+    r = !(tt < (double)d_in) ? d_in : max((int)ceil(tt), 1);
   }
   if (live && lane == 0) {
     p.r[tok] = r;

@@ -142,8 +142,14 @@ mca_status run_stage(Profiler* pr, int stage, mca::FwdParams& p, F&& launch) {
   p.ev_stop = slot >= 0 ? pr->stop[slot] : nullptr;
   const hipError_t e = launch();
   p.ev_start = p.ev_stop = nullptr;
-  if (e != hipSuccess)
+  if (e != hipSuccess) {
+    if (slot >= 0) {  // nothing was recorded on the slot's events: give it back
+      std::lock_guard<std::mutex> lk(pr->mu);
+      if (pr->used == slot + 1) --pr->used;
+      else pr->stage[slot] = -1;  // a later slot is taken: collect skips this one
+    }
     return fail(MCA_ERR_HIP, "stage %s launch failed: %s", mca_stage_name(stage), hipGetErrorString(e));
+  }
   return MCA_OK;
 }
 
@@ -300,6 +306,7 @@ mca_status mca_profiler_collect(void* handle, double* stage_ms, int64_t* launche
     launches[i] = 0;
   }
   for (int k = 0; k < pr->used; ++k) {
+    if (pr->stage[k] < 0) continue;  // a launch that failed: its events were never recorded
     if (hipEventSynchronize(pr->stop[k]) != hipSuccess) return fail(MCA_ERR_HIP, "hipEventSynchronize failed");
     float ms = 0.f;
     if (hipEventElapsedTime(&ms, pr->start[k], pr->stop[k]) != hipSuccess)

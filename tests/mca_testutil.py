@@ -7,8 +7,10 @@ Tolerances (per valid query row i, relative to the row's largest magnitude):
                   product in bf16, fp32 accumulation)
   H~ rows (float32 export): 1e-5 in both modes (bf16 inputs are exact in float32 and the
                   gather accumulates in float32)
-  column max m: relative 1e-5 (float32 softmax of float32-accumulated scores)
-Sample counts and sample indices are compared exactly.
+  column statistic m: a per-key relative bound derived from the inputs and the float32
+                  arithmetic of the score pass (``colmax_tolerance``)
+Sample counts and sample indices are compared exactly; counts may differ by one only for
+tokens whose float64 t^2 lies within that bound of an integer (``ambiguous_tokens``).
 """
 from __future__ import annotations
 
@@ -18,7 +20,106 @@ import numpy as np
 
 TOL_Y = {"f32": 1e-5, "bf16": 2e-2}
 TOL_H = 1e-5
-TOL_M = 1e-5
+
+# ---------------------------------------------------------------- column-max error bound
+# The score pass computes, per (batch row, head, query i, key k), in float32:
+#   dot~ = q_i . k_k                        MFMA, products of bf16 exact (of float32 rounded),
+#                                           float32 accumulation in an unknown order
+#   c~_i = M + log2(sum_k exp2(fma(dot~, s32, -M)))   the row normaliser (log2 units),
+#                                           s32 = float32(log2(e) / 8)
+#   t~   = fma(dot~_ik, s32, -c~_i)         (local window: -(c~_i - log2 |S_i|))
+#   m~_k = exp2(max over heads and valid queries of t~)
+# against the float64 oracle's m_k = max A = 2^(max t), t = s dot - c, s = log2(e) / 8.
+# Error terms (u = 2^-24, gamma_m = m u / (1 - m u), Higham's bound for any summation
+# order of m terms):
+#   |dot~ - dot| <= e_ik = gamma_65 sum_d |q_d k_d|
+#   the scale constant: |s32 - s| |dot|
+#   c: c = log2 sum_k 2^(z_k) has gradient p (the row's probabilities) and a Hessian whose
+#      quadratic form is at most ln2 |dz|_max^2, so perturbations dz_k of the logits move
+#      c by at most sum_k p_k |dz_k| + (ln2 / 2) max_k dz_k^2; the sum L of exp2 terms has
+#      relative error <= (u/2) ln2 R (rounding of each fma argument; R the row's logit
+#      range) + eps_exp (each exp2) + gamma_{n/16 + 6} (a lane adds its keys in sequence,
+#      then four butterfly levels combine 16 lanes), plus, in the streaming kernel, one
+#      rescale per visited key tile at most (eps_exp + u each, arguments summing to at
+#      most R) and four DPP combination levels; log2 L within 2u max(1, log2 L); the add
+#      M + log2 L rounds by |c| u / 2
+#   t: the fma rounds by |t| u / 2
+#   m: exp2 of the maximum: eps_exp; the maximum of perturbed values moves by at most
+#      the largest perturbation among the pairs that can be the maximum
+# eps_exp = 2 ulp: v_exp_f32 and v_log_f32 are specified to 1 ulp; a factor of two is kept
+# as margin. The mean rule adds the summation of H len probabilities (gamma_{H len});
+# the median of perturbed values stays within the largest relative perturbation of all
+# the values.
+U32 = 2.0 ** -24
+EPS_EXP = 2.0 * U32
+LOG2E_8 = math.log2(math.e) / 8.0
+S32 = float(np.float32(LOG2E_8))
+
+
+def _gamma(m):
+    return m * U32 / (1.0 - m * U32)
+
+
+def colmax_tolerance(L, importance="max", window=None):
+    """Per-key relative bound [B, n] on |m_gpu - m_ref| / m_ref (0 for padded keys)."""
+    import oracle
+
+    window = L.window if window is None else window
+    B, n, H = L.batch, L.seq, L.heads
+    ntiles = (n + 63) // 64
+    streaming = ntiles > 8
+    ln2 = math.log(2.0)
+    ds = abs(S32 - LOG2E_8)
+    near_w = 1e-2  # log2 units: pairs this far below a key's maximum cannot become it
+    tol = np.zeros((B, n))
+    for b in range(B):
+        Lb = int(L.lens[b])
+        att = oracle.attended(np.arange(Lb), Lb, Lb, window)
+        nk = att.sum(axis=1).astype(np.float64)  # keys per query
+        tmax_h = np.full((H, Lb), -np.inf)
+        dnear_h = np.zeros((H, Lb))
+        dall = np.zeros(Lb)
+        for h in range(H):
+            cs = slice(64 * h, 64 * h + 64)
+            q = L.Q[b, :Lb, cs].astype(np.float64)
+            k = L.K[b, :Lb, cs].astype(np.float64)
+            dot = q @ k.T
+            e = _gamma(65) * (np.abs(q) @ np.abs(k).T)
+            z = np.where(att, LOG2E_8 * dot, -np.inf)
+            zmax = z.max(axis=1)
+            Ls = np.exp2(z - zmax[:, None]).sum(axis=1)
+            c = zmax + np.log2(Ls)
+            R = zmax - np.where(att, z, np.inf).min(axis=1)
+            dL = ln2 * (U32 / 2) * R + EPS_EXP + _gamma(-(-n // 16) + 6)
+            if streaming:
+                dL = dL + ntiles * (EPS_EXP + U32) + ln2 * (U32 / 2) * R + 4 * (EPS_EXP + 1.5 * U32) \
+                     + ln2 * (U32 / 2) * R
+            dz = np.where(att, S32 * e + ds * np.abs(dot), 0.0)  # logit perturbations
+            P = np.exp2(z - c[:, None])  # the row's probabilities (0 off the pattern)
+            dzmax = dz.max(axis=1)
+            Ec = (P * dz).sum(axis=1) + (ln2 / 2) * dzmax ** 2 + dL / ln2 * (1 + 1e-6) \
+                + 2 * U32 * np.maximum(1.0, np.log2(Ls)) + np.abs(c) * U32 / 2
+            t = z - c[:, None]
+            if window > 0:  # t = log2(|S_i| A[i, k]) against c~ - log2 |S_i|
+                lg = np.log2(nk)
+                t = t + lg[:, None]
+                Ec = Ec + np.abs(c - lg) * U32 / 2 + 2 * U32 * np.maximum(1.0, lg)
+            Dt = np.where(att, dz + Ec[:, None] + np.abs(np.where(att, t, 0)) * U32 / 2, 0.0)
+            assert Dt.max() < near_w / 4, Dt.max()
+            tmax = t.max(axis=0)
+            tmax_h[h] = tmax
+            dnear_h[h] = np.where(t >= tmax[None, :] - near_w, Dt, 0.0).max(axis=0)
+            dall = np.maximum(dall, Dt.max(axis=0))
+        if importance == "max":
+            T = tmax_h.max(axis=0)
+            delta = np.where(tmax_h >= T[None, :] - near_w, dnear_h, 0.0).max(axis=0)
+            tol[b, :Lb] = np.exp2(delta) * (1 + EPS_EXP) - 1
+        else:  # every probability enters the mean or the median
+            tol[b, :Lb] = np.exp2(dall) * (1 + EPS_EXP) - 1
+            if importance == "mean":
+                tol[b, :Lb] += _gamma(H * Lb) + 2 * U32
+        tol[b, :Lb] += 1e-12  # the oracle's own float64 rounding
+    return tol
 
 
 def to_device(L, dev):
@@ -72,22 +173,35 @@ def row_rel_err(Y, Yref, lens):
     return worst
 
 
-def ambiguous_tokens(m_ref, lens, alpha, d_in, tol=TOL_M, window=0):
-    """Tokens whose count could change when m moves by a relative `tol`: the float64
-    rule's t^2 range [t^2 (1-tol)^2, t^2 (1+tol)^2] straddles an integer below d_in.
-    (Local window: m carries the per-row factor and t = m / alpha.)"""
+def ambiguous_tokens(m_ref, lens, alpha, d_in, tol, window=0):
+    """Tokens whose count could change when m moves by the relative bound `tol` (a scalar
+    or a per-key array like m_ref): the float64 rule's t^2 range
+    [t^2 (1-tol)^2, t^2 (1+tol)^2] straddles an integer below d_in. (Local window: m
+    carries the per-row factor and t = m / alpha.)"""
+    tol = np.broadcast_to(np.asarray(tol, np.float64), m_ref.shape)
     amb = np.zeros(m_ref.shape, bool)
     for b in range(m_ref.shape[0]):
         L = int(lens[b])
         for j in range(L):
             t = (1 if window else L) * float(m_ref[b, j]) / alpha
-            lo, hi = (t * (1 - tol)) ** 2, (t * (1 + tol)) ** 2
+            lo, hi = (t * (1 - tol[b, j])) ** 2, (t * (1 + tol[b, j])) ** 2
 
             def rule(tt):
                 return d_in if tt >= d_in else max(math.ceil(tt), 1)
 
             amb[b, j] = rule(lo) != rule(hi)
     return amb
+
+
+def check_colmax(m_gpu, m_ref, lens, tol):
+    """m of every valid key within its bound; padded keys exactly 0. Returns the largest
+    error as a fraction of the bound."""
+    valid = np.arange(m_ref.shape[1])[None, :] < np.asarray(lens)[:, None]
+    assert np.all(m_gpu[~valid] == 0)
+    rel = np.abs(m_gpu[valid].astype(np.float64) - m_ref[valid]) / m_ref[valid]
+    bad = rel > tol[valid]
+    assert not bad.any(), (rel[bad][:5], tol[valid][bad][:5])
+    return float((rel / tol[valid]).max())
 
 
 def check_rule_property(r, m, lens, alpha, d_in, window=0):
