@@ -204,6 +204,27 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
                                  float* Y, int32_t* r, void* workspace, size_t workspace_bytes,
                                  void* stream);
 
+/*
+ * For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc): mca_attention_forward without a
+ * workspace argument. The scratch memory (column-max partials, row normalisers, H~ and the
+ * sample lists) is a device array of MCA_NOALLOC_SCRATCH_BYTES inside the library, one per
+ * device, held from the first call on that device until the process ends; the call itself
+ * allocates nothing. Inputs, outputs and results are those of mca_attention_forward with
+ * the same desc (the same kernels run).
+ * Every call on a device shares that device's array and leaves its contents behind (the
+ * kernels need none of them on entry): calls that overlap in time on one device (other
+ * streams, other threads) race on it and must be serialised by the caller.
+ * Errors: as mca_attention_forward, plus MCA_ERR_WORKSPACE_TOO_SMALL when
+ * mca_workspace_size(desc) exceeds MCA_NOALLOC_SCRATCH_BYTES (then nothing is enqueued),
+ * MCA_ERR_INVALID_ARGUMENT when desc->profiler is set (the profiler creates HIP events), and
+ * MCA_ERR_HIP when the array's device address cannot be obtained.
+ */
+#define MCA_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+mca_status mca_attention_forward_noalloc(const mca_forward_desc* desc, const void* Q, const void* K,
+                                         const void* X, const void* W_v, const void* prepared,
+                                         float* Y, int32_t* r, void* stream);
+
 /* Static description of a status code. */
 const char* mca_status_string(mca_status status);
 

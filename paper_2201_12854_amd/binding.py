@@ -83,6 +83,11 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
         return _lib
     if not os.path.exists(path):
         raise RuntimeError(f"{path} is not built; run paper_2201_12854_amd.build_lib.build() first")
+    # torch first: its HIP runtime (same soname as the one libmca.so was linked against)
+    # then serves the library too. Loaded the other way round, the process would end up
+    # with two HIP runtimes, and the second finds no device.
+    import torch  # noqa: F401
+
     lib = ctypes.CDLL(path)
     vp, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     lib.mca_prepared_size.argtypes = [i32, i64, i64, ctypes.POINTER(sz)]
@@ -93,6 +98,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.mca_workspace_size.restype = ctypes.c_int
     lib.mca_attention_forward.argtypes = [ctypes.POINTER(ForwardDesc), vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.mca_attention_forward.restype = ctypes.c_int
+    lib.mca_attention_forward_noalloc.argtypes = [ctypes.POINTER(ForwardDesc), vp, vp, vp, vp, vp, vp, vp, vp]
+    lib.mca_attention_forward_noalloc.restype = ctypes.c_int
     lib.mca_status_string.argtypes = [ctypes.c_int]
     lib.mca_status_string.restype = ctypes.c_char_p
     lib.mca_last_error.argtypes = []
@@ -201,10 +208,14 @@ class ForwardResult:
     encoded: object = None
 
 
+MCA_NOALLOC_SCRATCH_BYTES = 64 << 20  # the no-allocation entry's scratch array per device
+
+
 def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, heads: int,
                       seq_lens=None, r_in=None, export: bool = False, export_samples: bool = False,
                       workspace=None, out=None, profiler=None, sampling: str = "token",
-                      window: int = 0, importance: str = "max", exact_from: int = 0) -> ForwardResult:
+                      window: int = 0, importance: str = "max", exact_from: int = 0,
+                      noalloc: bool = False) -> ForwardResult:
     """One MCA forward pass through libmca on the current HIP stream.
 
     Q, K: [B, n, heads*64]; X: [B, n, d_in]; W_v: [d_in, heads*64]; all float32 or
@@ -212,7 +223,9 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
     seq_lens: optional int32 [B]. r_in: optional int32 [B, n] overriding the count
     rule. ``export`` also returns the column max and H~ (float32); ``export_samples``
     the per-draw indices and coefficients ([B, n, d_in], first r_j entries valid).
-    ``out`` may pass preallocated (Y, r). ``sampling``: "token" (Eq. 4, per token) or
+    ``out`` may pass preallocated (Y, r). ``noalloc``: call mca_attention_forward_noalloc,
+    whose scratch memory is the library's own device array (no workspace; the outputs are
+    still allocated here unless ``out`` passes them). ``sampling``: "token" (Eq. 4, per token) or
     "weight" (Eq. 6, the paper's input-independent probability). ``window``: 0 for full
     attention, or an even local window (keys within window / 2 of each query, plus a
     global first token). ``importance``: "max" (Eq. 8-9), "mean" or "median", the per-key
@@ -250,17 +263,22 @@ def attention_forward(Q, K, X, W_v, prepared, alpha: float, seed: int = 0, *, he
                      sample_coef_out=res.sample_coef, encoded_out=res.encoded, profiler=profiler,
                      sampling=_sampling_code(sampling), window=window,
                      importance=_importance_code(importance), exact_from=exact_from)
-    ws_bytes = workspace_size(desc)
-    if workspace is None or workspace.numel() < ws_bytes:
-        workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
     if out is None:
         Y = torch.empty((B, n, d_out), dtype=torch.float32, device=dev)
         r = torch.empty((B, n), dtype=torch.int32, device=dev)
     else:
         Y, r = out
-    _check(lib.mca_attention_forward(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(prepared),
-                                     _ptr(Y), _ptr(r), _ptr(workspace), workspace.numel(),
-                                     _stream_handle(dev)), "mca_attention_forward")
+    if noalloc:
+        _check(lib.mca_attention_forward_noalloc(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v),
+                                                 _ptr(prepared), _ptr(Y), _ptr(r), _stream_handle(dev)),
+               "mca_attention_forward_noalloc")
+    else:
+        ws_bytes = workspace_size(desc)
+        if workspace is None or workspace.numel() < ws_bytes:
+            workspace = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+        _check(lib.mca_attention_forward(ctypes.byref(desc), _ptr(Q), _ptr(K), _ptr(X), _ptr(W_v), _ptr(prepared),
+                                         _ptr(Y), _ptr(r), _ptr(workspace), workspace.numel(),
+                                         _stream_handle(dev)), "mca_attention_forward")
     res.Y, res.r = Y, r
     return res
 

@@ -1,6 +1,7 @@
 // C ABI of libmca: argument checks, workspace layout, stage launches, profiler.
 #include <hip/hip_runtime.h>
 
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -215,11 +216,16 @@ mca_status mca_prepare_weights(const void* W_v, int32_t dtype, int64_t d_in, int
   return ok();
 }
 
-mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, const void* K, const void* X,
-                                 const void* W_v, const void* prepared, float* Y, int32_t* r, void* workspace,
-                                 size_t workspace_bytes, void* stream) {
-  mca_status st = check_desc(desc);
-  if (st != MCA_OK) return st;
+}  // extern "C"
+
+namespace {
+
+// Checks the tensors of a forward call and enqueues its stage kernels with `workspace` as the
+// scratch memory (the caller's workspace, or the no-allocation entry's device array).
+mca_status forward_impl(const mca_forward_desc* desc, const void* Q, const void* K, const void* X, const void* W_v,
+                        const void* prepared, float* Y, int32_t* r, void* workspace, size_t workspace_bytes,
+                        void* stream) {
+  mca_status st;
   if (!Q || !K || !X || !W_v || !prepared || !Y || !r || !workspace)
     return fail(MCA_ERR_INVALID_ARGUMENT, "Q, K, X, W_v, prepared, Y, r and workspace must not be NULL");
   const void* req[] = {Q, K, X, W_v, prepared, Y, r, workspace};
@@ -286,6 +292,66 @@ mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, co
   if ((st = run_stage(pr, MCA_STAGE_GATHER, p, [&] { return mca::launch_gather(p, s); })) != MCA_OK) return st;
   if ((st = run_stage(pr, MCA_STAGE_ATTN_OUT, p, [&] { return mca::launch_attn_out(p, s); })) != MCA_OK) return st;
   return ok();
+}
+
+// ------------------------------------------------------------------ no-allocation entry
+// Scratch memory of mca_attention_forward_noalloc: one array per device, held from the first
+// call on that device until the process ends. Host code never passes the array's name to a
+// kernel (on the host it is only a stand-in for the symbol): the device address comes from
+// hipGetSymbolAddress, taken once per device with that device current, and is kept per device.
+constexpr size_t kScratchBytes = MCA_NOALLOC_SCRATCH_BYTES;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+mca_status scratch_of_current_device(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fail(MCA_ERR_HIP, "hipGetDevice failed: %s", hipGetErrorString(e));
+  if (dev < 0 || dev >= kMaxDevices) return fail(MCA_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kMaxDevices);
+  void* ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!ptr) {
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    ptr = g_scratch_ptr[dev].load(std::memory_order_relaxed);
+    if (!ptr) {
+      e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+      if (e != hipSuccess || !ptr)
+        return fail(MCA_ERR_HIP, "hipGetSymbolAddress of the scratch array failed on device %d: %s", dev,
+                    hipGetErrorString(e));
+      g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+    }
+  }
+  *out = ptr;
+  return MCA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+mca_status mca_attention_forward(const mca_forward_desc* desc, const void* Q, const void* K, const void* X,
+                                 const void* W_v, const void* prepared, float* Y, int32_t* r, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  mca_status st = check_desc(desc);
+  if (st != MCA_OK) return st;
+  return forward_impl(desc, Q, K, X, W_v, prepared, Y, r, workspace, workspace_bytes, stream);
+}
+
+mca_status mca_attention_forward_noalloc(const mca_forward_desc* desc, const void* Q, const void* K, const void* X,
+                                         const void* W_v, const void* prepared, float* Y, int32_t* r, void* stream) {
+  mca_status st = check_desc(desc);
+  if (st != MCA_OK) return st;
+  if (desc->profiler)
+    return fail(MCA_ERR_INVALID_ARGUMENT, "mca_attention_forward_noalloc takes no profiler (it creates HIP events)");
+  const size_t need = layout_for(*desc).total;
+  if (need > kScratchBytes)
+    return fail(MCA_ERR_WORKSPACE_TOO_SMALL, "the call needs %zu bytes of scratch; the no-allocation entry holds %zu",
+                need, kScratchBytes);
+  void* ws = nullptr;
+  if ((st = scratch_of_current_device(&ws)) != MCA_OK) return st;
+  return forward_impl(desc, Q, K, X, W_v, prepared, Y, r, ws, kScratchBytes, stream);
 }
 
 mca_status mca_profiler_create(void** handle) {
