@@ -952,29 +952,40 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
 // Streaming score pass (rows longer than 8 key tiles): 128 queries per block, two 16-query
 // tiles per wave, so that every K fragment read from LDS feeds two MFMAs and the per-tile
 // work (tile loads and stores, barriers, lane swaps, partial stores) serves twice the
-// queries. Two sweeps over the visited tiles: per-lane statistics, then the column
+// queries. Two sweeps over the visited tiles: per-lane row statistics, then the column
 // statistic, one partial per (key, head, 128-query tile).
+//
+// Both sweeps are software pipelined: the MFMAs of tile t + 1 are issued before the VALU
+// work on tile t's scores, so the matrix cores and the vector units of a wave work at the
+// same time (a wave's MFMA results are only read one iteration later). The loop is unrolled
+// by two so that the two accumulator sets swap roles without register copies.
+//
+// Sweep 2 folds the row normaliser into the MFMA: its accumulators start at -c_q / s
+// (s = log2(e) / 8) instead of 0, so an accumulator holds dot - c_q / s, whose maximum over
+// the lane's queries needs no per-score arithmetic; the maximum over the block is scaled by
+// s once per key: t = s * max(dot - c_q / s) = max(dot s - c_q) (s > 0).
 
-// S = Q K^T of two 16-query tiles: acc[m][s][i] = dot(query 16 m + 4 g + i, key 16 s + r16).
+// S = Q K^T of two 16-query tiles: acc[m][s][i] = dot(query 16 m + 4 g + i, key 16 s + r16)
+// + init[m][i].
 __device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const uint16_t* Ks, const QFrag<1> q[2], int r16,
-                                               int g) {
+                                               int g, const f32x4_t init[2]) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    acc[0][s] = acc[1][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 * ks + 8 * g);
-      acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[0].v[ks], b, acc[0][s], 0, 0, 0);
-      acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[1].v[ks], b, acc[1][s], 0, 0, 0);
-    }
+    const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 8 * g);
+    const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 + 8 * g);
+    acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[0].v[0], b0, init[0], 0, 0, 0);
+    acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[1].v[0], b0, init[1], 0, 0, 0);
+    acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[0].v[1], b1, acc[0][s], 0, 0, 0);
+    acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[1].v[1], b1, acc[1][s], 0, 0, 0);
   }
 }
 
 __device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const float* Ks, const QFrag<0> q[2], int r16,
-                                               int g) {
+                                               int g, const f32x4_t init[2]) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    acc[0][s] = acc[1][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    acc[0][s] = init[0];
+    acc[1][s] = init[1];
     const float* krow = Ks + (16 * s + r16) * kStrideF + 16 * g;
 #pragma unroll
     for (int t = 0; t < 16; ++t) {
@@ -985,12 +996,15 @@ __device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const float* K
   }
 }
 
-template <int BF, bool BAND>
+// IMP: the column statistic, 0 max (Eq. 8-9), 1 mean, 2 median (every probability to acol).
+template <int BF, bool BAND, int IMP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_scores_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[2][kTile * S];
-  __shared__ float cm[2][4][kTile];
+  // sweep 2: per tile (three in flight), per wave and lane row, the lane row's value of key
+  // 16 s + r16 at [r16][s]
+  __shared__ __align__(16) float cm[3][4][4][16][4];
   const BlockCtx c = block_ctx_q<128>(p);
   const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
@@ -1025,66 +1039,97 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
           if (!ok) acc[m][s][i] = -INFINITY;
         }
   };
+  const int nvis = tile_count(c);
+  // One sweep over the visited tiles, software pipelined: K tile t + 1 is staged in LDS buffer
+  // (t + 1) & 1 and its scores issued on the matrix cores before `work` runs on tile t's
+  // scores. The barrier of iteration t orders the LDS stores of tile t + 1 before their reads
+  // and the reads of tile t - 1 (same buffer, two iterations earlier) before those stores.
+  // Every iteration does the same (the last one stages and multiplies the last tile again,
+  // with results unused), so that the MFMAs and the VALU work of an iteration form one
+  // straight-line region that `work` can interleave; it also gives every iteration a barrier
+  // (sweep 2 combines the waves' values of tile t - 1 after iteration t's barrier).
+  auto sweep = [&](const f32x4_t init[2], auto&& work) {
+    TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+    tile_store<BF>(kr, Ks[0], c.tid);
+    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(1, nvis - 1)) * kTile, c.n, c.tid);
+    lds_barrier();
+    f32x4_t accA[2][4], accB[2][4];
+    score_tile_qk2(accA, Ks[0], qf, c.r16, c.g, init);
+    auto step = [&](f32x4_t cur[2][4], f32x4_t nxt[2][4], int t) {
+      const int kt = tile_at(c, t);
+      const int lim = c.len - kt * kTile;
+      if (BAND || lim < kTile) mask(cur, kt, lim);  // tile-uniform
+      T* buf = Ks[(t + 1) & 1];
+      tile_store<BF>(kr, buf, c.tid);
+      lds_barrier();
+      kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 2, nvis - 1)) * kTile, c.n, c.tid);
+      score_tile_qk2(nxt, buf, qf, c.r16, c.g, init);
+      work(cur, t, kt);
+    };
+    int t = 0;
+    for (; t + 1 < nvis; t += 2) {
+      step(accA, accB, t);
+      step(accB, accA, t + 1);
+    }
+    if (t < nvis) step(accA, accB, t);
+  };
 
   // Sweep 1: per lane and query, a reference logit M and the sum of exp2(logit - M) over
-  // the lane's keys; the 16 lanes of a row are combined at the end. M is raised to the
-  // running max only when a tile holds a logit more than kRescale above it (after the
-  // first tiles, rarely): otherwise the terms, all below 2^kRescale, are added without
-  // rescaling. The branch is wave-uniform.
+  // the lane's keys; the 16 lanes of a row are combined at the end. The terms are added
+  // under the current reference as long as a tile's four terms of a query sum to at most
+  // 2^16 (no score more than 16 log2 units above M); otherwise (the first tile, and rarely
+  // later) the wave redoes the tile with M raised to the running max and rescales the sum.
+  // The branch is wave-uniform.
   constexpr float kNoMax = -1e30f;  // below every logit: no attended key seen yet
-  constexpr float kRescale = 16.f;
-  constexpr float kInvScale = (float)(8.0 / 1.4426950408889634);  // 1 / (log2(e) / 8)
-  float M[8], Ls[8], thr[8];  // thr: the largest dot product M admits, (M + kRescale) / (log2(e) / 8)
+  constexpr float kRaise = 65536.f;
+  float M[8], Ls[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     M[k] = kNoMax;
     Ls[k] = 0.f;
-    thr[k] = kNoMax;
   }
-  const int nvis = tile_count(c);
-  TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  for (int t = 0; t < nvis; ++t) {
-    const int kt = tile_at(c, t);
-    T* buf = Ks[t & 1];
-    tile_store<BF>(kr, buf, c.tid);
-    lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
-    f32x4_t acc[2][4];
-    score_tile_qk2(acc, buf, qf, c.r16, c.g);
-    const int lim = c.len - kt * kTile;
-    if (BAND || lim < kTile) mask(acc, kt, lim);  // tile-uniform
-    float dm[8];
+  const f32x4_t zero2[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
+  sweep(zero2, [&](f32x4_t acc[2][4], int, int) {
+    float ts[8];
     bool raise = false;
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int m = k >> 2, i = k & 3;
-      dm[k] = vmax(vmax3(acc[m][0][i], acc[m][1][i], acc[m][2][i]), acc[m][3][i]);
-      raise |= dm[k] > thr[k];
+      float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -M[k]));
+#pragma unroll
+      for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
+      ts[k] = e;
+      raise |= !(e <= kRaise);
+    }
+    // interleave the next tile's LDS reads and MFMAs with this tile's VALU work
+#pragma unroll
+    for (int s = 0; s < 4; ++s) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads: K fragments of one s
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // six VALU
+      }
     }
     if (__any(raise)) {
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
         const int m = k >> 2, i = k & 3;
-        const float Mn = vmax(M[k], __fmul_rn(dm[k], kLog2eOver8));
-        float sum = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -Mn));
+        const float dm = vmax(vmax3(acc[m][0][i], acc[m][1][i], acc[m][2][i]), acc[m][3][i]);
+        const float Mn = vmax(M[k], __fmul_rn(dm, kLog2eOver8));
+        float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -Mn));
 #pragma unroll
-        for (int s = 1; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -Mn));
-        Ls[k] = __fmul_rn(Ls[k], exp2_fast(__fsub_rn(M[k], Mn))) + sum;
+        for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -Mn));
+        Ls[k] = __fmul_rn(Ls[k], exp2_fast(__fsub_rn(M[k], Mn))) + e;
         M[k] = Mn;
-        thr[k] = __fmul_rn(Mn + kRescale, kInvScale);
       }
     } else {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int m = k >> 2, i = k & 3;
-        float sum = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -M[k]));
-#pragma unroll
-        for (int s = 1; s < 4; ++s) sum += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
-        Ls[k] += sum;
-      }
+      for (int k = 0; k < 8; ++k) Ls[k] += ts[k];
     }
-  }
+  });
   float cq[8], cc[8];
+  f32x4_t dneg[2];  // sweep 2's accumulator start: -cc / s per query (-inf for padded queries)
 #pragma unroll
   for (int k = 0; k < 8; ++k) {
     float Mi = M[k], Li = Ls[k];
@@ -1099,6 +1144,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     float off = cq[k];
     if constexpr (BAND) off = cq[k] - __builtin_amdgcn_logf((float)(kspan[k] + 1 + (klo[k] > 0 ? 1 : 0)));
     cc[k] = q >= c.len ? INFINITY : off;
+    dneg[k >> 2][k & 3] = -__fdiv_rn(cc[k], kLog2eOver8);
   }
   {  // c of query qw + 16 m + 4 g + i from lane r16 = 4 m + i of each lane row
     float v = cq[0];
@@ -1108,10 +1154,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     if (c.r16 < 8 && q < c.n) p.row_c[((int64_t)c.b * p.H + c.h) * c.n + q] = v;
   }
 
-  // Sweep 2: the per-key column statistic of this block's valid queries. The t-th visited
-  // tile uses K buffer t & 1 and column slot t & 1; the barrier after its LDS store also
-  // orders the reads of tile t - 2's slot before this tile's writes.
-  lds_barrier();  // sweep 1 is done with both K buffers
+  // Sweep 2: the per-key column statistic of this block's valid queries. Each lane row of each
+  // wave leaves its value of tile t's keys (over its four queries of each of the wave's two
+  // query tiles) in cm[t % 3][wave][row]; after the barrier of iteration t + 1 (or the final
+  // one), threads 0..63 combine the sixteen values of a key in a fixed order and store the
+  // block's partial. A slot is reused three tiles later, after two more barriers.
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
   if (BAND) {  // valid keys of the tiles outside the window get a zero partial
     for (int key = kTile + c.tid; key < c.len; key += kThreads) {
@@ -1119,51 +1166,89 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
     }
   }
-  const bool sum = p.importance == 1;
-  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  for (int t = 0; t < nvis; ++t) {
-    const int kt = tile_at(c, t);
-    T* buf = Ks[t & 1];
-    float (*cmk)[kTile] = cm[t & 1];
-    tile_store<BF>(kr, buf, c.tid);
-    lds_barrier();
-    kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
-    f32x4_t acc[2][4];
-    score_tile_qk2(acc, buf, qf, c.r16, c.g);
-    const int lim = c.len - kt * kTile;
-    if (BAND || lim < kTile) mask(acc, kt, lim);  // tile-uniform
-    // t = dot a log2(e) - cc over the lane's eight queries: max (or sum of exp2) per key,
-    // then over the four lane rows; lane row 0 leaves the wave's value in LDS
+  constexpr bool sum = IMP == 1;
+  auto combine = [&](int t) {  // the block's partial of tile t's keys
+    if (c.tid < kTile) {
+      const int e = c.tid, r16 = e & 15, sk = e >> 4;  // key 16 sk + r16 of the tile
+      float x[16];
+#pragma unroll
+      for (int w = 0; w < 4; ++w)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) x[4 * w + g] = cm[t % 3][w][g][r16][sk];
+      float r;
+      if constexpr (sum) {
+        float a[4];
+#pragma unroll
+        for (int w = 0; w < 4; ++w) a[w] = (x[4 * w] + x[4 * w + 1]) + (x[4 * w + 2] + x[4 * w + 3]);
+        r = (a[0] + a[1]) + (a[2] + a[3]);
+      } else {
+        const float a = vmax3(x[0], x[1], x[2]), b = vmax3(x[3], x[4], x[5]), c2 = vmax3(x[6], x[7], x[8]);
+        const float d = vmax3(x[9], x[10], x[11]), f = vmax3(x[12], x[13], x[14]);
+        r = exp2_fast(__fmul_rn(vmax3(vmax3(a, b, c2), vmax3(d, f, x[15]), a), kLog2eOver8));
+      }
+      const int key = tile_at(c, t) * kTile + e;
+      if (key < c.n) part[(int64_t)key * p.nparts] = r;
+    }
+  };
+  lds_barrier();  // sweep 1 is done with both K buffers
+  sweep(dneg, [&](f32x4_t acc[2][4], int t, int kt) {
+    // the lane's eight queries per key: the max of dot - cc / s (or the sum of the
+    // probabilities exp2(s (dot - cc / s))), left in cm for the combination over the lane
+    // rows and waves
     float v[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) {
-      float x[8];
+      if constexpr (sum) {
+        float e = 0.f;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) x[k] = __fmaf_rn(acc[k >> 2][s][k & 3], kLog2eOver8, -cc[k]);
-      if (sum) {
-        float e = exp2_fast(x[0]);
-#pragma unroll
-        for (int k = 1; k < 8; ++k) e += exp2_fast(x[k]);
-        v[s] = pair32_sum(pair16_sum(e));
+        for (int k = 0; k < 8; ++k) e += exp2_fast(__fmul_rn(acc[k >> 2][s][k & 3], kLog2eOver8));
+        v[s] = e;
       } else {
-        v[s] = pair32_max(pair16_max(vmax3(vmax3(x[0], x[1], x[2]), vmax3(x[3], x[4], x[5]), vmax(x[6], x[7]))));
+        v[s] = vmax3(vmax3(acc[0][s][0], acc[0][s][1], acc[0][s][2]), vmax3(acc[0][s][3], acc[1][s][0], acc[1][s][1]),
+                     vmax(acc[1][s][2], acc[1][s][3]));
       }
     }
-    if (c.g == 0) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s) cmk[c.wave][16 * s + c.r16] = v[s];
-    }
-    if (p.acol) {
+    for (int s = 0; s < 4; ++s) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads: K fragments of one s
 #pragma unroll
-      for (int m = 0; m < 2; ++m) store_probs(p, c, acc[m], kt, cq + 4 * m, qw + 16 * m + 4 * c.g);
+      for (int j = 0; j < 4; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // two VALU
+      }
     }
-    lds_barrier();
-    if (c.tid < kTile) {
-      const float w = sum ? (cmk[0][c.tid] + cmk[1][c.tid]) + (cmk[2][c.tid] + cmk[3][c.tid])
-                          : exp2_fast(vmax(vmax3(cmk[0][c.tid], cmk[1][c.tid], cmk[2][c.tid]), cmk[3][c.tid]));
-      const int key = kt * kTile + c.tid;
-      if (key < c.n) part[(int64_t)key * p.nparts] = w;
+    *reinterpret_cast<float4*>(&cm[t % 3][c.wave][c.g][c.r16][0]) = make_float4(v[0], v[1], v[2], v[3]);
+    if constexpr (IMP == 2) {  // median rule: every probability, exp2(s (dot - cc / s))
+      float* ac = p.acol + (int64_t)c.b * c.n * p.H * c.n;
+#pragma unroll
+      for (int m = 0; m < 2; ++m)
+#pragma unroll
+        for (int s = 0; s < 4; ++s) {
+          const int key = kt * kTile + 16 * s + c.r16;
+          if (key < c.n) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int q = qw + 16 * m + 4 * c.g + i;
+              if (q < c.n) ac[((int64_t)key * p.H + c.h) * c.n + q] = exp2_fast(__fmul_rn(acc[m][s][i], kLog2eOver8));
+            }
+          }
+        }
     }
+    if (t > 0) combine(t - 1);  // the barrier of this iteration follows every wave's tile t - 1 values
+  });
+  lds_barrier();
+  combine(nvis - 1);
+}
+
+template <int BF, bool BAND>
+hipError_t launch_scores_stream(const FwdParams& p, hipStream_t s) {
+  const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
+  if constexpr (BAND) {  // the mean and median rules are defined for full attention only
+    return launch_stage_kernel((k_scores_stream<BF, true, 0>), grid, blk, 0, s, p);
+  } else {
+    if (p.importance == 1) return launch_stage_kernel((k_scores_stream<BF, false, 1>), grid, blk, 0, s, p);
+    if (p.importance == 2) return launch_stage_kernel((k_scores_stream<BF, false, 2>), grid, blk, 0, s, p);
+    return launch_stage_kernel((k_scores_stream<BF, false, 0>), grid, blk, 0, s, p);
   }
 }
 
@@ -1177,12 +1262,12 @@ hipError_t launch_scores_band(const FwdParams& p, hipStream_t s) {
     else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2, BAND>), grid, blk, 0, s, p);
     else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4, BAND>), grid, blk, 0, s, p);
     else if (nt <= 8) return launch_stage_kernel((k_scores_rs<1, 8, BAND>), grid, blk, 0, s, p);
-    else return launch_stage_kernel((k_scores_stream<1, BAND>), dim3((unsigned)(p.qtiles * p.H * p.B)), blk, 0, s, p);
+    else return launch_scores_stream<1, BAND>(p, s);
   } else {
     if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1, BAND>), grid, blk, 0, s, p);
     else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2, BAND>), grid, blk, 0, s, p);
     else if (nt <= 8) return launch_stage_kernel((k_scores_rs<0, 8, BAND>), grid, blk, 0, s, p);
-    else return launch_stage_kernel((k_scores_stream<0, BAND>), dim3((unsigned)(p.qtiles * p.H * p.B)), blk, 0, s, p);
+    else return launch_scores_stream<0, BAND>(p, s);
   }
 }
 

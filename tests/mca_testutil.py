@@ -46,6 +46,11 @@ TOL_H = 1e-5
 #   t: the fma rounds by |t| u / 2
 #   m: exp2 of the maximum: eps_exp; the maximum of perturbed values moves by at most
 #      the largest perturbation among the pairs that can be the maximum
+# The streaming kernel (rows longer than 8 key tiles) differs in three places: its running
+# reference sits up to 16 log2 units below the row max (the exp2 arguments reach R + 16);
+# its column statistic starts the MFMA accumulator at d = float32(c~ / s32) and takes
+# t~ = s32 max(dot - d): the rounding of d (|c| u / 2) and the accumulation of 64 products
+# onto it (gamma_65 |c|, as the products' own term) add to the error of t.
 # eps_exp = 2 ulp: v_exp_f32 and v_log_f32 are specified to 1 ulp; a factor of two is kept
 # as margin. The mean rule adds the summation of H len probabilities (gamma_{H len});
 # the median of perturbed values stays within the largest relative perturbation of all
@@ -90,7 +95,7 @@ def colmax_tolerance(L, importance="max", window=None):
             Ls = np.exp2(z - zmax[:, None]).sum(axis=1)
             c = zmax + np.log2(Ls)
             R = zmax - np.where(att, z, np.inf).min(axis=1)
-            dL = ln2 * (U32 / 2) * R + EPS_EXP + _gamma(-(-n // 16) + 6)
+            dL = ln2 * (U32 / 2) * (R + (16.0 if streaming else 0.0)) + EPS_EXP + _gamma(-(-n // 16) + 6)
             if streaming:
                 dL = dL + ntiles * (EPS_EXP + U32) + ln2 * (U32 / 2) * R + 4 * (EPS_EXP + 1.5 * U32) \
                      + ln2 * (U32 / 2) * R
@@ -104,6 +109,9 @@ def colmax_tolerance(L, importance="max", window=None):
                 lg = np.log2(nk)
                 t = t + lg[:, None]
                 Ec = Ec + np.abs(c - lg) * U32 / 2 + 2 * U32 * np.maximum(1.0, lg)
+            if streaming:  # the accumulator's start d = c' / s (c' = c, or c - log2 |S_i|)
+                cp = np.abs(c - np.log2(nk)) if window > 0 else np.abs(c)
+                Ec = Ec + (_gamma(65) * (1 + U32) + U32 / 2) * cp
             Dt = np.where(att, dz + Ec[:, None] + np.abs(np.where(att, t, 0)) * U32 / 2, 0.0)
             assert Dt.max() < near_w / 4, Dt.max()
             tmax = t.max(axis=0)
