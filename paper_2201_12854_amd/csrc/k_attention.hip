@@ -872,6 +872,12 @@ __device__ __forceinline__ void pv_tile_m(f32x4_t y[MT][4], const f32x4_t acc[MT
     }
 }
 
+// Software pipelined like the streaming score pass: iteration t issues the Q K^T MFMAs of tile
+// t + 1 before the VALU work (exp2, bf16 packing) on tile t's scores and tile t's P V MFMAs.
+// K and H~ tiles are double buffered in LDS with different schedules: K tile t + 1 is
+// stored before iteration t's barrier (its buffer was last read by the Q K^T of tile t - 1,
+// issued in iteration t - 2), H~ tile t + 1 after it (its buffer was last read by the P V of
+// tile t - 1 in iteration t - 1, which every wave has finished once it passes the barrier).
 template <int BF, bool BAND, int MT>
 __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
@@ -885,9 +891,6 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   const T* Kb = static_cast<const T*>(p.K) + off;
   const T* Vb = static_cast<const T*>(p.Henc) + off;
 
-  TileRegs kr, vr;
-  kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-  vr = tile_load<BF>(Vb, c.d_out, 0, c.n, c.tid);
   QFrag<BF> qf[MT];
   float cq[MT];
   int klo[MT], kspan[MT];
@@ -907,33 +910,53 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
 #pragma unroll
     for (int cc = 0; cc < 4; ++cc) y[m][cc] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   const int nvis = tile_count(c);
-  for (int t = 0; t < nvis; ++t) {
+  TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  TileRegs vr = tile_load<BF>(Vb, c.d_out, 0, c.n, c.tid);
+  tile_store<BF>(kr, Ks[0], c.tid);
+  tile_store_v<BF>(vr, Vs[0], c.tid);
+  const int t1 = tile_at(c, min(1, nvis - 1)) * kTile;
+  kr = tile_load<BF>(Kb, c.d_out, t1, c.n, c.tid);
+  vr = tile_load<BF>(Vb, c.d_out, t1, c.n, c.tid);
+  lds_barrier();
+  f32x4_t accA[MT][4], accB[MT][4];
+  score_tile_m<MT>(accA, Ks[0], qf, c.r16, c.g);
+  auto step = [&](f32x4_t cur[MT][4], f32x4_t nxt[MT][4], int t) {
     const int kt = tile_at(c, t);
-    T* kb = Ks[t & 1];
-    T* vb = Vs[t & 1];
-    tile_store<BF>(kr, kb, c.tid);
-    tile_store_v<BF>(vr, vb, c.tid);
+    const int lim = c.len - kt * kTile;
+    if (__builtin_expect(BAND || lim < kTile, 0)) {  // tile-uniform: masked scores give probability 0
+#pragma unroll
+      for (int m = 0; m < MT; ++m) {
+        c.klo = klo[m];
+        c.kspan = kspan[m];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+          for (int i = 0; i < 4; ++i)
+            if (!key_ok<BAND>(c, kt, lim, s, i)) cur[m][s][i] = -INFINITY;
+      }
+    }
+    const int nb = (t + 1) & 1;
+    tile_store<BF>(kr, Ks[nb], c.tid);
     lds_barrier();
-    const int next = tile_at(c, min(t + 1, nvis - 1)) * kTile;
+    tile_store_v<BF>(vr, Vs[nb], c.tid);
+    const int next = tile_at(c, min(t + 2, nvis - 1)) * kTile;
     kr = tile_load<BF>(Kb, c.d_out, next, c.n, c.tid);
     vr = tile_load<BF>(Vb, c.d_out, next, c.n, c.tid);
-    f32x4_t acc[MT][4];
-    score_tile_m<MT>(acc, kb, qf, c.r16, c.g);
-    const int lim = c.len - kt * kTile;
+    score_tile_m<MT>(nxt, Ks[nb], qf, c.r16, c.g);  // tile t + 1 (the last iteration repeats a tile, unused)
 #pragma unroll
-    for (int m = 0; m < MT; ++m) {
+    for (int m = 0; m < MT; ++m)
 #pragma unroll
       for (int s = 0; s < 4; ++s)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) acc[m][s][i] = exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -cq[m]));
-      if (BAND || lim < kTile) {  // tile-uniform
-        c.klo = klo[m];
-        c.kspan = kspan[m];
-        mask_tile<BAND>(acc[m], c, kt, lim);
-      }
-    }
-    pv_tile_m<MT>(y, acc, vb, c.r16, c.g);
+        for (int i = 0; i < 4; ++i) cur[m][s][i] = exp2_fast(__fmaf_rn(cur[m][s][i], kLog2eOver8, -cq[m]));
+    pv_tile_m<MT>(y, cur, Vs[t & 1], c.r16, c.g);
+  };
+  int t = 0;
+  for (; t + 1 < nvis; t += 2) {
+    step(accA, accB, t);
+    step(accB, accA, t + 1);
   }
+  if (t < nvis) step(accA, accB, t);
   // y[m][cc][i] = Y[query c.q - r16 + 16 m + 4 g + i][column 16 cc + r16]
 #pragma unroll
   for (int m = 0; m < MT; ++m)
@@ -1045,8 +1068,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // scores. The barrier of iteration t orders the LDS stores of tile t + 1 before their reads
   // and the reads of tile t - 1 (same buffer, two iterations earlier) before those stores.
   // Every iteration does the same (the last one stages and multiplies the last tile again,
-  // with results unused), so that the MFMAs and the VALU work of an iteration form one
-  // straight-line region that `work` can interleave; it also gives every iteration a barrier
+  // with results unused): one straight-line region per tile, and a barrier in every iteration
   // (sweep 2 combines the waves' values of tile t - 1 after iteration t's barrier).
   auto sweep = [&](const f32x4_t init[2], auto&& work) {
     TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
@@ -1100,16 +1122,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
       ts[k] = e;
       raise |= !(e <= kRaise);
-    }
-    // interleave the next tile's LDS reads and MFMAs with this tile's VALU work
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads: K fragments of one s
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 6, 0);  // six VALU
-      }
     }
     if (__any(raise)) {
 #pragma unroll
@@ -1206,15 +1218,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       } else {
         v[s] = vmax3(vmax3(acc[0][s][0], acc[0][s][1], acc[0][s][2]), vmax3(acc[0][s][3], acc[1][s][0], acc[1][s][1]),
                      vmax(acc[1][s][2], acc[1][s][3]));
-      }
-    }
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);  // DS reads: K fragments of one s
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one MFMA
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);  // two VALU
       }
     }
     *reinterpret_cast<float4*>(&cm[t % 3][c.wave][c.g][c.r16][0]) = make_float4(v[0], v[1], v[2], v[3]);
