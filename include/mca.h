@@ -225,8 +225,9 @@ mca_status mca_attention_forward_noalloc(const mca_forward_desc* desc, const voi
                                          const void* X, const void* W_v, const void* prepared,
                                          float* Y, int32_t* r, void* stream);
 
-/* Static description of a status code. */
-const char* mca_status_string(mca_status status);
+/* Static description of a status code (an mca_status value; any other value gives
+   "MCA_ERR_UNKNOWN"). */
+const char* mca_status_string(int status);
 
 /* Reason for the last non-OK status returned on this thread ("" if none). */
 const char* mca_last_error(void);

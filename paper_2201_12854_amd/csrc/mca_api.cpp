@@ -158,7 +158,7 @@ mca_status run_stage(Profiler* pr, int stage, mca::FwdParams& p, F&& launch) {
 
 extern "C" {
 
-const char* mca_status_string(mca_status s) {
+const char* mca_status_string(int s) {
   switch (s) {
     case MCA_OK: return "MCA_OK";
     case MCA_ERR_INVALID_ARGUMENT: return "MCA_ERR_INVALID_ARGUMENT";
