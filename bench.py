@@ -99,9 +99,10 @@ def qk_flops(L):
 def stage_work(L, r, idx):
     """Algorithmic bytes and flops of every stage for one forward pass.
 
-    Score pass: one Q K^T (its second sweep, which recomputes the scores once the row
-    normalisers are known, is reported as executed work, not algorithmic). Output pass:
-    Q K^T and A H~. Sampled tokens: s_x d_in + r_j d_out s_W bytes and 2 r_j d_out flops
+    Score pass: Q K^T once per sweep over the keys (the streaming pass for rows longer than
+    8 key tiles sweeps twice, recomputing the scores once the row normalisers are known;
+    the work figure counts every sweep, as the measurement plan counts recomputed passes;
+    one_sweep_flops is the single Q K^T). Output pass: Q K^T and A H~. Sampled tokens: s_x d_in + r_j d_out s_W bytes and 2 r_j d_out flops
     (every draw counted; merged duplicates are reported beside it); saturated tokens:
     2 d_in d_out MFMA flops."""
     B, n, d_in, d_out, H = L.batch, L.seq, L.d_in, L.d_out, L.heads
@@ -122,7 +123,7 @@ def stage_work(L, r, idx):
     streaming = (n + 63) // 64 > 8
     w = {}
     w["scores_colmax"] = dict(bytes=2.0 * B * n * d_out * elem + 4.0 * B * H * n + 4.0 * B * n * nparts,
-                              flops=qk, executed_flops=(2 if streaming else 1) * qk)
+                              flops=(2 if streaming else 1) * qk, one_sweep_flops=qk)
     w["sample"] = dict(bytes=4.0 * B * n * nparts + n_valid * d_in * elem + 4.0 * d_in + 4.0 * B * n
                        + 8.0 * distinct + n_zero * d_out * elem, flops=0.0)
     gather_bytes = 8.0 * distinct + distinct * d_out * elem + n_sampled * d_out * elem
@@ -133,7 +134,7 @@ def stage_work(L, r, idx):
                        bytes_every_draw=8.0 * distinct + draws * d_out * elem + n_sampled * d_out * elem + sat_bytes,
                        mfma_flops=2.0 * n_sat * d_in * d_out)
     w["attn_out"] = dict(bytes=2.0 * B * n * d_out * elem + B * n * d_out * elem + 4.0 * B * n * d_out
-                         + 4.0 * B * H * n, flops=2 * qk, executed_flops=2 * qk)
+                         + 4.0 * B * H * n, flops=2 * qk)
     w["saturated"] = dict(bytes=sat_bytes, flops=2.0 * n_sat * d_in * d_out)
     stats = dict(sampled_tokens=n_sampled, saturated_tokens=n_sat, draws=draws, distinct_rows=distinct)
     return w, stats
@@ -278,10 +279,12 @@ def roofline(L, stage_us, work, workload):
         ach = work[dom]["flops"] / dur / 1e12
         roof = {"kernel": kname, "bound": "mfma", "achieved": ach, "peak": peak, "unit": "TFLOP/s",
                 "frac": ach / peak}
-        if "executed_flops" in work[dom]:
-            roof["executed_TFLOPs"] = work[dom]["executed_flops"] / dur / 1e12
-            roof["work"] = ("one Q K^T per launch (the second sweep recomputes the scores: executed_TFLOPs)"
-                            if dom == "scores_colmax" else "Q K^T and A H~ per launch")
+        if dom == "scores_colmax":
+            sweeps = int(round(work[dom]["flops"] / work[dom]["one_sweep_flops"]))
+            roof["work"] = (f"Q K^T once per sweep, {sweeps} sweep(s) per launch (2 x 64 x H x sum len^2 flops each)")
+            roof["one_sweep_TFLOPs"] = work[dom]["one_sweep_flops"] / dur / 1e12
+        else:
+            roof["work"] = "Q K^T and A H~ per launch"
     tr = measured_traffic(kname, workload, STAGE_SOURCE[dom])
     roof["traffic"] = tr["bytes"] if tr else None
     if tr:
@@ -303,7 +306,7 @@ def run_config(mca, L, dev, alpha, seed, steps, warmup, *, dense=True):
     r = plan.r.cpu().numpy()
     res = {"workload": L.name, "batch": L.batch, "seq_len": L.seq, "hidden": L.d_in, "heads": L.heads,
            "dtype": L.dtype, "tokens": L.tokens, "ms_per_step": ms, "tokens_per_s": L.tokens / (ms * 1e-3),
-           "stage_us": st, "flop_reduction": flop_reduction(L, r)}
+           "stage_us": st, "flop_reduction": flop_reduction(L, r), "dense_stage_rates": dense_stage_rates(L, st, r)}
     if dense:
         d = dense_baseline(t, L, steps, warmup)
         res["dense_exact"] = d
@@ -345,16 +348,24 @@ def c2_extras(mca, L, t, prep, alpha, seed, steps, warmup):
     return out
 
 
-def dense_stage_rates(L, st):
-    """MFMA rates of the dense stages: the score pass (one Q K^T), the output pass (Q K^T and
-    A H~) and the separate saturated-encoding kernel, against the dtype's dense peak."""
+def dense_stage_rates(L, st, r=None):
+    """MFMA rates of the dense stages against the dtype's dense peak: the score pass (Q K^T
+    per sweep: two sweeps beyond 8 key tiles; `one_sweep` counts one), the output pass (Q K^T
+    and A H~) and, when it runs, the separate saturated-encoding kernel (2 d_in d_out per
+    saturated token)."""
     peak = MFMA_PEAK_TFLOPS[L.dtype]
     qk = qk_flops(L)
+    sweeps = 2 if (L.seq + 63) // 64 > 8 else 1
     out = {}
-    for stage, flops in (("scores_colmax", qk), ("attn_out", 2 * qk)):
+    for stage, flops in (("scores_colmax", sweeps * qk), ("attn_out", 2 * qk)):
         if st.get(stage):
             tf = flops / (st[stage] * 1e-6) / 1e12
             out[stage] = {"TFLOP/s": tf, "mfma_frac": tf / peak}
+    if st.get("scores_colmax"):
+        out["scores_colmax"]["one_sweep_mfma_frac"] = qk / (st["scores_colmax"] * 1e-6) / 1e12 / peak
+    if st.get("saturated") and r is not None:
+        tf = 2.0 * float((r == L.d_in).sum()) * L.d_in * L.d_out / (st["saturated"] * 1e-6) / 1e12
+        out["saturated"] = {"TFLOP/s": tf, "mfma_frac": tf / peak}
     return out
 
 
@@ -572,7 +583,7 @@ def main():
               "config": {"workload": L.name, "batch": L.batch, "seq_len": L.seq, "hidden": L.d_in,
                          "heads": L.heads, "d_head": 64, "alpha": args.alpha, "seed": args.seed},
               "roofline": roof, "stages": stages, "dense_exact": head["dense_exact"],
-              "speedup_vs_dense": head["speedup_vs_dense"], "dense_stage_rates": dense_stage_rates(L, st),
+              "speedup_vs_dense": head["speedup_vs_dense"], "dense_stage_rates": head["dense_stage_rates"],
               "prepare_us": prep_ms * 1e3, "flop_reduction": {**head["flop_reduction"], **wstats}}
     del plan, t, prep
     torch.cuda.empty_cache()
@@ -582,7 +593,6 @@ def main():
         for name in OTHER_CONFIGS:
             Lc = wl.WORKLOADS[name]()
             res, tc, pc, _ = run_config(mca, Lc, dev, args.alpha, args.seed, args.steps, args.warmup)
-            res["dense_stage_rates"] = dense_stage_rates(Lc, res["stage_us"])
             log(f"{Lc.name}: {res['ms_per_step'] * 1e3:.1f} us/step, dense {res['dense_exact']['ms'] * 1e3:.1f} us "
                 f"({res['speedup_vs_dense']:.2f}x), stages "
                 + ", ".join(f"{k}={v:.1f}" for k, v in res["stage_us"].items()))

@@ -191,26 +191,6 @@ __device__ __forceinline__ float vmax3(float a, float b, float c) {
   return r;
 }
 
-// Combination with lane ^ 16 and lane ^ 32 (the four 16-lane rows hold one query's partial
-// results for different keys) by the gfx950 lane swaps: swapping a value with itself gives
-// each lane the pair {own, partner}, in some order, in registers.
-__device__ __forceinline__ float pair16_max(float v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair32_max(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return vmax(__uint_as_float(r[0]), __uint_as_float(r[1]));
-}
-__device__ __forceinline__ float pair16_sum(float v) {
-  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-__device__ __forceinline__ float pair32_sum(float v) {
-  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
-}
-
 __device__ __forceinline__ int valid_len(const FwdParams& p, int b) {
   int len = p.seq_lens ? p.seq_lens[b] : p.n;
   return min(max(len, 1), p.n);
@@ -466,29 +446,51 @@ __device__ __forceinline__ void row_stat_step(float& M, float& L) {
 }
 
 // Column statistic of one tile, t = dot a log2(e) - cc[i]: the max of t over the lane's four
-// queries, then over the four lane rows (max rule; the block's partial is exp2 of the max),
-// or the sum of exp2(t) = A (mean rule); lane row 0 leaves the wave's value of key
-// 16 s + r16 in cmw[16 s + r16].
-__device__ __forceinline__ void tile_colmax(const f32x4_t acc[4], const float cc[4], float* cmw, const BlockCtx& c,
-                                            bool sum) {
+// queries (max rule) or the sum of exp2(t) = A (mean rule), per key 16 s + r16, left in
+// cml[g][r16][s] (the wave's slot of the tile) for the combination over the four lane rows
+// and the four waves (col_combine).
+template <int IMP>
+__device__ __forceinline__ void tile_colstat(const f32x4_t acc[4], const float cc[4], float (*cml)[16][4],
+                                             const BlockCtx& c) {
   float v[4];
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    if (sum) {
+    if constexpr (IMP == 1) {
       float t = 0.f;
 #pragma unroll
       for (int i = 0; i < 4; ++i) t += exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]));
-      v[s] = pair32_sum(pair16_sum(t));
+      v[s] = t;
     } else {
       float t[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) t[i] = __fmaf_rn(acc[s][i], kLog2eOver8, -cc[i]);
-      v[s] = pair32_max(pair16_max(vmax(vmax3(t[0], t[1], t[2]), t[3])));
+      v[s] = vmax(vmax3(t[0], t[1], t[2]), t[3]);
     }
   }
-  if (c.g == 0) {
+  *reinterpret_cast<float4*>(&cml[c.g][c.r16][0]) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
+// The block's partial of key e (< 64) of a tile from its sixteen values (four waves x four
+// lane rows) in a fixed order: exp2 of the max (max rule; SCALED: the values are dot - c / s
+// and the max is multiplied by s first) or the sum (mean rule).
+template <int IMP, bool SCALED = false>
+__device__ __forceinline__ float col_combine(const float (*cmt)[4][16][4], int e) {
+  const int r16 = e & 15, sk = e >> 4;
+  float x[16];
 #pragma unroll
-    for (int s = 0; s < 4; ++s) cmw[16 * s + c.r16] = v[s];
+  for (int w = 0; w < 4; ++w)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) x[4 * w + g] = cmt[w][g][r16][sk];
+  if constexpr (IMP == 1) {
+    float a[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) a[w] = (x[4 * w] + x[4 * w + 1]) + (x[4 * w + 2] + x[4 * w + 3]);
+    return (a[0] + a[1]) + (a[2] + a[3]);
+  } else {
+    const float a = vmax3(x[0], x[1], x[2]), b = vmax3(x[3], x[4], x[5]), d = vmax3(x[6], x[7], x[8]);
+    const float f = vmax3(x[9], x[10], x[11]), g = vmax3(x[12], x[13], x[14]);
+    const float m = vmax3(vmax3(a, b, d), vmax3(f, g, x[15]), a);
+    return exp2_fast(SCALED ? __fmul_rn(m, kLog2eOver8) : m);
   }
 }
 
@@ -519,12 +521,12 @@ __device__ __forceinline__ void store_row_c(const FwdParams& p, const BlockCtx& 
 }
 
 // Resident variant: all ntl <= NT tiles in LDS and all scores in registers.
-template <int BF, int NT, bool BAND>
+template <int BF, int NT, bool BAND, int IMP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) void k_scores_res(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[NT][kTile * S];
-  __shared__ float cm[NT][4][kTile];
+  __shared__ __align__(16) float cm[NT][4][4][16][4];  // [tile][wave][lane row][r16][s]
   const BlockCtx c = block_ctx(p);
   const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
@@ -584,20 +586,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 
   // column max (or, mean rule, column sum) of the block's valid queries, every tile in its
   // own LDS slot (one barrier); median rule: every probability to acol as well
-  const bool sum = p.importance == 1;
 #pragma unroll
   for (int kt = 0; kt < NT; ++kt) {
     if (kt < c.ntl) {
-      tile_colmax(acc[kt], cc, cm[kt][c.wave], c, sum);
-      if (p.acol) store_probs(p, c, acc[kt], kt, cq, c.qt * kTile + c.wave * 16 + 4 * c.g);
+      tile_colstat<IMP>(acc[kt], cc, cm[kt][c.wave], c);
+      if constexpr (IMP == 2) store_probs(p, c, acc[kt], kt, cq, c.qt * kTile + c.wave * 16 + 4 * c.g);
     }
   }
   lds_barrier();
   float* part = p.colmax_part + (int64_t)c.b * c.n * p.nparts + c.h * p.qtiles + c.qt;
   for (int e = c.tid; e < c.ntl * kTile; e += kThreads) {
-    const int kt = e / kTile, k = e % kTile;
-    const float v = sum ? (cm[kt][0][k] + cm[kt][1][k]) + (cm[kt][2][k] + cm[kt][3][k])
-                        : exp2_fast(vmax(vmax3(cm[kt][0][k], cm[kt][1][k], cm[kt][2][k]), cm[kt][3][k]));
+    const float v = col_combine<IMP>(cm[e / kTile], e % kTile);
     if (e < c.n) part[(int64_t)e * p.nparts] = v;
   }
 }
@@ -606,12 +605,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(3))) v
 // streamed through two LDS buffers as in the streaming variant, but every score stays in
 // registers, so a single sweep over K gives the statistics and the column statistic (the
 // streaming variant computes every score twice and keeps online statistics).
-template <int BF, int NT, bool BAND>
+template <int BF, int NT, bool BAND, int IMP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_scores_rs(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[2][kTile * S];
-  __shared__ float cm[NT][4][kTile];
+  __shared__ __align__(16) float cm[NT][4][4][16][4];  // [tile][wave][lane row][r16][s]
   const BlockCtx c = block_ctx(p);
   const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
@@ -672,19 +671,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       if (kt < c.tlo || kt > c.thi) part[(int64_t)key * p.nparts] = 0.f;
     }
   }
-  const bool sum = p.importance == 1;
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     if (t < nvis) {
-      tile_colmax(acc[t], cc, cm[t][c.wave], c, sum);
-      if (p.acol) store_probs(p, c, acc[t], tile_at(c, t), cq, c.qt * kTile + c.wave * 16 + 4 * c.g);
+      tile_colstat<IMP>(acc[t], cc, cm[t][c.wave], c);
+      if constexpr (IMP == 2) store_probs(p, c, acc[t], tile_at(c, t), cq, c.qt * kTile + c.wave * 16 + 4 * c.g);
     }
   }
   lds_barrier();
   for (int e = c.tid; e < nvis * kTile; e += kThreads) {
     const int t = e / kTile, k = e % kTile;
-    const float v = sum ? (cm[t][0][k] + cm[t][1][k]) + (cm[t][2][k] + cm[t][3][k])
-                        : exp2_fast(vmax(vmax3(cm[t][0][k], cm[t][1][k], cm[t][2][k]), cm[t][3][k]));
+    const float v = col_combine<IMP>(cm[t], k);
     const int key = tile_at(c, t) * kTile + k;
     if (key < c.n) part[(int64_t)key * p.nparts] = v;
   }
@@ -1181,24 +1178,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   constexpr bool sum = IMP == 1;
   auto combine = [&](int t) {  // the block's partial of tile t's keys
     if (c.tid < kTile) {
-      const int e = c.tid, r16 = e & 15, sk = e >> 4;  // key 16 sk + r16 of the tile
-      float x[16];
-#pragma unroll
-      for (int w = 0; w < 4; ++w)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) x[4 * w + g] = cm[t % 3][w][g][r16][sk];
-      float r;
-      if constexpr (sum) {
-        float a[4];
-#pragma unroll
-        for (int w = 0; w < 4; ++w) a[w] = (x[4 * w] + x[4 * w + 1]) + (x[4 * w + 2] + x[4 * w + 3]);
-        r = (a[0] + a[1]) + (a[2] + a[3]);
-      } else {
-        const float a = vmax3(x[0], x[1], x[2]), b = vmax3(x[3], x[4], x[5]), c2 = vmax3(x[6], x[7], x[8]);
-        const float d = vmax3(x[9], x[10], x[11]), f = vmax3(x[12], x[13], x[14]);
-        r = exp2_fast(__fmul_rn(vmax3(vmax3(a, b, c2), vmax3(d, f, x[15]), a), kLog2eOver8));
-      }
-      const int key = tile_at(c, t) * kTile + e;
+      const float r = col_combine<IMP == 1 ? 1 : 0, true>(cm[t % 3], c.tid);
+      const int key = tile_at(c, t) * kTile + c.tid;
       if (key < c.n) part[(int64_t)key * p.nparts] = r;
     }
   };
@@ -1255,21 +1236,38 @@ hipError_t launch_scores_stream(const FwdParams& p, hipStream_t s) {
   }
 }
 
-// Resident variants for padded lengths up to 256 keys (bf16) or 128 keys (fp32).
+// The one-sweep score passes with the importance rule as a template parameter (the mean and
+// median rules are defined for full attention only).
+template <int BF, int NT, bool BAND, bool RS>
+hipError_t launch_scores_onesweep(const FwdParams& p, hipStream_t s) {
+  const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
+  if (!BAND && p.importance == 1) {
+    if constexpr (RS) return launch_stage_kernel(k_scores_rs<BF, NT, BAND, 1>, grid, blk, 0, s, p);
+    else return launch_stage_kernel(k_scores_res<BF, NT, BAND, 1>, grid, blk, 0, s, p);
+  }
+  if (!BAND && p.importance == 2) {
+    if constexpr (RS) return launch_stage_kernel(k_scores_rs<BF, NT, BAND, 2>, grid, blk, 0, s, p);
+    else return launch_stage_kernel(k_scores_res<BF, NT, BAND, 2>, grid, blk, 0, s, p);
+  }
+  if constexpr (RS) return launch_stage_kernel(k_scores_rs<BF, NT, BAND, 0>, grid, blk, 0, s, p);
+  else return launch_stage_kernel(k_scores_res<BF, NT, BAND, 0>, grid, blk, 0, s, p);
+}
+
+// Resident variants for padded lengths up to 256 keys (bf16) or 128 keys (fp32), the
+// one-sweep streamed variant up to 8 key tiles, the two-sweep streaming variant beyond.
 template <bool BAND>
 hipError_t launch_scores_band(const FwdParams& p, hipStream_t s) {
-  const dim3 grid((unsigned)(p.qtiles * p.H * p.B)), blk(kThreads);
   const int nt = (p.n + kTile - 1) / kTile;
   if (p.bf16) {
-    if (nt <= 1) return launch_stage_kernel((k_scores_res<1, 1, BAND>), grid, blk, 0, s, p);
-    else if (nt <= 2) return launch_stage_kernel((k_scores_res<1, 2, BAND>), grid, blk, 0, s, p);
-    else if (nt <= 4) return launch_stage_kernel((k_scores_res<1, 4, BAND>), grid, blk, 0, s, p);
-    else if (nt <= 8) return launch_stage_kernel((k_scores_rs<1, 8, BAND>), grid, blk, 0, s, p);
+    if (nt <= 1) return launch_scores_onesweep<1, 1, BAND, false>(p, s);
+    else if (nt <= 2) return launch_scores_onesweep<1, 2, BAND, false>(p, s);
+    else if (nt <= 4) return launch_scores_onesweep<1, 4, BAND, false>(p, s);
+    else if (nt <= 8) return launch_scores_onesweep<1, 8, BAND, true>(p, s);
     else return launch_scores_stream<1, BAND>(p, s);
   } else {
-    if (nt <= 1) return launch_stage_kernel((k_scores_res<0, 1, BAND>), grid, blk, 0, s, p);
-    else if (nt <= 2) return launch_stage_kernel((k_scores_res<0, 2, BAND>), grid, blk, 0, s, p);
-    else if (nt <= 8) return launch_stage_kernel((k_scores_rs<0, 8, BAND>), grid, blk, 0, s, p);
+    if (nt <= 1) return launch_scores_onesweep<0, 1, BAND, false>(p, s);
+    else if (nt <= 2) return launch_scores_onesweep<0, 2, BAND, false>(p, s);
+    else if (nt <= 8) return launch_scores_onesweep<0, 8, BAND, true>(p, s);
     else return launch_scores_stream<0, BAND>(p, s);
   }
 }
