@@ -129,6 +129,23 @@ __device__ uint32_t column_select(const ColumnValues& cv, uint32_t k, uint32_t* 
   return prefix;
 }
 
+// The same selection for values held in registers (cached), without LDS: the rank-k value
+// is the largest bit pattern v with #{x < v} <= k, built bit by bit from the top (the sign
+// bit of non-negative floats is 0); each step counts the values below the candidate with one
+// compare and one wave ballot per register. Register slots past N hold 0xffffffff, which no
+// candidate exceeds.
+__device__ uint32_t column_select_regs(const ColumnValues& cv, uint32_t k) {
+  uint32_t prefix = 0u;
+  for (int bit = 30; bit >= 0; --bit) {
+    const uint32_t cand = prefix | (1u << bit);
+    uint32_t below = 0u;
+#pragma unroll
+    for (int u = 0; u < kSelRegs; ++u) below += (uint32_t)__popcll(__ballot(__float_as_uint(cv.reg[u]) < cand));
+    if (below <= k) prefix = cand;
+  }
+  return prefix;
+}
+
 __device__ float column_median(const float* v, int H, int n, int len, uint32_t* hist, int lane) {
   ColumnValues cv;
   cv.v = v;
@@ -140,11 +157,11 @@ __device__ float column_median(const float* v, int H, int n, int len, uint32_t* 
 #pragma unroll
     for (int u = 0; u < kSelRegs; ++u) {
       const int idx = u * kWave + lane, h = idx / len;
-      cv.reg[u] = idx < cv.N ? v[(int64_t)h * n + idx - h * len] : 0.f;
+      cv.reg[u] = idx < cv.N ? v[(int64_t)h * n + idx - h * len] : __uint_as_float(0xffffffffu);
     }
   }
   const uint32_t N = (uint32_t)cv.N;
-  const uint32_t lo = column_select(cv, (N - 1) / 2, hist, lane);
+  const uint32_t lo = cv.cached ? column_select_regs(cv, (N - 1) / 2) : column_select(cv, (N - 1) / 2, hist, lane);
   if (N % 2) return __uint_as_float(lo);
   // rank N / 2: lo again if more than N / 2 values are <= lo, else the smallest value above
   uint32_t le = 0u, above = 0xffffffffu;

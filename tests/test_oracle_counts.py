@@ -74,3 +74,12 @@ def test_huge_alpha_gives_one_sample():
     L = wl.make_layer(1, 16, 64, 1, "f32", data_seed=23)
     m = oracle.column_max(L.Q, L.K, L.lens, 1)
     assert np.all(oracle.sample_counts(m, L.lens, 1e12, L.d_in) == 1)
+
+
+def test_non_finite_column_max_saturates():
+    # Eq. 9 with an infinite or undefined m (non-finite scores) asks for unboundedly many
+    # samples: the count is capped at d_in (an exactly encoded token), never left at the
+    # floor of 1; a zero m gives the floor
+    m = np.array([[np.inf, np.nan, 0.0, 1e-300, 1e300]])
+    r = oracle.sample_counts(m, np.array([5]), 0.4, 64)
+    assert r.tolist() == [[64, 64, 1, 1, 64]]
