@@ -71,34 +71,31 @@ __device__ __forceinline__ float wave_sum(float v) {
 
 // Median of the N = H len values v[h n + i], h < H, i < len (all non-negative floats, so
 // their bit patterns order like the values): the value of rank (N - 1) / 2 (counting from
-// 0) by a radix select over 8-bit digits, most significant first (each pass counts the
-// values that match the digits found so far in a 256-bin histogram in the wave's LDS
-// region; the bin holding the rank gives the next digit), then, for even N, the next value
-// up from one more pass (the count of values <= it and the smallest value above it). Up to
-// 2048 values are kept in registers (32 per lane); longer columns are read again per pass.
+// 0), then, for even N, the mean with the next value up (the count of values <= it and the
+// smallest value above it). Up to 2048 values are held in registers (32 per lane) and the
+// rank is selected there; longer columns are selected by a radix select over 8-bit digits
+// that reads the column again per pass.
 constexpr int kSelRegs = 32;
 
-struct ColumnValues {
-  const float* v;
-  int n, len, N;
-  float reg[kSelRegs];
-  bool cached;
-  __device__ __forceinline__ uint32_t at(int u, int lane) const {  // value u * 64 + lane (< N)
-    if (cached) return __float_as_uint(reg[u]);
-    const int idx = u * kWave + lane, h = idx / len;
-    return __float_as_uint(v[(int64_t)h * n + idx - h * len]);
-  }
-};
+// Value u * 64 + lane of the column (u * 64 + lane < N), read from memory.
+__device__ __forceinline__ uint32_t column_at(const float* v, int n, int len, int u, int lane) {
+  const int idx = u * kWave + lane, h = idx / len;
+  return __float_as_uint(v[(int64_t)h * n + idx - h * len]);
+}
 
-__device__ uint32_t column_select(const ColumnValues& cv, uint32_t k, uint32_t* hist, int lane) {
-  const int rounds = (cv.N + kWave - 1) / kWave;
+// Radix select from memory: each pass counts the values that match the digits found so far
+// in a 256-bin histogram in the wave's LDS region; the bin holding the rank gives the next
+// digit, most significant first.
+__device__ __forceinline__ uint32_t column_select(const float* v, int n, int len, int N, uint32_t k, uint32_t* hist,
+                                                  int lane) {
+  const int rounds = (N + kWave - 1) / kWave;
   uint32_t prefix = 0u, pmask = 0u;
   for (int shift = 24; shift >= 0; shift -= 8) {
     for (int bb = lane; bb < 256; bb += kWave) hist[bb] = 0u;
     wave_lds_sync();
     for (int u = 0; u < rounds; ++u) {
-      if (u * kWave + lane < cv.N) {
-        const uint32_t x = cv.at(u, lane);
+      if (u * kWave + lane < N) {
+        const uint32_t x = column_at(v, n, len, u, lane);
         if ((x & pmask) == prefix) atomicAdd(hist + ((x >> shift) & 255u), 1u);
       }
     }
@@ -129,56 +126,97 @@ __device__ uint32_t column_select(const ColumnValues& cv, uint32_t k, uint32_t* 
   return prefix;
 }
 
-// The same selection for values held in registers (cached), without LDS: the rank-k value
-// is the largest bit pattern v with #{x < v} <= k, built bit by bit from the top (the sign
-// bit of non-negative floats is 0); each step counts the values below the candidate with one
-// compare and one wave ballot per register. Register slots past N hold 0xffffffff, which no
-// candidate exceeds.
-__device__ uint32_t column_select_regs(const ColumnValues& cv, uint32_t k) {
+// The same selection for values held in registers: the rank-k value is the largest bit
+// pattern v with #{x < v} <= k, built bit by bit from the top (the sign bit of non-negative
+// floats is 0); each step counts the values below the candidate with one compare and one
+// wave ballot per register. Register slots past N hold 0xffffffff, which no candidate
+// exceeds.
+// R: the registers that hold values (the first R of reg; N <= 64 R).
+template <int R>
+__device__ __forceinline__ uint32_t column_select_regs(const uint32_t (&reg)[kSelRegs], uint32_t k) {
   uint32_t prefix = 0u;
   for (int bit = 30; bit >= 0; --bit) {
     const uint32_t cand = prefix | (1u << bit);
     uint32_t below = 0u;
 #pragma unroll
-    for (int u = 0; u < kSelRegs; ++u) below += (uint32_t)__popcll(__ballot(__float_as_uint(cv.reg[u]) < cand));
+    for (int u = 0; u < R; ++u) below += (uint32_t)__popcll(__ballot(reg[u] < cand));
     if (below <= k) prefix = cand;
   }
   return prefix;
 }
 
-__device__ float column_median(const float* v, int H, int n, int len, uint32_t* hist, int lane) {
-  ColumnValues cv;
-  cv.v = v;
-  cv.n = n;
-  cv.len = len;
-  cv.N = H * len;
-  cv.cached = cv.N <= kSelRegs * kWave;
-  if (cv.cached) {
+__device__ __forceinline__ float column_median(const float* v, int H, int n, int len, uint32_t* hist, int lane) {
+  const int N = H * len;
+  const bool cached = N <= kSelRegs * kWave;
+  uint32_t reg[kSelRegs];
+  uint32_t lo;
+  if (cached) {
+    // value u * 64 + lane is v[h n + i] with h = (u * 64 + lane) / len, stepped without a
+    // division per value
+    int h = lane / len, i = lane - h * len;
+    const int dh = kWave / len, di = kWave - dh * len;  // 64 = dh len + di
 #pragma unroll
     for (int u = 0; u < kSelRegs; ++u) {
-      const int idx = u * kWave + lane, h = idx / len;
-      cv.reg[u] = idx < cv.N ? v[(int64_t)h * n + idx - h * len] : __uint_as_float(0xffffffffu);
+      reg[u] = u * kWave + lane < N ? __float_as_uint(v[(int64_t)h * n + i]) : 0xffffffffu;
+      h += dh;
+      i += di;
+      if (i >= len) {
+        i -= len;
+        ++h;
+      }
     }
+    const uint32_t k = (uint32_t)(N - 1) / 2;
+    if (N <= 8 * kWave) lo = column_select_regs<8>(reg, k);
+    else if (N <= 16 * kWave) lo = column_select_regs<16>(reg, k);
+    else if (N <= 24 * kWave) lo = column_select_regs<24>(reg, k);
+    else lo = column_select_regs<32>(reg, k);
+  } else {
+    lo = column_select(v, n, len, N, (uint32_t)(N - 1) / 2, hist, lane);
   }
-  const uint32_t N = (uint32_t)cv.N;
-  const uint32_t lo = cv.cached ? column_select_regs(cv, (N - 1) / 2) : column_select(cv, (N - 1) / 2, hist, lane);
   if (N % 2) return __uint_as_float(lo);
   // rank N / 2: lo again if more than N / 2 values are <= lo, else the smallest value above
+  // (a register slot past N, 0xffffffff, is above every lo and counts for neither)
   uint32_t le = 0u, above = 0xffffffffu;
-  const int rounds = (cv.N + kWave - 1) / kWave;
-  for (int u = 0; u < rounds; ++u) {
-    if (u * kWave + lane < cv.N) {
-      const uint32_t x = cv.at(u, lane);
-      le += x <= lo ? 1u : 0u;
-      if (x > lo) above = min(above, x);
+  if (cached) {
+#pragma unroll
+    for (int u = 0; u < kSelRegs; ++u) {
+      le += reg[u] <= lo ? 1u : 0u;
+      if (reg[u] > lo) above = min(above, reg[u]);
+    }
+  } else {
+    const int rounds = (N + kWave - 1) / kWave;
+    for (int u = 0; u < rounds; ++u) {
+      if (u * kWave + lane < N) {
+        const uint32_t x = column_at(v, n, len, u, lane);
+        le += x <= lo ? 1u : 0u;
+        if (x > lo) above = min(above, x);
+      }
     }
   }
   for (int o = 32; o >= 1; o >>= 1) {  // wave sums and minima
     le += (uint32_t)__shfl_xor((int)le, o);
     above = min(above, (uint32_t)__shfl_xor((int)above, o));
   }
-  const uint32_t hi = le > N / 2 ? lo : above;
+  const uint32_t hi = le > (uint32_t)N / 2 ? lo : above;
   return (float)(0.5 * ((double)__uint_as_float(lo) + (double)__uint_as_float(hi)));
+}
+
+// The median rule's column statistic, before the sampler: one wavefront per key j < len of
+// batch row b takes the median of its H len probabilities (written key-major by the score
+// pass) and leaves it in the key's first column-max partial slot, the only one the sampler
+// reads under this rule. Padded keys are skipped (the sampler gives them r = 0).
+constexpr int kMedWaves = 4;
+__global__ __launch_bounds__(64 * kMedWaves) void k_colmedian(FwdParams p) {
+  __shared__ __align__(16) uint32_t hist[kMedWaves][256];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t tok = (int64_t)blockIdx.x * kMedWaves + wave;
+  if (tok >= (int64_t)p.B * p.n) return;  // wave-uniform; no block barrier follows
+  const int b = (int)(tok / p.n), j = (int)(tok - (int64_t)b * p.n);
+  int len = p.seq_lens ? p.seq_lens[b] : p.n;
+  len = min(max(len, 1), p.n);
+  if (j >= len) return;
+  const float m = column_median(p.acol + tok * (int64_t)p.H * p.n, p.H, p.n, len, hist[wave], lane);
+  if (lane == 0) p.colmax_part[tok * p.nparts] = m;
 }
 
 // Per-wave results of phase 1, shared with the block for the pooled draws.
@@ -198,10 +236,8 @@ static_assert(sizeof(TokInfo) <= kHeader, "header");
 //          float32 [d_in].
 __host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
 __host__ __device__ inline int sample_shared_bytes(int d_in, bool table) { return table ? round16(8 * d_in) : 0; }
-// (at least 1 KB: the median rule's histogram uses the region before phase 1 fills it)
 __host__ __device__ inline int sample_region_bytes(int d_in, bool table) {
-  const int b = table ? 2 * round16(4 * d_in) : round16(8 * d_in) + round16(4 * d_in);
-  return b > 1024 ? b : 1024;
+  return table ? 2 * round16(4 * d_in) : round16(8 * d_in) + round16(4 * d_in);
 }
 __host__ __device__ inline int sample_lds_bytes(int d_in, bool table, int nw) {
   return kHeader + sample_shared_bytes(d_in, table) + nw * sample_region_bytes(d_in, table);
@@ -333,9 +369,19 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   len = min(max(len, 1), n);
   const int rin = p.r_in ? p.r_in[tk] : 0;
   const float* part = p.colmax_part + tk * p.nparts;
-  float m = 0.f;
   const bool mean_rule = p.importance == 1;
-  for (int t = lane; t < p.nparts; t += kWave) m = mean_rule ? m + part[t] : fmaxf(m, part[t]);
+  // the token's column-max partials (column sums under the mean rule): the first eight of
+  // each lane are loaded here, before x, so that all of phase 1's loads are in flight at
+  // once (slots past the end re-read the last partial and count as 0)
+  const bool median_rule = p.importance == 2;
+  const int nparts = median_rule ? 1 : p.nparts;  // the median rule: one value, from k_colmedian
+  float pv[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    const int t = lane + u * kWave;
+    const float v = part[min(t, nparts - 1)];
+    pv[u] = t < nparts ? v : 0.f;
+  }
   const int per = (d_in + kWave - 1) / kWave;
   const int i0 = min(lane * per, d_in);
   const int nrows = min(per, d_in - i0);
@@ -376,14 +422,29 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
       }
     }
   }
+  // per lane in ascending order; a slot past the end adds 0 or takes the max with 0 (every
+  // partial is >= 0), which leaves the result unchanged. Rows of more than 512 partials
+  // continue eight at a time.
+  float m = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) m = mean_rule ? m + pv[u] : fmaxf(m, pv[u]);
+  for (int t0 = lane + 8 * kWave; t0 < nparts; t0 += 8 * kWave) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int t = t0 + u * kWave;
+      const float v = part[min(t, nparts - 1)];
+      pv[u] = t < nparts ? v : 0.f;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) m = mean_rule ? m + pv[u] : fmaxf(m, pv[u]);
+  }
   if (mean_rule) {  // the partials are column sums: the mean over H len values
     m = (float)((double)wave_sum(m) / ((double)p.H * (double)len));
+  } else if (median_rule) {  // the key's median, as k_colmedian left it (a NaN stays NaN)
+    m = __shfl(pv[0], 0);
   } else {
     m = wave_max(m);
   }
-  if (p.importance == 2 && j < len)  // median of the H len probabilities of key j
-    m = column_median(p.acol + tk * (int64_t)p.H * n, p.H, n, len,
-                      reinterpret_cast<uint32_t*>(smem + region_off(d_in, TABLE, wave)), lane);
   if constexpr (TABLE) __syncthreads();  // the shared table is in LDS
 
   // 1a. sample count (Eq. 9)
@@ -615,7 +676,16 @@ hipError_t launch_bf(const FwdParams& p, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_sample(const FwdParams& p, hipStream_t s) {
-  return p.bf16 ? launch_bf<1>(p, s) : launch_bf<0>(p, s);
+  if (p.importance != 2) return p.bf16 ? launch_bf<1>(p, s) : launch_bf<0>(p, s);
+  // the median rule: k_colmedian, then the sampler; a profiler's event pair spans both
+  FwdParams p1 = p, p2 = p;
+  p1.ev_stop = nullptr;
+  p2.ev_start = nullptr;
+  const int64_t ntok = (int64_t)p.B * p.n;
+  const dim3 grid((unsigned)((ntok + kMedWaves - 1) / kMedWaves));
+  const hipError_t e = launch_stage_kernel(k_colmedian, grid, dim3(64 * kMedWaves), 0, s, p1);
+  if (e != hipSuccess) return e;
+  return p.bf16 ? launch_bf<1>(p2, s) : launch_bf<0>(p2, s);
 }
 
 }  // namespace mca

@@ -83,14 +83,15 @@ struct FwdParams {
   float* coef_out;
   float* enc_out;
   // profiling: when set, the stage's kernel is launched with these events, which the
-  // dispatch stamps at the kernel's start and end (kernel execution time only)
+  // dispatch stamps at the kernel's start and end (kernel execution time only); a stage of
+  // two kernels gives the start event to the first and the stop event to the second
   hipEvent_t ev_start, ev_stop;
 };
 
-// Launches a stage kernel (one per stage), with the profiling events when they are set.
+// Launches a stage kernel, with the profiling events that are set.
 template <typename K>
 inline hipError_t launch_stage_kernel(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const FwdParams& p) {
-  if (p.ev_start) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, p.ev_start, p.ev_stop, 0u, p);
+  if (p.ev_start || p.ev_stop) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, p.ev_start, p.ev_stop, 0u, p);
   else hipLaunchKernelGGL(kernel, grid, block, lds, s, p);
   return hipGetLastError();
 }
