@@ -494,6 +494,20 @@ __device__ __forceinline__ float col_combine(const float (*cmt)[4][16][4], int e
   }
 }
 
+// Four probabilities of queries q .. q + 3 (q a multiple of 4) of one key, at dst = the
+// key's row + q: one 16-byte store when all four queries exist and the row is 16-byte
+// aligned (n a multiple of 4), else one store per existing query.
+__device__ __forceinline__ void store_probs4(float* dst, float a0, float a1, float a2, float a3, int q, int n) {
+  if ((n & 3) == 0 && q + 3 < n) {
+    *reinterpret_cast<float4*>(dst) = make_float4(a0, a1, a2, a3);
+  } else {
+    if (q < n) dst[0] = a0;
+    if (q + 1 < n) dst[1] = a1;
+    if (q + 2 < n) dst[2] = a2;
+    if (q + 3 < n) dst[3] = a3;
+  }
+}
+
 // Median rule: the probabilities of one tile, A = exp2(dot a log2(e) - c), into the per-key
 // array acol[b n + key][h][query].
 __device__ __forceinline__ void store_probs(const FwdParams& p, const BlockCtx& c, const f32x4_t acc[4], int kt,
@@ -503,10 +517,10 @@ __device__ __forceinline__ void store_probs(const FwdParams& p, const BlockCtx& 
   for (int s = 0; s < 4; ++s) {
     const int key = kt * kTile + 16 * s + c.r16;
     if (key < c.n) {
+      float a[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (qw + i < c.n)
-          ac[((int64_t)key * p.H + c.h) * c.n + qw + i] = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq[i]));
+      for (int i = 0; i < 4; ++i) a[i] = exp2_fast(__fmaf_rn(acc[s][i], kLog2eOver8, -cq[i]));
+      store_probs4(ac + ((int64_t)key * p.H + c.h) * c.n + qw, a[0], a[1], a[2], a[3], qw, c.n);
     }
   }
 }
@@ -1210,11 +1224,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         for (int s = 0; s < 4; ++s) {
           const int key = kt * kTile + 16 * s + c.r16;
           if (key < c.n) {
+            const int q = qw + 16 * m + 4 * c.g;
+            float a[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-              const int q = qw + 16 * m + 4 * c.g + i;
-              if (q < c.n) ac[((int64_t)key * p.H + c.h) * c.n + q] = exp2_fast(__fmul_rn(acc[m][s][i], kLog2eOver8));
-            }
+            for (int i = 0; i < 4; ++i) a[i] = exp2_fast(__fmul_rn(acc[m][s][i], kLog2eOver8));
+            store_probs4(ac + ((int64_t)key * p.H + c.h) * c.n + q, a[0], a[1], a[2], a[3], q, c.n);
           }
         }
     }

@@ -129,13 +129,12 @@ __device__ __forceinline__ uint32_t column_select(const float* v, int n, int len
 // The same selection for values held in registers: the rank-k value is the largest bit
 // pattern v with #{x < v} <= k, built bit by bit from the top (the sign bit of non-negative
 // floats is 0); each step counts the values below the candidate with one compare and one
-// wave ballot per register. Register slots past N hold 0xffffffff, which no candidate
-// exceeds.
-// R: the registers that hold values (the first R of reg; N <= 64 R).
+// wave ballot per register. Register slots past the values hold 0xffffffff, which no
+// candidate exceeds. Bits hi .. lo are decided here, the ones above come in as prefix.
 template <int R>
-__device__ __forceinline__ uint32_t column_select_regs(const uint32_t (&reg)[kSelRegs], uint32_t k) {
-  uint32_t prefix = 0u;
-  for (int bit = 30; bit >= 0; --bit) {
+__device__ __forceinline__ uint32_t select_bits(const uint32_t (&reg)[kSelRegs], uint32_t k, uint32_t prefix, int hi,
+                                                int lo) {
+  for (int bit = hi; bit >= lo; --bit) {
     const uint32_t cand = prefix | (1u << bit);
     uint32_t below = 0u;
 #pragma unroll
@@ -143,6 +142,44 @@ __device__ __forceinline__ uint32_t column_select_regs(const uint32_t (&reg)[kSe
     if (below <= k) prefix = cand;
   }
   return prefix;
+}
+
+// Rank-k selection of the values in the first R registers: the top 12 bits (bits 30 .. 19)
+// over every value, then, when at most 256 values share those bits with the result, the
+// rest over those values only, moved into at most four registers through the wave's LDS
+// region buf (256 words): a value with smaller top bits is below every remaining candidate
+// and a value with larger ones below none, so the rank among the shared values is k minus
+// the count of smaller ones.
+constexpr int kTopShift = 19;
+template <int R>
+__device__ __forceinline__ uint32_t column_select_regs(const uint32_t (&reg)[kSelRegs], uint32_t k, uint32_t* buf,
+                                                      int lane) {
+  const uint32_t prefix = select_bits<R>(reg, k, 0u, 30, kTopShift);
+  const uint32_t top = prefix >> kTopShift;
+  uint32_t smaller = 0u, same = 0u, mine = 0u;
+#pragma unroll
+  for (int u = 0; u < R; ++u) {
+    const uint32_t t = reg[u] >> kTopShift;  // padding: 0x1fff, above every top
+    smaller += (uint32_t)__popcll(__ballot(t < top));
+    const bool eq = t == top;
+    same += (uint32_t)__popcll(__ballot(eq));
+    mine += eq ? 1u : 0u;
+  }
+  if (same > 256u) return select_bits<R>(reg, k, prefix, kTopShift - 1, 0);
+  const uint32_t incl = wave_inclusive_scan<uint32_t>(mine);
+  uint32_t at = incl - mine;
+#pragma unroll
+  for (int u = 0; u < R; ++u)
+    if ((reg[u] >> kTopShift) == top) buf[at++] = reg[u];
+  wave_lds_sync();
+  uint32_t r2[kSelRegs];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) r2[u] = (uint32_t)(u * kWave + lane) < same ? buf[u * kWave + lane] : 0xffffffffu;
+  wave_lds_sync();  // every lane has read buf before a later use of the region
+  const uint32_t k2 = k - smaller;
+  if (same <= 64u) return select_bits<1>(r2, k2, prefix, kTopShift - 1, 0);
+  if (same <= 128u) return select_bits<2>(r2, k2, prefix, kTopShift - 1, 0);
+  return select_bits<4>(r2, k2, prefix, kTopShift - 1, 0);
 }
 
 __device__ __forceinline__ float column_median(const float* v, int H, int n, int len, uint32_t* hist, int lane) {
@@ -166,10 +203,10 @@ __device__ __forceinline__ float column_median(const float* v, int H, int n, int
       }
     }
     const uint32_t k = (uint32_t)(N - 1) / 2;
-    if (N <= 8 * kWave) lo = column_select_regs<8>(reg, k);
-    else if (N <= 16 * kWave) lo = column_select_regs<16>(reg, k);
-    else if (N <= 24 * kWave) lo = column_select_regs<24>(reg, k);
-    else lo = column_select_regs<32>(reg, k);
+    if (N <= 8 * kWave) lo = column_select_regs<8>(reg, k, hist, lane);
+    else if (N <= 16 * kWave) lo = column_select_regs<16>(reg, k, hist, lane);
+    else if (N <= 24 * kWave) lo = column_select_regs<24>(reg, k, hist, lane);
+    else lo = column_select_regs<32>(reg, k, hist, lane);
   } else {
     lo = column_select(v, n, len, N, (uint32_t)(N - 1) / 2, hist, lane);
   }

@@ -479,6 +479,58 @@ def test_importance_rules_single_token_row_and_eq6(dev, rule):
     _full_check(L, dev, 0.1, seed=2, importance=rule, sampling="weight")
 
 
+def _median_of(vals):
+    """Median of float32 values as the median rule defines it: the middle value, or for an
+    even count the mean of the two middle values taken in float64 and rounded once."""
+    v = np.sort(vals.astype(np.float32))
+    N = v.size
+    lo, hi = v[(N - 1) // 2], v[N // 2]
+    return np.float32(0.5 * (np.float64(lo) + np.float64(hi)))
+
+
+@pytest.mark.parametrize("case", ["bert_base", "uniform", "small", "long"])
+def test_median_selection_exact(dev, case):
+    # the per-key median must be exactly the median of the probabilities the score pass
+    # wrote (read back from the workspace), whichever selection path the column takes:
+    # register select with compaction (BERT-base), without it (uniform attention: every
+    # probability equal), eight registers (H len <= 512) and the LDS radix select
+    # (H len > 2048)
+    import torch
+
+    import paper_2201_12854_amd as mca
+
+    if case == "bert_base":
+        L = wl.bert_base_bf16().subset([0, 1, 2])
+    elif case == "uniform":
+        L = wl.make_layer(2, 128, 96, 12, "bf16", data_seed=13, lens=np.array([128, 77]))
+        L.Q[...] = 0.0
+    elif case == "small":
+        L = wl.make_layer(3, 40, 64, 4, "f32", data_seed=14, lens=np.array([40, 23, 1]), q_scale=2.0)
+    else:
+        L = wl.make_layer(2, 600, 128, 4, "bf16", data_seed=10, lens=np.array([600, 413]), q_scale=2.0)
+    print(f"[case] median selection {case}: B={L.batch} n={L.seq} H={L.heads}", flush=True)
+    t = to_device(L, dev)
+    prep = mca.prepare_weights(t["Wv"])
+    B, n, H = L.batch, L.seq, L.heads
+    desc = mca.make_desc(B, n, H, L.d_in, 1 if L.dtype == "bf16" else 0, 0.4, 0,
+                         importance=2)
+    ws_bytes = mca.workspace_size(desc)
+    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device=dev)
+    out = mca.attention_forward(t["Q"], t["K"], t["X"], t["Wv"], prep, 0.4, 0, heads=H, seq_lens=t["lens"],
+                                export=True, workspace=ws, importance="median")
+    torch.cuda.synchronize()
+    acol_bytes = (4 * B * n * H * n + 255) // 256 * 256  # the last workspace segment
+    acol = ws[ws_bytes - acol_bytes:ws_bytes - acol_bytes + 4 * B * n * H * n].view(torch.float32)
+    acol = acol.reshape(B, n, H, n).cpu().numpy()
+    m = out.colmax.cpu().numpy()
+    for b in range(B):
+        ln = int(L.lens[b])
+        want = np.array([_median_of(acol[b, j, :, :ln].ravel()) for j in range(ln)])
+        got = m[b, :ln]
+        assert np.array_equal(got.view(np.uint32), want.view(np.uint32)), \
+            (b, np.flatnonzero(got != want)[:5])
+
+
 # ------------------------------------------------------------------ exact encoding from a count
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("exact_from", [1, 20, 64])
