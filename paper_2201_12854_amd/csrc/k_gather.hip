@@ -635,11 +635,14 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated(FwdParams p) {
     }
 }
 
-// k_saturated_lds (16-byte x chunks): 32 NTW columns per block (256 with NTW = 8), 16 NTW
-// per wave, the operands staged through LDS by direct global-to-LDS loads (16 bytes per
-// lane, no registers) with kSatStages - 1 k steps in flight. Per k step the block stages
-// its four 16-row A tiles and 2 NTW 16-column B tiles in fragment order (1 KB each; lane
-// l's 16 bytes at 16 l), and every wave reads its two A and NTW B fragments from there. A
+// k_saturated_lds (16-byte x chunks): 32 NTW columns (256 with NTW = 8) and 32 MTW tokens
+// per block, a quarter of both per wave (2 x 2 waves: 16 MTW tokens x 16 NTW columns
+// each), the operands staged through LDS by direct global-to-LDS loads (16 bytes per lane,
+// no registers) with ST - 1 k steps in flight. Per k step the block stages its 2 MTW
+// 16-row A tiles and 2 NTW 16-column B tiles in fragment order (1 KB each; lane l's 16 bytes
+// at 16 l), and every wave reads its MTW A and NTW B fragments from there: with MTW = 4 a
+// wave's twelve fragment reads feed 32 MFMAs (MTW = 2: ten feed 16), so the LDS reads and
+// the loads into LDS per MFMA are what a 128 x 256 tile needs rather than a 64 x 256 one. A
 // chunk past the end of a row re-reads the row's last chunk: the prepared W_v^T is zero
 // there.
 constexpr int kSatStages = 3;
@@ -668,22 +671,26 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int BF, int NTW>
+template <int BF, int NTW, int MTW, int ST>
 __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int E = BF ? 8 : 4;     // elements per 16 bytes
   constexpr int KS = BF ? 32 : 16;  // k per step
+  constexpr int NA = 2 * MTW;       // A tiles per block (16 tokens each)
   constexpr int NB = 2 * NTW;       // B tiles per block (16 columns each)
+  constexpr int TOK = 16 * NA;      // tokens per block
   constexpr int COLS = 16 * NB;     // columns per block
-  constexpr int TILES = 4 + NB;     // 1 KB tiles per step slot: A tiles 0-3, then the B tiles
-  constexpr int kLoads = 1 + NB / 4;  // direct loads per wave per step: A tile w, B tiles w NB/4 ..
+  constexpr int TILES = NA + NB;    // 1 KB tiles per step slot: the A tiles, then the B tiles
+  static_assert(NA % 4 == 0 && NB % 4 == 0, "every wave loads the same number of tiles");
+  static_assert(ST >= 2, "stages");
+  constexpr int kLoads = (NA + NB) / 4;  // direct loads per wave per step
   constexpr int kSlot = TILES * 64 * 16;
-  __shared__ int satl[kSatTokens];
+  __shared__ int satl[TOK];
   __shared__ int nsat_s;
-  __shared__ __align__(16) uint4 stage[kSatStages * TILES * 64];
+  __shared__ __align__(16) uint4 stage[ST * TILES * 64];
   const int ncb = p.d_out / COLS;
   const int cb = blockIdx.x % ncb, tb = blockIdx.x / ncb;
-  const int64_t t0 = (int64_t)tb * kSatTokens;
+  const int64_t t0 = (int64_t)tb * TOK;
   const int64_t ntok = (int64_t)p.B * p.n;
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -691,49 +698,54 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
   const int d_in = p.d_in;
   if (tid == 0) nsat_s = 0;
   __syncthreads();
-  if (tid < kSatTokens && t0 + tid < ntok && exact_token(p.r[t0 + tid], d_in, p.exact_from))
-    satl[atomicAdd(&nsat_s, 1)] = tid;
+  for (int i = tid; i < TOK; i += kSatThreads)
+    if (t0 + i < ntok && exact_token(p.r[t0 + i], d_in, p.exact_from)) satl[atomicAdd(&nsat_s, 1)] = i;
   __syncthreads();
   const int nsat = nsat_s;
   if (nsat == 0) return;  // block-uniform
   const int nks = p.din_pad / KS;
-  // this wave's loads: A tile `wave` (list rows 16 wave + r16, chunk E g of the step) and
-  // B tiles 2 wave, 2 wave + 1 of the block's 128 columns
-  const T* xrow = static_cast<const T*>(p.X) + (t0 + satl[min(16 * wave + r16, nsat - 1)]) * d_in;
+  // this wave's loads: A tiles (NA / 4) wave + j (list rows 16 tile + r16, chunk E g of the
+  // step) and B tiles (NB / 4) wave + j of the block's columns
+  const T* xrow[NA / 4];
+#pragma unroll
+  for (int j = 0; j < NA / 4; ++j)
+    xrow[j] = static_cast<const T*>(p.X) + (t0 + satl[min(16 * ((NA / 4) * wave + j) + r16, nsat - 1)]) * d_in;
   const int klast = d_in - E;  // last chunk of a row
   const T* wt = static_cast<const T*>(p.Wt) + ((int64_t)(cb * COLS / 16) * nks * 64 + lane) * E;
   const uint32_t st0 = lds_addr(stage);
   auto issue = [&](int ks) {
-    const uint32_t slot = st0 + (uint32_t)(ks % kSatStages) * kSlot;
-    load_lds16(xrow + min(ks * KS + E * g, klast), slot + (uint32_t)wave * 1024u);
+    const uint32_t slot = st0 + (uint32_t)(ks % ST) * kSlot;
+#pragma unroll
+    for (int j = 0; j < NA / 4; ++j)
+      load_lds16(xrow[j] + min(ks * KS + E * g, klast), slot + (uint32_t)((NA / 4) * wave + j) * 1024u);
 #pragma unroll
     for (int j = 0; j < NB / 4; ++j) {
       const int nt = (NB / 4) * wave + j;
-      load_lds16(wt + ((int64_t)nt * nks + ks) * 64 * E, slot + (uint32_t)(4 + nt) * 1024u);
+      load_lds16(wt + ((int64_t)nt * nks + ks) * 64 * E, slot + (uint32_t)(NA + nt) * 1024u);
     }
   };
   const int wm = wave >> 1, wn = wave & 1;
-  const bool active = 32 * wm < nsat;  // wave-uniform
-  f32x4_t acc[2][NTW];
+  const bool active = 16 * MTW * wm < nsat;  // wave-uniform
+  f32x4_t acc[MTW][NTW];
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+  for (int mt = 0; mt < MTW; ++mt)
 #pragma unroll
     for (int nt = 0; nt < NTW; ++nt) acc[mt][nt] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int ks = 0; ks < kSatStages - 1; ++ks) issue(min(ks, nks - 1));
+  for (int ks = 0; ks < ST - 1; ++ks) issue(min(ks, nks - 1));
   for (int ks = 0; ks < nks; ++ks) {
-    wait_vmcnt<(kSatStages - 2) * kLoads>();  // this wave's loads of step ks have landed
-    stage_barrier();                           // everyone's; and step ks - 1's slot is free
-    issue(min(ks + kSatStages - 1, nks - 1));  // past the end: reloads of the last step into a free slot
+    wait_vmcnt<(ST - 2) * kLoads>();   // this wave's loads of step ks have landed
+    stage_barrier();                    // everyone's; and step ks - 1's slot is free
+    issue(min(ks + ST - 1, nks - 1));  // past the end: reloads of the last step into a free slot
     if (active) {
-      const uint4* st = stage + (ks % kSatStages) * TILES * 64;
-      uint4 a[2], b[NTW];
+      const uint4* st = stage + (ks % ST) * TILES * 64;
+      uint4 a[MTW], b[NTW];
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt) a[mt] = st[(2 * wm + mt) * 64 + lane];
+      for (int mt = 0; mt < MTW; ++mt) a[mt] = st[(MTW * wm + mt) * 64 + lane];
 #pragma unroll
-      for (int nt = 0; nt < NTW; ++nt) b[nt] = st[(4 + NTW * wn + nt) * 64 + lane];
+      for (int nt = 0; nt < NTW; ++nt) b[nt] = st[(NA + NTW * wn + nt) * 64 + lane];
 #pragma unroll
-      for (int mt = 0; mt < 2; ++mt)
+      for (int mt = 0; mt < MTW; ++mt)
 #pragma unroll
         for (int nt = 0; nt < NTW; ++nt) {
           if constexpr (BF) {
@@ -751,12 +763,12 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
   wait_vmcnt<0>();  // the trailing reloads have landed before the wave ends
   if (!active) return;
   const int c0 = cb * COLS + 16 * NTW * wn;
-  // acc[mt][nt][i] = H~[list row 32 wm + 16 mt + 4 g + i][c0 + 16 nt + r16]
+  // acc[mt][nt][i] = H~[list row 16 MTW wm + 16 mt + 4 g + i][c0 + 16 nt + r16]
 #pragma unroll
-  for (int mt = 0; mt < 2; ++mt)
+  for (int mt = 0; mt < MTW; ++mt)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int row = 32 * wm + 16 * mt + 4 * g + i;
+      const int row = 16 * MTW * wm + 16 * mt + 4 * g + i;
       if (row < nsat) {
         const int64_t base = (t0 + satl[row]) * p.d_out + c0 + r16;
 #pragma unroll
@@ -815,10 +827,11 @@ hipError_t launch_saturated(const FwdParams& p, hipStream_t s) {
   const bool vec = p.d_in % (p.bf16 ? 8 : 4) == 0;
   const int64_t ntok = (int64_t)p.B * p.n;
   const dim3 grid((unsigned)(((ntok + kSatTokens - 1) / kSatTokens) * (p.d_out / kSatCols))), blk(kSatThreads);
-  if (vec) {  // 64 tokens x 256 columns per block
-    const dim3 g2((unsigned)(((ntok + kSatTokens - 1) / kSatTokens) * (p.d_out / 256)));
-    return p.bf16 ? launch_stage_kernel(k_saturated_lds<1, 8>, g2, blk, 0, s, p)
-                  : launch_stage_kernel(k_saturated_lds<0, 8>, g2, blk, 0, s, p);
+  if (vec && p.d_out % 256 == 0) {  // 128 (bf16) or 64 (float32) tokens x 256 columns per block
+    const int tok = p.bf16 ? 128 : 64;
+    const dim3 g2((unsigned)(((ntok + tok - 1) / tok) * (p.d_out / 256)));
+    return p.bf16 ? launch_stage_kernel(k_saturated_lds<1, 8, 4, kSatStages>, g2, blk, 0, s, p)
+                  : launch_stage_kernel(k_saturated_lds<0, 8, 2, kSatStages>, g2, blk, 0, s, p);
   }
   return p.bf16 ? launch_stage_kernel(k_saturated<1, false>, grid, blk, 0, s, p)
                 : launch_stage_kernel(k_saturated<0, false>, grid, blk, 0, s, p);
