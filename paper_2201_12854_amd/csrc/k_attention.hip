@@ -45,19 +45,29 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTile = 64;                // queries per block and keys per tile
-// LDS row strides of bf16 tiles (elements). The streaming kernels use 160-byte rows: a
-// 16-byte fragment read (16 rows of one column group, four groups) and a transposing 8-byte
-// read of an H~ tile are then free of bank conflicts on gfx950, where 144-byte rows take two
-// passes per read (measured with the LDS bank-conflict counter). The kernels that keep every
-// tile of a row in LDS use 144-byte rows: there the smaller footprint leaves room for one
-// more block per CU, which measured faster than conflict-free reads.
-constexpr int kStrideBf = kDHead + 8;
+// bf16 tiles in LDS: rows of 64 elements (128 bytes, no padding) whose eight 16-byte
+// chunks are permuted per row, chunk c of row r stored at chunk c ^ (r & 7). gfx950 serves a
+// wave's 16-byte LDS accesses in four cycles, and its transposing 8-byte reads in two, only
+// when the lanes served together fall in distinct banks; with this permutation that holds
+// for the three accesses to a tile (a bank-conflict probe measured each): the fragment
+// reads of Q K^T (16 consecutive rows, one chunk), the transposing reads of P V (rows
+// 4 g + i, one pair of chunks) and the row stores. Unpermuted 128-byte rows serialise the
+// fragment reads four ways, 144-byte rows two ways.
+constexpr int kStrideBf = kDHead;
+// The streaming output pass keeps its H~ tiles unpermuted in 160-byte rows instead (also
+// conflict-free for the transposing reads): there the four column groups of a read are
+// constant offsets from one address, where the permutation would need a register per group
+// and take the kernel past the register count that allows three waves per SIMD.
 constexpr int kStrideBfWide = kDHead + 16;
+// element offset of (row, col) in a bf16 tile; col a multiple of 4 (an 8-byte piece)
+__device__ __forceinline__ int kv_at(int row, int col) {
+  return row * kStrideBf + ((((col >> 3) ^ (row & 7)) << 3) | (col & 7));
+}
 constexpr int kStrideF = kDHead + 4;     // LDS row stride of fp32 tiles (elements)
 
 template <int BF> struct Elem { using T = float; };
 template <> struct Elem<1> { using T = uint16_t; };
-template <int BF, bool WIDE = false> constexpr int stride_of() { return BF ? (WIDE ? kStrideBfWide : kStrideBf) : kStrideF; }
+template <int BF> constexpr int stride_of() { return BF ? kStrideBf : kStrideF; }
 
 // ------------------------------------------------------------------ Q fragments
 // The wave's 16 queries as the B operand of S^T = K Q^T.
@@ -115,19 +125,20 @@ __device__ __forceinline__ TileRegs tile_load(const void* base, int64_t ld, int 
 }
 
 // row-major LDS tile [key][d]
-template <int BF, bool WIDE = false>
+template <int BF>
 __device__ __forceinline__ void tile_vec_store(uint4 u, typename Elem<BF>::T* lds, int v) {
   constexpr int R = BF ? 8 : 16;
-  *reinterpret_cast<uint4*>(lds + (v / R) * stride_of<BF, WIDE>() + (v % R) * (BF ? 8 : 4)) = u;
+  if constexpr (BF) *reinterpret_cast<uint4*>(lds + kv_at(v / R, (v % R) * 8)) = u;
+  else *reinterpret_cast<uint4*>(lds + (v / R) * kStrideF + (v % R) * 4) = u;
 }
 
-template <int BF, bool WIDE = false>
+template <int BF>
 __device__ __forceinline__ void tile_store(const TileRegs& t, typename Elem<BF>::T* lds, int tid) {
-  tile_vec_store<BF, WIDE>(t.v0, lds, tid);
-  tile_vec_store<BF, WIDE>(t.v1, lds, tid + kThreads);
+  tile_vec_store<BF>(t.v0, lds, tid);
+  tile_vec_store<BF>(t.v1, lds, tid + kThreads);
   if constexpr (!BF) {
-    tile_vec_store<BF, WIDE>(t.v2, lds, tid + 2 * kThreads);
-    tile_vec_store<BF, WIDE>(t.v3, lds, tid + 3 * kThreads);
+    tile_vec_store<BF>(t.v2, lds, tid + 2 * kThreads);
+    tile_vec_store<BF>(t.v3, lds, tid + 3 * kThreads);
   }
 }
 
@@ -135,7 +146,12 @@ __device__ __forceinline__ void tile_store(const TileRegs& t, typename Elem<BF>:
 // operand (8 keys of one column per lane) with the transposing LDS read below.
 template <int BF, bool WIDE = false>
 __device__ __forceinline__ void tile_store_v(const TileRegs& t, typename Elem<BF>::T* lds, int tid) {
-  tile_store<BF, WIDE>(t, lds, tid);
+  if constexpr (BF && WIDE) {
+    *reinterpret_cast<uint4*>(lds + (tid / 8) * kStrideBfWide + (tid % 8) * 8) = t.v0;
+    *reinterpret_cast<uint4*>(lds + (tid / 8 + kThreads / 8) * kStrideBfWide + (tid % 8) * 8) = t.v1;
+  } else {
+    tile_store<BF>(t, lds, tid);
+  }
 }
 
 // ds_read_b64_tr_b16 (gfx950). Within each row of 16 lanes, every lane supplies the address
@@ -159,7 +175,7 @@ __device__ __forceinline__ void score_tile(f32x4_t acc[4], const uint16_t* Ks, c
     acc[s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 * ks + 8 * g);
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + kv_at(16 * s + r16, 32 * ks + 8 * g));
       acc[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, q.v[ks], acc[s], 0, 0, 0);
     }
   }
@@ -215,7 +231,8 @@ __device__ __forceinline__ void pv_tile(f32x4_t y[4], const f32x4_t acc[4], cons
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       // lane (g, r16) addresses key 32 pp + 4 g + r16 / 4, columns 16 c + 4 (r16 % 4) .. + 3
-      const uint16_t* vrow = Vs + (32 * pp + 4 * g + (r16 >> 2)) * kStrideBf + 16 * c + 4 * (r16 & 3);
+      // rows 32 pp + 4 g + r16 / 4 and 16 further (the same permutation: it depends on row & 7)
+      const uint16_t* vrow = Vs + kv_at(32 * pp + 4 * g + (r16 >> 2), 16 * c + 4 * (r16 & 3));
       const uint2 lo = lds_read_tr16(vrow);
       const uint2 hi = lds_read_tr16(vrow + 16 * kStrideBf);
       const bf16x8_t bv = __builtin_bit_cast(bf16x8_t, make_uint4(lo.x, lo.y, hi.x, hi.y));
@@ -411,7 +428,7 @@ __device__ __forceinline__ void score_tile_qk(f32x4_t acc[4], const uint16_t* Ks
     acc[s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBf + 32 * ks + 8 * g);
+      const bf16x8_t b = *reinterpret_cast<const bf16x8_t*>(Ks + kv_at(16 * s + r16, 32 * ks + 8 * g));
       acc[s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q.v[ks], b, acc[s], 0, 0, 0);
     }
   }
@@ -824,7 +841,7 @@ __device__ __forceinline__ void score_tile_m(f32x4_t acc[MT][4], const uint16_t*
     for (int m = 0; m < MT; ++m) acc[m][s] = f32x4_t{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int ks = 0; ks < 2; ++ks) {
-      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBfWide + 32 * ks + 8 * g);
+      const bf16x8_t a = *reinterpret_cast<const bf16x8_t*>(Ks + kv_at(16 * s + r16, 32 * ks + 8 * g));
 #pragma unroll
       for (int m = 0; m < MT; ++m) acc[m][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, q[m].v[ks], acc[m][s], 0, 0, 0);
     }
@@ -896,13 +913,16 @@ __device__ __forceinline__ void pv_tile_m(f32x4_t y[MT][4], const f32x4_t acc[MT
 // stored before iteration t's barrier (its buffer was last read by the Q K^T of tile t - 1,
 // issued in iteration t - 2), H~ tile t + 1 after it (its buffer was last read by the P V of
 // tile t - 1 in iteration t - 1, which every wave has finished once it passes the barrier).
+// The bf16 full-attention instance is held to 168 registers (three waves per SIMD), which it
+// meets without spilling; the others need more.
 template <int BF, bool BAND, int MT>
-__global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((BF && !BAND) ? 3 : 1))) void k_attn_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
-  constexpr int S = stride_of<BF, true>();
+  constexpr int S = stride_of<BF>();
   constexpr int QB = 64 * MT;  // queries per block
   __shared__ __align__(16) T Ks[2][kTile * S];
-  __shared__ __align__(16) T Vs[2][kTile * S];
+  constexpr int SV = BF ? kStrideBfWide : kStrideF;  // H~ tiles: unpermuted rows
+  __shared__ __align__(16) T Vs[2][kTile * SV];
   BlockCtx c = block_ctx_q<QB>(p);
   const int64_t off = (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Qb = static_cast<const T*>(p.Q) + off;
@@ -930,7 +950,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
   const int nvis = tile_count(c);
   TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
   TileRegs vr = tile_load<BF>(Vb, c.d_out, 0, c.n, c.tid);
-  tile_store<BF, true>(kr, Ks[0], c.tid);
+  tile_store<BF>(kr, Ks[0], c.tid);
   tile_store_v<BF, true>(vr, Vs[0], c.tid);
   const int t1 = tile_at(c, min(1, nvis - 1)) * kTile;
   kr = tile_load<BF>(Kb, c.d_out, t1, c.n, c.tid);
@@ -954,7 +974,7 @@ __global__ __launch_bounds__(kThreads) void k_attn_stream(FwdParams p) {
       }
     }
     const int nb = (t + 1) & 1;
-    tile_store<BF, true>(kr, Ks[nb], c.tid);
+    tile_store<BF>(kr, Ks[nb], c.tid);
     lds_barrier();
     tile_store_v<BF, true>(vr, Vs[nb], c.tid);
     const int next = tile_at(c, min(t + 2, nvis - 1)) * kTile;
@@ -1012,8 +1032,8 @@ __device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const uint16_t
                                                int g, const f32x4_t init[2]) {
 #pragma unroll
   for (int s = 0; s < 4; ++s) {
-    const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBfWide + 8 * g);
-    const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(Ks + (16 * s + r16) * kStrideBfWide + 32 + 8 * g);
+    const bf16x8_t b0 = *reinterpret_cast<const bf16x8_t*>(Ks + kv_at(16 * s + r16, 8 * g));
+    const bf16x8_t b1 = *reinterpret_cast<const bf16x8_t*>(Ks + kv_at(16 * s + r16, 32 + 8 * g));
     acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[0].v[0], b0, init[0], 0, 0, 0);
     acc[1][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[1].v[0], b0, init[1], 0, 0, 0);
     acc[0][s] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(q[0].v[1], b1, acc[0][s], 0, 0, 0);
@@ -1041,7 +1061,7 @@ __device__ __forceinline__ void score_tile_qk2(f32x4_t acc[2][4], const float* K
 template <int BF, bool BAND, int IMP>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void k_scores_stream(FwdParams p) {
   using T = typename Elem<BF>::T;
-  constexpr int S = stride_of<BF, true>();
+  constexpr int S = stride_of<BF>();
   __shared__ __align__(16) T Ks[2][kTile * S];
   // sweep 2: per tile (three in flight), per wave and lane row, the lane row's value of key
   // 16 s + r16 at [r16][s]
@@ -1090,7 +1110,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // (sweep 2 combines the waves' values of tile t - 1 after iteration t's barrier).
   auto sweep = [&](const f32x4_t init[2], auto&& work) {
     TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
-    tile_store<BF, true>(kr, Ks[0], c.tid);
+    tile_store<BF>(kr, Ks[0], c.tid);
     kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(1, nvis - 1)) * kTile, c.n, c.tid);
     lds_barrier();
     f32x4_t accA[2][4], accB[2][4];
@@ -1100,7 +1120,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       const int lim = c.len - kt * kTile;
       if (BAND || lim < kTile) mask(cur, kt, lim);  // tile-uniform
       T* buf = Ks[(t + 1) & 1];
-      tile_store<BF, true>(kr, buf, c.tid);
+      tile_store<BF>(kr, buf, c.tid);
       lds_barrier();
       kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 2, nvis - 1)) * kTile, c.n, c.tid);
       score_tile_qk2(nxt, buf, qf, c.r16, c.g, init);
