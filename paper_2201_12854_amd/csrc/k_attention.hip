@@ -1108,13 +1108,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   // Every iteration does the same (the last one stages and multiplies the last tile again,
   // with results unused): one straight-line region per tile, and a barrier in every iteration
   // (sweep 2 combines the waves' values of tile t - 1 after iteration t's barrier).
-  auto sweep = [&](const f32x4_t init[2], auto&& work) {
+  // `first` sees tile 0's scores (masked) before the loop.
+  auto sweep = [&](const f32x4_t init[2], auto&& first, auto&& work) {
     TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
     tile_store<BF>(kr, Ks[0], c.tid);
     kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(1, nvis - 1)) * kTile, c.n, c.tid);
     lds_barrier();
     f32x4_t accA[2][4], accB[2][4];
     score_tile_qk2(accA, Ks[0], qf, c.r16, c.g, init);
+    first(accA);
     auto step = [&](f32x4_t cur[2][4], f32x4_t nxt[2][4], int t) {
       const int kt = tile_at(c, t);
       const int lim = c.len - kt * kTile;
@@ -1135,49 +1137,84 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   };
 
   // Sweep 1: per lane and query, a reference logit M and the sum of exp2(logit - M) over
-  // the lane's keys; the 16 lanes of a row are combined at the end. The terms are added
-  // under the current reference as long as a tile's four terms of a query sum to at most
-  // 2^16 (no score more than 16 log2 units above M); otherwise (the first tile, and rarely
-  // later) the wave redoes the tile with M raised to the running max and rescales the sum.
-  // The branch is wave-uniform.
+  // the lane's keys; the 16 lanes of a row are combined at the end. M is the row's largest
+  // logit in tile 0 (finite: key 0 is attended by every query), and every later term is
+  // added under it, with no check per tile: the terms of a positive sum may exceed 1 without
+  // losing relative precision, and only a logit more than 127 log2 units above M would
+  // overflow. If any sum came out non-finite (that, or non-finite scores), the wave runs the
+  // sweep again the careful way: terms added under the current reference as long as a tile's
+  // four terms of a query sum to at most 2^16, otherwise (the first tile, and rarely later)
+  // the tile redone with M raised to the running max and the sum rescaled. Both branches
+  // are wave-uniform.
   constexpr float kNoMax = -1e30f;  // below every logit: no attended key seen yet
   constexpr float kRaise = 65536.f;
   float M[8], Ls[8];
-#pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    M[k] = kNoMax;
-    Ls[k] = 0.f;
-  }
   const f32x4_t zero2[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
-  sweep(zero2, [&](f32x4_t acc[2][4], int, int) {
-    float ts[8];
-    bool raise = false;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) Ls[k] = 0.f;
+  sweep(
+      zero2,
+      [&](f32x4_t acc[2][4]) {
+        if (BAND || c.len < kTile) mask(acc, 0, c.len);
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int m = k >> 2, i = k & 3;
+          const float dm = vmax(vmax3(acc[m][0][i], acc[m][1][i], acc[m][2][i]), acc[m][3][i]);
+          M[k] = __fmul_rn(row16_max(dm), kLog2eOver8);
+        }
+      },
+      [&](f32x4_t acc[2][4], int, int) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k) {
+          const int m = k >> 2, i = k & 3;
+          float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -M[k]));
+#pragma unroll
+          for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
+          Ls[k] += e;
+        }
+      });
+  bool overflow = false;
+#pragma unroll
+  for (int k = 0; k < 8; ++k) overflow |= !(Ls[k] < INFINITY);
+  if (__any(overflow)) {
+    lds_barrier();  // the first sweep is done with both K buffers
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
-      const int m = k >> 2, i = k & 3;
-      float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -M[k]));
-#pragma unroll
-      for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
-      ts[k] = e;
-      raise |= !(e <= kRaise);
+      M[k] = kNoMax;
+      Ls[k] = 0.f;
     }
-    if (__any(raise)) {
+    sweep(
+        zero2, [&](f32x4_t[2][4]) {},
+        [&](f32x4_t acc[2][4], int, int) {
+          float ts[8];
+          bool raise = false;
 #pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        const int m = k >> 2, i = k & 3;
-        const float dm = vmax(vmax3(acc[m][0][i], acc[m][1][i], acc[m][2][i]), acc[m][3][i]);
-        const float Mn = vmax(M[k], __fmul_rn(dm, kLog2eOver8));
-        float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -Mn));
+          for (int k = 0; k < 8; ++k) {
+            const int m = k >> 2, i = k & 3;
+            float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -M[k]));
 #pragma unroll
-        for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -Mn));
-        Ls[k] = __fmul_rn(Ls[k], exp2_fast(__fsub_rn(M[k], Mn))) + e;
-        M[k] = Mn;
-      }
-    } else {
+            for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -M[k]));
+            ts[k] = e;
+            raise |= !(e <= kRaise);
+          }
+          if (__any(raise)) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k) Ls[k] += ts[k];
-    }
-  });
+            for (int k = 0; k < 8; ++k) {
+              const int m = k >> 2, i = k & 3;
+              const float dm = vmax(vmax3(acc[m][0][i], acc[m][1][i], acc[m][2][i]), acc[m][3][i]);
+              const float Mn = vmax(M[k], __fmul_rn(dm, kLog2eOver8));
+              float e = exp2_fast(__fmaf_rn(acc[m][0][i], kLog2eOver8, -Mn));
+#pragma unroll
+              for (int s = 1; s < 4; ++s) e += exp2_fast(__fmaf_rn(acc[m][s][i], kLog2eOver8, -Mn));
+              Ls[k] = __fmul_rn(Ls[k], exp2_fast(__fsub_rn(M[k], Mn))) + e;
+              M[k] = Mn;
+            }
+          } else {
+#pragma unroll
+            for (int k = 0; k < 8; ++k) Ls[k] += ts[k];
+          }
+        });
+  }
   float cq[8], cc[8];
   f32x4_t dneg[2];  // sweep 2's accumulator start: -cc / s per query (-inf for padded queries)
 #pragma unroll
@@ -1225,7 +1262,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
   };
   lds_barrier();  // sweep 1 is done with both K buffers
-  sweep(dneg, [&](f32x4_t acc[2][4], int t, int kt) {
+  sweep(dneg, [&](f32x4_t[2][4]) {}, [&](f32x4_t acc[2][4], int t, int kt) {
     // the lane's eight queries per key: the max of dot - cc / s (or the sum of the
     // probabilities exp2(s (dot - cc / s))), left in cm for the combination over the lane
     // rows and waves

@@ -81,9 +81,7 @@ def colmax_tolerance(L, importance="max", window=None):
         Lb = int(L.lens[b])
         att = oracle.attended(np.arange(Lb), Lb, Lb, window)
         nk = att.sum(axis=1).astype(np.float64)  # keys per query
-        tmax_h = np.full((H, Lb), -np.inf)
-        dnear_h = np.zeros((H, Lb))
-        dall = np.zeros(Lb)
+        ts, Dts = [], []
         for h in range(H):
             cs = slice(64 * h, 64 * h + 64)
             q = L.Q[b, :Lb, cs].astype(np.float64)
@@ -113,14 +111,19 @@ def colmax_tolerance(L, importance="max", window=None):
                 cp = np.abs(c - np.log2(nk)) if window > 0 else np.abs(c)
                 Ec = Ec + (_gamma(65) * (1 + U32) + U32 / 2) * cp
             Dt = np.where(att, dz + Ec[:, None] + np.abs(np.where(att, t, 0)) * U32 / 2, 0.0)
-            assert Dt.max() < near_w / 4, Dt.max()
-            tmax = t.max(axis=0)
-            tmax_h[h] = tmax
-            dnear_h[h] = np.where(t >= tmax[None, :] - near_w, Dt, 0.0).max(axis=0)
-            dall = np.maximum(dall, Dt.max(axis=0))
+            ts.append(np.where(att, t, -np.inf))
+            Dts.append(Dt)
+        # a pair whose t lies more than near_w below a key's maximum cannot become the GPU's
+        # maximum when near_w exceeds twice every perturbation; 1e-2 unless the logits are
+        # so large that the perturbations reach a quarter of it
+        nw = max(near_w, 4.0 * max(float(D.max()) for D in Dts))
+        tmax_h = np.stack([t.max(axis=0) for t in ts])
+        dnear_h = np.stack([np.where(t >= tm[None, :] - nw, D, 0.0).max(axis=0)
+                            for t, D, tm in zip(ts, Dts, tmax_h)])
+        dall = np.max(np.stack([D.max(axis=0) for D in Dts]), axis=0)
         if importance == "max":
             T = tmax_h.max(axis=0)
-            delta = np.where(tmax_h >= T[None, :] - near_w, dnear_h, 0.0).max(axis=0)
+            delta = np.where(tmax_h >= T[None, :] - nw, dnear_h, 0.0).max(axis=0)
             tol[b, :Lb] = np.exp2(delta) * (1 + EPS_EXP) - 1
         else:  # every probability enters the mean or the median
             tol[b, :Lb] = np.exp2(dall) * (1 + EPS_EXP) - 1
@@ -201,15 +204,24 @@ def ambiguous_tokens(m_ref, lens, alpha, d_in, tol, window=0):
     return amb
 
 
+FLT_MIN = 2.0 ** -126  # smallest normal float32
+
+
 def check_colmax(m_gpu, m_ref, lens, tol):
-    """m of every valid key within its bound; padded keys exactly 0. Returns the largest
-    error as a fraction of the bound."""
+    """m of every valid key within its bound; padded keys exactly 0. A column maximum
+    below the float32 normal range may come out as anything from 0 to FLT_MIN (the
+    hardware exp2 flushes subnormal results); its count is 1 either way for any alpha
+    above n FLT_MIN. Returns the largest error as a fraction of the bound."""
     valid = np.arange(m_ref.shape[1])[None, :] < np.asarray(lens)[:, None]
     assert np.all(m_gpu[~valid] == 0)
-    rel = np.abs(m_gpu[valid].astype(np.float64) - m_ref[valid]) / m_ref[valid]
-    bad = rel > tol[valid]
-    assert not bad.any(), (rel[bad][:5], tol[valid][bad][:5])
-    return float((rel / tol[valid]).max())
+    mg = m_gpu[valid].astype(np.float64)
+    mr = m_ref[valid]
+    tiny = mr < FLT_MIN
+    assert np.all((mg[tiny] >= 0) & (mg[tiny] <= FLT_MIN * (1 + tol[valid][tiny]))), mg[tiny].max()
+    rel = np.abs(mg[~tiny] - mr[~tiny]) / mr[~tiny]
+    bad = rel > tol[valid][~tiny]
+    assert not bad.any(), (rel[bad][:5], tol[valid][~tiny][bad][:5])
+    return float((rel / tol[valid][~tiny]).max()) if rel.size else 0.0
 
 
 def check_rule_property(r, m, lens, alpha, d_in, window=0):

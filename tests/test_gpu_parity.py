@@ -31,8 +31,10 @@ def dev():
     return torch.device("cuda:0")
 
 
-def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", importance="max", exact_from=0):
+def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", importance="max", exact_from=0,
+                tol_y=None):
     """Oracle vs GPU on every stage; returns (#ambiguous tokens, #sampled tokens)."""
+    tol_y = TOL_Y[L.dtype] if tol_y is None else tol_y
     print(f"[case] {L.name} dtype={L.dtype} B={L.batch} n={L.seq} d_in={L.d_in} H={L.heads} "
           f"alpha={alpha} seed={seed} sampling={sampling} window={L.window} importance={importance} "
           f"exact_from={exact_from}", flush=True)
@@ -51,14 +53,14 @@ def _full_check(L, dev, alpha, seed, *, check_e2e_y=True, sampling="token", impo
     assert not np.any(diff & ~amb), np.argwhere(diff & ~amb)[:5]
     assert np.all(np.abs(g["r"] - ref["r"])[amb] <= 1)
     if check_e2e_y and not amb.any():
-        assert row_rel_err(g["Y"], ref["Y"], L.lens) <= TOL_Y[L.dtype]
+        assert row_rel_err(g["Y"], ref["Y"], L.lens) <= tol_y
     # counts fixed to the oracle's: indices, coefficients, H~ and Y
     g2 = run_gpu(L, dev, alpha, seed, r_in=ref["r"], export_samples=True, tensors=t, sampling=sampling,
                  importance=importance, exact_from=exact_from)
     assert np.array_equal(g2["r"], ref["r"])
     n_tok = compare_samples(g2, ref, L)
     assert row_rel_err(g2["H"], ref["Htilde"], L.lens) <= TOL_H
-    assert row_rel_err(g2["Y"], ref["Y"], L.lens) <= TOL_Y[L.dtype]
+    assert row_rel_err(g2["Y"], ref["Y"], L.lens) <= tol_y
     return int(amb.sum()), n_tok
 
 
@@ -384,16 +386,28 @@ def test_score_pass_variants_ragged(dev, dtype, n, lens, window):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("bump", [20.0, 30.0, 40.0])
+@pytest.mark.parametrize("bump", [20.0, 30.0, 40.0, 100.0])
 def test_streaming_score_pass_raised_reference(dev, dtype, bump):
     # a few shared keys with a large logit bump (20 is about 29 in log2 units) at random
-    # places in rows of 700 keys: when a query meets one after its first tiles, the
-    # streaming score pass must raise its reference logit and rescale its running sum. The
-    # large logits also stretch the float32 error of the column max (the row normaliser
-    # reaches |c| near 60 at bump 40), which the per-key bound must still cover.
+    # places in rows of 700 keys: a query that meets one after its first tile adds terms far
+    # above its reference logit (its largest logit in tile 0). At bump 100 (144 log2 units)
+    # some of them pass the 127 log2 units a float32 term can take, so the streaming score
+    # pass must notice the overflow and redo its first sweep with a raised reference and
+    # rescaled sums. The large logits also stretch the float32 error of the column max (the
+    # row normaliser reaches |c| near 60 at bump 40), which the per-key bound must still
+    # cover.
     L = wl.make_layer(2, 700, 128, 4, dtype, data_seed=12, lens=np.array([700, 555]), salient_keys=6,
                       salient_bump=bump, token_scale_sigma=0.5)
-    amb, n_tok = _full_check(L, dev, 0.4, seed=4)
+    q = L.Q.astype(np.float64).reshape(2, 700, 4, 64)
+    k = L.K.astype(np.float64).reshape(2, 700, 4, 64)
+    lg = np.einsum("bqhd,bkhd->bhqk", q, k) * (np.log2(np.e) / 8)  # logits, log2 units
+    if bump == 100.0:  # the input does reach the overflow: some query's logit lies > 127 above tile 0's
+        assert np.any(lg.max(axis=3) - lg[..., :64].max(axis=3) > 127)
+    # the float32 logit and its row normaliser each carry a rounding error of about
+    # |logit| 2^-24, which moves a probability by ln 2 times that: above ~70 log2 units
+    # this, not the 1e-5 of the float32 path, bounds the output's relative error
+    tol_y = max(TOL_Y[dtype], 4 * np.log(2) * 2.0 ** -24 * np.abs(lg).max())
+    amb, n_tok = _full_check(L, dev, 0.4, seed=4, tol_y=tol_y)
     assert n_tok > 0
 
 
