@@ -506,6 +506,12 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
     const int nsampled = ctr[kCtrOff + kNumKeys];
     const int ngroups = (nsat + 15) / 16;
     const int nitems = ngroups + (nsampled + G - 1) / G;
+    // the next pass's r and U, loaded now so that their latency passes under this pass's items
+    int r_next = 0, u_next = 0;
+    if (t0 + kChunk + tid < t_end) {
+      r_next = p.r[t0 + kChunk + tid];
+      u_next = p.ucount[t0 + kChunk + tid];
+    }
 
     // ---- work items from the block's queue
     for (;;) {
@@ -524,7 +530,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
     if (t0 >= t_end) break;
     if (tid < kNumCtr) ctr[tid] = 0;
     __syncthreads();
-    MCA_CLASSIFY(t0, p.r[t0 + tid], p.ucount[t0 + tid])
+    MCA_CLASSIFY(t0, r_next, u_next)
   }
 #undef MCA_CLASSIFY
 #undef MCA_SLICE_LOAD
