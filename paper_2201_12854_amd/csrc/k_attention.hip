@@ -96,28 +96,48 @@ __device__ __forceinline__ void load_qfrag(QFrag<0>& f, const float* qrow, int g
 // A 64-row x 64-column tile of a [*, d_out] matrix (the head's column slice) held in
 // registers between its global load and its LDS store: 16-byte vectors v0, v1 (bf16) or
 // v0..v3 (fp32) per thread; vector v of the tile is row v / R, chunk v % R (R vectors per
-// row). Row indices past the padded length are clamped to the last row. (Plain members,
-// no arrays: the tiles are carried across loop iterations and must stay in registers.)
+// row). Rows past the padded length read as zeros. (Plain members, no arrays: the tiles
+// are carried across loop iterations and must stay in registers.)
 struct TileRegs {
   uint4 v0, v1, v2, v3;
 };
 
+// The loads go through a buffer descriptor built per tile in scalar registers: its base is
+// the tile's first row and its size ends with the head's slice of the last valid row, so
+// the per-lane offset (row within the tile times the row pitch, plus the chunk) is the
+// same for every tile and no per-tile address arithmetic runs on the vector units; the
+// hardware range check returns zeros for rows at or past n (whose keys are masked).
+constexpr int kBufWord3 = 0x00020000;  // gfx9 descriptor word 3: 32-bit data format
+
+// The descriptor of the tile whose first row is key0: with r = min(n - key0, 64) valid rows
+// its size is (r - 1) pitch + 64 elements, and 0 when r <= 0 (the pitch, d_out elements, is
+// at least 256 of them, so the max() below needs no branch).
 template <int BF>
-__device__ __forceinline__ uint4 tile_vec_load(const void* base, int64_t ld, int key0, int n, int v) {
-  using T = typename Elem<BF>::T;
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rsrc(const void* base, int64_t ld, int key0, int n) {
+  constexpr int ES = (int)sizeof(typename Elem<BF>::T);
+  const int bytes = max((min(n - key0, kTile) - 1) * (int)ld * ES + kDHead * ES, 0);
+  return __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<char*>(static_cast<const char*>(base) + (int64_t)key0 * ld * ES), 0, bytes, kBufWord3);
+}
+
+// vector v of the tile
+template <int BF>
+__device__ __forceinline__ uint4 tile_vec_load(__amdgpu_buffer_rsrc_t rs, int64_t ld, int v) {
   constexpr int R = BF ? 8 : 16;
-  const int key = min(key0 + v / R, n - 1);
-  return *reinterpret_cast<const uint4*>(static_cast<const T*>(base) + (int64_t)key * ld + (v % R) * (16 / (int)sizeof(T)));
+  constexpr int ES = (int)sizeof(typename Elem<BF>::T);
+  const int off = (v / R) * (int)ld * ES + (v % R) * 16;
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0));
 }
 
 template <int BF>
 __device__ __forceinline__ TileRegs tile_load(const void* base, int64_t ld, int key0, int n, int tid) {
+  const __amdgpu_buffer_rsrc_t rs = tile_rsrc<BF>(base, ld, key0, n);
   TileRegs t;
-  t.v0 = tile_vec_load<BF>(base, ld, key0, n, tid);
-  t.v1 = tile_vec_load<BF>(base, ld, key0, n, tid + kThreads);
+  t.v0 = tile_vec_load<BF>(rs, ld, tid);
+  t.v1 = tile_vec_load<BF>(rs, ld, tid + kThreads);
   if constexpr (!BF) {
-    t.v2 = tile_vec_load<BF>(base, ld, key0, n, tid + 2 * kThreads);
-    t.v3 = tile_vec_load<BF>(base, ld, key0, n, tid + 3 * kThreads);
+    t.v2 = tile_vec_load<BF>(rs, ld, tid + 2 * kThreads);
+    t.v3 = tile_vec_load<BF>(rs, ld, tid + 3 * kThreads);
   } else {
     t.v2 = t.v3 = make_uint4(0, 0, 0, 0);
   }
