@@ -267,8 +267,8 @@ constexpr int kHeader = 512;  // bytes of LDS before the per-token regions
 static_assert(sizeof(TokInfo) <= kHeader, "header");
 
 // LDS of a block: the header, then
-//   Eq. 4: per wave C uint64 [d_in] (after the draws: record x float32 [d_in], record w
-//          uint32 [d_in]) and cnt uint32 [d_in] (after the draws: record row | count);
+//   Eq. 4: per wave C uint64 [d_in] (after the draws: records (x bits, w), uint32 pairs
+//          [d_in]) and cnt uint32 [d_in] (after the draws: record row | count);
 //   Eq. 6: the shared C uint64 [d_in], then per wave cnt uint32 [d_in] and record x
 //          float32 [d_in].
 __host__ __device__ inline int round16(int v) { return (v + 15) / 16 * 16; }
@@ -377,24 +377,25 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   static_assert(NW >= 1 && NW <= kMaxWaves, "tokens per block");
   using T = typename Elem<BF>::T;
   extern __shared__ __align__(16) unsigned char smem[];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // the token's values are scalar
   const int64_t ntok = (int64_t)p.B * p.n;
   const int64_t tok = (int64_t)blockIdx.x * NW + wave;
   const int d_in = p.d_in, n = p.n;
   TokInfo& I = *reinterpret_cast<TokInfo*>(smem);
   uint64_t* C;      // this token's prefix sums (Eq. 6: the shared table)
   uint32_t* cnt;    // this token's draw counts, then record row | count
-  float* rec_x;     // record x
-  uint32_t* rec_w;  // record w (Eq. 4 only)
+  float* rec_x;     // record x (Eq. 6)
+  uint2* rec_xw;    // record (x, w) (Eq. 4)
   C = reinterpret_cast<uint64_t*>(smem + c_off(d_in, TABLE, wave));
   cnt = reinterpret_cast<uint32_t*>(smem + cnt_off(d_in, TABLE, wave));
   if constexpr (TABLE) {
     rec_x = reinterpret_cast<float*>(smem + cnt_off(d_in, true, wave) + round16(4 * d_in));
-    rec_w = nullptr;
+    rec_xw = nullptr;
     for (int i = threadIdx.x; i < d_in; i += 64 * NW) C[i] = p.wtable[i];
   } else {
-    rec_x = reinterpret_cast<float*>(C);
-    rec_w = reinterpret_cast<uint32_t*>(reinterpret_cast<unsigned char*>(C) + 4 * d_in);
+    rec_x = nullptr;
+    rec_xw = reinterpret_cast<uint2*>(C);
   }
   const bool live = tok < ntok;
   const int64_t tk = live ? tok : ntok - 1;  // a wave without a token reads a valid one
@@ -521,10 +522,18 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
       (void)frexpf(vmax, &e);  // vmax = f 2^e, f in [0.5, 1)
       const int shift = 32 - e;
       uint64_t lsum = 0;
+      if (full) {
 #pragma unroll
-      for (int k = 0; k < PER; ++k) {
-        wv[k] = (k < nrows) ? (uint32_t)ldexpf(vv[k], shift) : 0u;
-        lsum += wv[k];
+        for (int k = 0; k < PER; ++k) {
+          wv[k] = (uint32_t)ldexpf(vv[k], shift);
+          lsum += wv[k];
+        }
+      } else {
+#pragma unroll
+        for (int k = 0; k < PER; ++k) {
+          wv[k] = (k < nrows) ? (uint32_t)ldexpf(vv[k], shift) : 0u;
+          lsum += wv[k];
+        }
       }
       const uint64_t incl = wave_inclusive_scan<uint64_t>(lsum);
       Tw = __shfl(incl, kWave - 1, kWave);  // = C[d_in - 1]
@@ -618,14 +627,23 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
 #pragma unroll
     for (int k = 0; k < PER; ++k) cv[k] = k < nrows ? cnt[i0 + k] : 0u;
   }
+  // full rows with PER even: every lane's run starts on an even row, so row i0 + k has the
+  // parity of k (known at compile time)
+  const bool even_runs = full && PER % 2 == 0;
+  const auto odd_static = [](int k) { return (k & 1) != 0; };
+  const auto odd_lane = [&](int k) { return ((i0 + k) & 1) != 0; };
   int ne = 0, no = 0;
+  auto count = [&](auto odd) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    if (cv[k] != 0u) {
-      if ((i0 + k) & 1) ++no;
-      else ++ne;
+    for (int k = 0; k < PER; ++k) {
+      if (cv[k] != 0u) {
+        if (odd(k)) ++no;
+        else ++ne;
+      }
     }
-  }
+  };
+  if (even_runs) count(odd_static);
+  else count(odd_lane);
   const int cnt2 = ne | (no << 16);  // both counts <= d_in < 2^16
   const int incl2 = (int)wave_inclusive_scan<uint32_t>((uint32_t)cnt2);
   const int tot2 = __builtin_amdgcn_readlane(incl2, kWave - 1);
@@ -633,16 +651,20 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   int pe = (incl2 - cnt2) & 0xffff;
   int po = NE + ((incl2 - cnt2) >> 16);
   wave_lds_sync();  // every lane has its counts before the records overwrite them
+  auto records = [&](auto odd) {
 #pragma unroll
-  for (int k = 0; k < PER; ++k) {
-    const uint32_t c = cv[k];
-    if (c) {
-      const int at = ((i0 + k) & 1) ? po++ : pe++;
-      cnt[at] = (uint32_t)(i0 + k) | (c << 16);
-      rec_x[at] = xv[k];
-      if constexpr (!TABLE) rec_w[at] = wv[k];
+    for (int k = 0; k < PER; ++k) {
+      const uint32_t c = cv[k];
+      if (c) {
+        const int at = odd(k) ? po++ : pe++;
+        cnt[at] = (uint32_t)(i0 + k) | (c << 16);
+        if constexpr (TABLE) rec_x[at] = xv[k];
+        else rec_xw[at] = make_uint2(__float_as_uint(xv[k]), wv[k]);
+      }
     }
-  }
+  };
+  if (even_runs) records(odd_static);
+  else records(odd_lane);
   wave_lds_sync();
   const int nepad = (NE + 1) & ~1, nopad = (NO + 1) & ~1;
   uint2* lst = p.list + tok * list_stride(d_in);
@@ -651,10 +673,16 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
     const uint32_t e = cnt[q];
     const int row = (int)(e & 0xffffu);
     const uint32_t c = e >> 16;
-    const float x = rec_x[q];
+    float x;
     uint32_t w;
-    if constexpr (TABLE) w = (uint32_t)(C[row] - (row > 0 ? C[row - 1] : 0ull));
-    else w = rec_w[q];
+    if constexpr (TABLE) {
+      x = rec_x[q];
+      w = (uint32_t)(C[row] - (row > 0 ? C[row - 1] : 0ull));
+    } else {
+      const uint2 xw = rec_xw[q];
+      x = __uint_as_float(xw.x);
+      w = xw.y;
+    }
     const float coef = (float)(((double)c * (double)x * (double)Tw) / ((double)r * (double)w));
     lst[q < NE ? q : q + (nepad - NE)] = make_uint2((uint32_t)(row * rb), __float_as_uint(coef));
   }
