@@ -673,7 +673,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const int nvis = tile_count(c);  // <= NT (the launch checks the padded length)
+  // two K tiles in flight: the work per tile before its buffer's barrier is short
   TileRegs kr = tile_load<BF>(Kb, c.d_out, 0, c.n, c.tid);
+  TileRegs kr2 = tile_load<BF>(Kb, c.d_out, tile_at(c, min(1, nvis - 1)) * kTile, c.n, c.tid);
   QFrag<BF> qf;
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
   const RowQ rq = row_queries<BAND>(c);
@@ -690,7 +692,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       T* buf = Ks[t & 1];
       tile_store<BF>(kr, buf, c.tid);
       lds_barrier();
-      kr = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 1, nvis - 1)) * kTile, c.n, c.tid);
+      kr = kr2;
+      kr2 = tile_load<BF>(Kb, c.d_out, tile_at(c, min(t + 2, nvis - 1)) * kTile, c.n, c.tid);
       score_tile_qk(acc[t], buf, qf, c.r16, c.g);
       const int lim = c.len - kt * kTile;
       if (BAND || lim < kTile) mask_tile_q<BAND>(acc[t], c, rq, kt, lim, -INFINITY);  // tile-uniform

@@ -554,6 +554,17 @@ constexpr int kSatTokens = 64;   // tokens per block
 constexpr int kSatCols = 128;    // columns per block
 constexpr int kSatThreads = 256;
 
+// The block's unit of the (token tile, column block) grid, column blocks fastest. Workgroups
+// go to the eight XCDs in turn (block b to XCD b mod 8), so units are dealt out in one
+// contiguous run per XCD: the column blocks of a token tile then share that XCD's L2 and
+// its x rows are fetched from memory once rather than by several XCDs. A bijection of
+// [0, gridDim.x).
+__device__ __forceinline__ int xcd_run_unit() {
+  const int nb = (int)gridDim.x, per = nb / 8, extra = nb % 8;
+  const int x = (int)blockIdx.x % 8, k = (int)blockIdx.x / 8;
+  return x * per + min(x, extra) + k;
+}
+
 template <int BF, bool VEC>
 __global__ __launch_bounds__(kSatThreads) void k_saturated(FwdParams p) {
   using T = typename Elem<BF>::T;
@@ -563,7 +574,8 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated(FwdParams p) {
   __shared__ int satl[kSatTokens];
   __shared__ int nsat_s;
   const int ncb = p.d_out / kSatCols;
-  const int cb = blockIdx.x % ncb, tb = blockIdx.x / ncb;
+  const int u = xcd_run_unit();
+  const int cb = u % ncb, tb = u / ncb;
   const int64_t t0 = (int64_t)tb * kSatTokens;
   const int64_t ntok = (int64_t)p.B * p.n;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -695,7 +707,8 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
   __shared__ int nsat_s;
   __shared__ __align__(16) uint4 stage[ST * TILES * 64];
   const int ncb = p.d_out / COLS;
-  const int cb = blockIdx.x % ncb, tb = blockIdx.x / ncb;
+  const int u = xcd_run_unit();
+  const int cb = u % ncb, tb = u / ncb;
   const int64_t t0 = (int64_t)tb * TOK;
   const int64_t ntok = (int64_t)p.B * p.n;
   const int tid = threadIdx.x, lane = tid & 63;
