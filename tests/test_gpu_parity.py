@@ -374,11 +374,14 @@ def test_window_streaming_ragged(dev, dtype, window, lens):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("n,lens,window", [(300, (300, 181), 0), (600, (600, 531), 0), (600, (600, 77), 128)])
+@pytest.mark.parametrize("n,lens,window", [(300, (300, 181), 0), (600, (600, 531), 0), (600, (600, 77), 128),
+                                           (449, (449, 449), 0), (577, (577, 320), 0)])
 def test_score_pass_variants_ragged(dev, dtype, n, lens, window):
     # n = 300: the one-sweep score pass that keeps every score in registers (up to 8 key
     # tiles); n = 600: the two-sweep streaming score pass (its online row sum and its
-    # column max), with full attention and with a window; ragged rows
+    # column max), with full attention and with a window; ragged rows. n = 449 and 577 end
+    # with a key tile that holds one valid row, so the tile loads' range check covers all
+    # but the first row of that tile (one-sweep and streaming kernels, both passes)
     L = wl.make_layer(2, n, 128, 4, dtype, data_seed=9, lens=np.array(lens), q_scale=2.5,
                       token_scale_sigma=0.5, window=window)
     amb, n_tok = _full_check(L, dev, 0.4, seed=5)
