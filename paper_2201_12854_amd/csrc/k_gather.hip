@@ -374,6 +374,24 @@ __device__ void sampled_item(const FwdParams& p, const float* Ws, const uint32_t
   if (valid) store_h4<BF>(p, tk * p.d_out + c0 + 4 * v, acc[0]);
 }
 
+// The block's (slice, token range). Workgroups go to the eight XCDs in turn (block b to XCD
+// b mod 8). With the slices in four groups and the token ranges in two, XCD x takes slice
+// group x mod 4 of range group x / 4: every block still has one slice of one range, but an
+// XCD's L2 now serves the lists and saturated x rows of half the tokens (read by four XCDs
+// instead of eight) and a quarter of W_v (read by two), which about halves the kernel's
+// fetch from memory. Other grid shapes keep slice = b mod nslices.
+__device__ __forceinline__ void gather_block_unit(const FwdParams& p, int nslices, int& slice, int& range) {
+  const int b = (int)blockIdx.x;
+  if (nslices % 4 == 0 && p.gather_bps % 2 == 0 && (int)gridDim.x == nslices * p.gather_bps) {
+    const int x = b % 8, k = b / 8, sq = nslices / 4;
+    slice = (x % 4) * sq + k % sq;
+    range = (x / 4) * (p.gather_bps / 2) + k / sq;
+  } else {
+    slice = b % nslices;
+    range = b / nslices;
+  }
+}
+
 template <int BF, int WC, bool VEC, bool LDSB>
 __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   constexpr int RB = WC * 4;   // bytes per slice row in LDS
@@ -383,7 +401,8 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   unsigned char* smem = smem_raw + ((128u - (lds_addr(smem_raw) & 127u)) & 127u);
   const int d_in = p.d_in, d_out = p.d_out;
   const int nslices = d_out / WC;
-  const int slice = blockIdx.x % nslices, bis = blockIdx.x / nslices;
+  int slice, bis;
+  gather_block_unit(p, nslices, slice, bis);
   const int c0 = slice * WC;
   const int tid = threadIdx.x, lane = tid & 63;
   const int64_t ntok = (int64_t)p.B * p.n;
