@@ -306,7 +306,7 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
   const int d_in = p.d_in;
   uint64_t t[W];
   int lo[W], wt[W], kk[W];
-  const uint64_t* Cw[W];
+  uint32_t a[W], a0[W];  // LDS byte addresses: the search position, the token's C
 #pragma unroll
   for (int u = 0; u < W; ++u) {
     const int d = min(d0 + u * 64 * NW, D - 1);  // clamped: only d < D is counted
@@ -318,19 +318,15 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
     const u32x4 o = philox4x32_10(u32x4{(uint32_t)kk[u], (uint32_t)I.j[w], (uint32_t)I.b[w], 0u}, p.seed_lo,
                                   p.seed_hi);
     t[u] = __umul64hi((uint64_t)o.x | ((uint64_t)o.y << 32), I.T[w]);  // in [0, T)
-    Cw[u] = reinterpret_cast<const uint64_t*>(smem + c_off(d_in, TABLE, w));
+    a0[u] = lds_addr_u64(reinterpret_cast<const uint64_t*>(smem + c_off(d_in, TABLE, w)));
   }
   // s = #{i : C_i <= t} (C is non-decreasing and C[d_in-1] = T > t): a halving search
   // whose length sequence is the same for every lane (uniform), on LDS byte addresses
   // biased by -8 so that one add gives both the probe address and the candidate base.
   // Per step: add, 64-bit LDS read, compare, select. Step-major over the W draws so that
   // their LDS reads are in flight together.
-  uint32_t a[W], a0[W];
 #pragma unroll
-  for (int u = 0; u < W; ++u) {
-    a0[u] = lds_addr_u64(Cw[u]);
-    a[u] = a0[u] - 8;  // address of C[base - 1], base = 0
-  }
+  for (int u = 0; u < W; ++u) a[u] = a0[u] - 8;  // address of C[base - 1], base = 0
   for (int len = d_in; len > 1;) {
     const int half = len >> 1;
 #pragma unroll
@@ -355,7 +351,8 @@ __device__ __forceinline__ void draw_batch(const FwdParams& p, const TokInfo& I,
       const int64_t o2 = tok * d_in + kk[u];
       if (p.idx_out) p.idx_out[o2] = lo[u];
       if (p.coef_out) {
-        const uint64_t ws = Cw[u][lo[u]] - (lo[u] > 0 ? Cw[u][lo[u] - 1] : 0ull);
+        const uint64_t* Cw = reinterpret_cast<const uint64_t*>(smem + c_off(d_in, TABLE, w));
+        const uint64_t ws = Cw[lo[u]] - (lo[u] > 0 ? Cw[lo[u] - 1] : 0ull);
         const double xs = p.bf16 ? (double)load_f32(static_cast<const uint16_t*>(p.X) + tok * d_in, lo[u])
                                  : (double)load_f32(static_cast<const float*>(p.X) + tok * d_in, lo[u]);
         p.coef_out[o2] = (float)((xs * (double)I.T[w]) / ((double)I.r[w] * (double)ws));
