@@ -410,11 +410,16 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
   // once (slots past the end re-read the last partial and count as 0)
   const bool median_rule = p.importance == 2;
   const int nparts = median_rule ? 1 : p.nparts;  // the median rule: one value, from k_colmedian
+  // partial i of the token (clamped to the last): a 32-bit byte offset from the wave-uniform
+  // base (nparts < 2^24), so the address needs no 64-bit arithmetic per lane
+  auto part_at = [&](int i) {
+    return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(part) + (uint32_t)min(i, nparts - 1) * 4u);
+  };
   float pv[8];
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     const int t = lane + u * kWave;
-    const float v = part[min(t, nparts - 1)];
+    const float v = part_at(t);
     pv[u] = t < nparts ? v : 0.f;
   }
   const int per = (d_in + kWave - 1) / kWave;
@@ -467,7 +472,7 @@ __global__ __launch_bounds__(64 * NW) void k_sample(FwdParams p) {
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int t = t0 + u * kWave;
-      const float v = part[min(t, nparts - 1)];
+      const float v = part_at(t);
       pv[u] = t < nparts ? v : 0.f;
     }
 #pragma unroll
