@@ -425,7 +425,8 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
 
   // ---- the slice of W_v, as float32, into LDS, then two zero rows: 16-byte global loads,
   // four per thread in flight. The first four are issued now and stored after the first
-  // pass has classified its tokens, so that the classification overlaps their latency.
+  // pass has classified and counted its tokens, so that the classification overlaps their
+  // latency (and a block without work never stores them).
   using TW = typename Elem<BF>::T;
   constexpr int CE = BF ? 8 : 4;  // elements per 16-byte chunk
   constexpr int CPR = WC / CE;    // chunks per slice row
@@ -493,7 +494,33 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   if (tid < kNumCtr) ctr[tid] = 0;
   __syncthreads();  // the counters are clear
   MCA_CLASSIFY(t_begin, r_first, u_first)
-  // the slice into LDS while the first pass is being sorted (published by the barriers below)
+
+  // the classified pass's key offsets: every key's first slot in the order, longest first
+  auto offsets = [&]() {
+    __syncthreads();
+    if (tid < 64) {  // one wave; lane l: keys 95 - 2l, 94 - 2l
+      static_assert(kNumKeys == 96, "two keys per lane of one wave");
+      const int kh = kNumKeys - 1 - 2 * tid, kl = kh - 1;
+      const int ch = kl >= 0 ? ctr[2 + kh] : 0, cl = kl >= 0 ? ctr[2 + kl] : 0;
+      const int incl = (int)wave_inclusive_scan<uint32_t>((uint32_t)(ch + cl));
+      if (kl >= 0) {
+        ctr[kCtrOff + kh] = incl - ch - cl;
+        ctr[kCtrOff + kl] = incl - cl;
+      }
+      if (tid == 63) ctr[kCtrOff + kNumKeys] = incl;
+    }
+    __syncthreads();
+  };
+  if constexpr (!LDSB) {
+    // saturated tokens go to their own kernel: a block whose tokens fit one pass and make no
+    // work item (every token saturated, or without draws) has nothing to write and stops
+    // before filling the slice (block-uniform: every thread reads the same counts). With
+    // LDSB the saturated tokens are encoded here and a block almost always has work.
+    offsets();
+    if (ctr[0] == 0 && ctr[kCtrOff + kNumKeys] == 0 && t_begin + kChunk >= t_end) return;
+  }
+  // the slice into LDS (its first loads were issued before the classification), published
+  // by the barrier after the first pass's order
   MCA_SLICE_STORE(tid)
   if constexpr (LDSB) {
     if (tid < nfrag) Bl[tid] = fu0;
@@ -506,19 +533,7 @@ __global__ __launch_bounds__(kThreads) void k_gather(FwdParams p) {
   }
 
   for (int64_t t0 = t_begin;;) {
-    __syncthreads();
-    if (tid < 64) {  // one wave: offset of every key, longest first; lane l: keys 95 - 2l, 94 - 2l
-      static_assert(kNumKeys == 96, "two keys per lane of one wave");
-      const int kh = kNumKeys - 1 - 2 * tid, kl = kh - 1;
-      const int ch = kl >= 0 ? ctr[2 + kh] : 0, cl = kl >= 0 ? ctr[2 + kl] : 0;
-      const int incl = (int)wave_inclusive_scan<uint32_t>((uint32_t)(ch + cl));
-      if (kl >= 0) {
-        ctr[kCtrOff + kh] = incl - ch - cl;
-        ctr[kCtrOff + kl] = incl - cl;
-      }
-      if (tid == 63) ctr[kCtrOff + kNumKeys] = incl;
-    }
-    __syncthreads();
+    if (LDSB || t0 != t_begin) offsets();  // block-uniform
     if (key >= 0) order[ctr[kCtrOff + key] + rank] = ent;
     __syncthreads();
     const int nsat = ctr[0];
