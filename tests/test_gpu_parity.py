@@ -389,6 +389,17 @@ def test_score_pass_variants_ragged(dev, dtype, n, lens, window):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_streaming_passes_widest_rows(dev, dtype):
+    # 32 heads (d_out 2048, the widest row the library takes) with rows of 600 keys, one of
+    # them ragged: both streaming passes load their key and H~ tiles through descriptors
+    # whose row pitch is the largest allowed
+    L = wl.make_layer(1, 600, 128, 32, dtype, data_seed=21, lens=np.array([537]), q_scale=2.0,
+                      token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=9)
+    assert n_tok > 0
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("bump", [20.0, 30.0, 40.0, 100.0])
 def test_streaming_score_pass_raised_reference(dev, dtype, bump):
     # a few shared keys with a large logit bump (20 is about 29 in log2 units) at random
