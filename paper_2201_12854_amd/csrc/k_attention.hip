@@ -846,6 +846,14 @@ __device__ __forceinline__ BlockCtx block_ctx_q(const FwdParams& p) {
 }
 
 // The window of query q (klo .. klo + kspan, and key 0), as block_ctx sets it for c.q.
+// Under a local window: whether every key of tile kt is attended by every query q0 .. q0 +
+// nq - 1 (then the tile needs no mask): the keys are below len and within half of each of
+// those queries (query 0 attends every key below len). Wave-uniform arguments.
+__device__ __forceinline__ bool band_tile_inside(const BlockCtx& c, int kt, int q0, int nq) {
+  const int k0 = kt * kTile, k1 = k0 + kTile - 1;
+  return k1 < c.len && k0 >= q0 + nq - 1 - c.half && k1 <= max(q0, 1) + c.half;
+}
+
 __device__ __forceinline__ void query_window(const BlockCtx& c, int q, int& klo, int& kspan) {
   int lo = q == 0 ? 0 : max(0, q - c.half);
   int hi = q == 0 ? c.len - 1 : min(c.len - 1, q + c.half);
@@ -947,6 +955,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((BF &&
   constexpr int SV = BF ? kStrideBfWide : kStrideF;  // H~ tiles: unpermuted rows
   __shared__ __align__(16) T Vs[2][kTile * SV];
   BlockCtx c = block_ctx_q<QB>(p);
+  const int qw = __builtin_amdgcn_readfirstlane(c.qt * QB + c.wave * (QB / 4));  // the wave's first query
   const int64_t off = (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Qb = static_cast<const T*>(p.Q) + off;
   const T* Kb = static_cast<const T*>(p.K) + off;
@@ -984,7 +993,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu((BF &&
   auto step = [&](f32x4_t cur[MT][4], f32x4_t nxt[MT][4], int t) {
     const int kt = tile_at(c, t);
     const int lim = c.len - kt * kTile;
-    if (__builtin_expect(BAND || lim < kTile, 0)) {  // tile-uniform: masked scores give probability 0
+    // tile-uniform: masked scores give probability 0; under a window, tiles that every query
+    // of the wave attends whole need no mask
+    if (__builtin_expect(BAND ? !band_tile_inside(c, kt, qw, QB / 4) : lim < kTile, 0)) {
 #pragma unroll
       for (int m = 0; m < MT; ++m) {
         c.klo = klo[m];
@@ -1092,7 +1103,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   const BlockCtx c = block_ctx_q<128>(p);
   const T* Qb = static_cast<const T*>(p.Q) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
   const T* Kb = static_cast<const T*>(p.K) + (int64_t)c.b * c.n * c.d_out + c.h * kDHead;
-  const int qw = c.qt * 128 + c.wave * 32;  // the wave's first query
+  const int qw = __builtin_amdgcn_readfirstlane(c.qt * 128 + c.wave * 32);  // the wave's first query
   QFrag<BF> qf[2];
 #pragma unroll
   for (int m = 0; m < 2; ++m) load_qfrag(qf[m], Qb + (int64_t)min(qw + 16 * m + c.r16, c.n - 1) * c.d_out, c.g);
@@ -1143,7 +1154,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     auto step = [&](f32x4_t cur[2][4], f32x4_t nxt[2][4], int t) {
       const int kt = tile_at(c, t);
       const int lim = c.len - kt * kTile;
-      if (BAND || lim < kTile) mask(cur, kt, lim);  // tile-uniform
+      if (BAND ? !band_tile_inside(c, kt, qw, 32) : lim < kTile) mask(cur, kt, lim);  // tile-uniform
       T* buf = Ks[(t + 1) & 1];
       tile_store<BF>(kr, buf, c.tid);
       lds_barrier();
@@ -1178,7 +1189,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   sweep(
       zero2,
       [&](f32x4_t acc[2][4]) {
-        if (BAND || c.len < kTile) mask(acc, 0, c.len);
+        if (BAND ? !band_tile_inside(c, 0, qw, 32) : c.len < kTile) mask(acc, 0, c.len);
 #pragma unroll
         for (int k = 0; k < 8; ++k) {
           const int m = k >> 2, i = k & 3;
