@@ -388,6 +388,19 @@ def test_score_pass_variants_ragged(dev, dtype, n, lens, window):
     assert n_tok > 0
 
 
+@pytest.mark.parametrize("n,window,lens", [(520, 126, (520, 301)), (777, 256, (700, 777)), (640, 190, (640, 65)),
+                                            (900, 512, (899, 450))])
+def test_window_streaming_shapes(dev, n, window, lens):
+    # streaming passes under windows of several widths: key tiles that every query of a
+    # wave attends whole skip their mask, the others are masked; ragged rows move the
+    # boundary of "whole" (keys below len) and windows wider than 2 x 64 + 32 leave
+    # interior tiles on both sides of the diagonal
+    L = wl.make_layer(2, n, 96, 4, "bf16", data_seed=31 + n, lens=np.array(lens), q_scale=2.0,
+                      token_scale_sigma=0.5, window=window)
+    amb, n_tok = _full_check(L, dev, 0.4, seed=11)
+    assert n_tok > 0
+
+
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 def test_streaming_passes_widest_rows(dev, dtype):
     # 32 heads (d_out 2048, the widest row the library takes) with rows of 600 keys, one of
