@@ -680,11 +680,28 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
   load_qfrag(qf, Qb + (int64_t)min(c.q, c.n - 1) * c.d_out, c.g);
   const RowQ rq = row_queries<BAND>(c);
 
-  // scores in registers (masked keys -inf), the lane's max dot product per query; the t-th
-  // visited tile goes through K buffer t & 1 (the barrier after its store also orders the
-  // reads of tile t - 2, consumed by that tile's MFMAs, before it)
+  // scores in registers (masked keys -inf); the t-th visited tile goes through K buffer
+  // t & 1 (the barrier after its store also orders the reads of tile t - 2, consumed by
+  // that tile's MFMAs, before it). The row sums are software pipelined: once the MFMAs of
+  // tile t are issued, the terms of tile t - 1 are added, under a reference M that is the
+  // row's largest logit in tile 0 (finite: key 0 is attended by every query). A sum of
+  // positive terms keeps its relative precision when terms exceed 1; only a logit more than
+  // about 127 log2 units above M overflows it, and then (or with non-finite scores) the
+  // wave takes each row's largest logit as M and sums again (a wave-uniform branch).
   f32x4_t acc[NT][4];
-  float dmax[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
+  float M[4], Ls[4] = {0.f, 0.f, 0.f, 0.f};
+  auto tile0_ref = [&]() {
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      M[i] = __fmul_rn(row16_max_sel(vmax(vmax3(acc[0][0][i], acc[0][1][i], acc[0][2][i]), acc[0][3][i])),
+                       kLog2eOver8);
+  };
+  auto add_terms = [&](const f32x4_t a[4]) {
+#pragma unroll
+    for (int s = 0; s < 4; ++s)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) Ls[i] += exp2_fast(__fmaf_rn(a[s][i], kLog2eOver8, -M[i]));
+  };
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     if (t < nvis) {
@@ -697,30 +714,47 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
       score_tile_qk(acc[t], buf, qf, c.r16, c.g);
       const int lim = c.len - kt * kTile;
       if (BAND || lim < kTile) mask_tile_q<BAND>(acc[t], c, rq, kt, lim, -INFINITY);  // tile-uniform
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        dmax[i] = vmax3(vmax3(dmax[i], acc[t][0][i], acc[t][1][i]), acc[t][2][i], acc[t][3][i]);
+      if (t > 0) {
+        if (t == 1) tile0_ref();
+        add_terms(acc[t - 1]);
+      }
     }
   }
-  // row statistics as in the resident variant
-  float M[4], Ls[4], cq[4], cc[4];
+  if (nvis == 1) tile0_ref();
+#pragma unroll
+  for (int t = 0; t < NT; ++t)
+    if (t == nvis - 1) add_terms(acc[t]);
+  float Lr[4], cq[4], cc[4];
+  bool bad = false;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    M[i] = __fmul_rn(row16_max_sel(dmax[i]), kLog2eOver8);  // finite: key 0 is attended
-    Ls[i] = 0.f;
+    Lr[i] = row16_sum(Ls[i]);
+    bad |= !(Lr[i] < INFINITY);
   }
+  if (__any(bad)) {
+    float dmax[4] = {-INFINITY, -INFINITY, -INFINITY, -INFINITY};
 #pragma unroll
-  for (int t = 0; t < NT; ++t) {
-    if (t < nvis) {
+    for (int t = 0; t < NT; ++t) {
+      if (t < nvis) {
 #pragma unroll
-      for (int s = 0; s < 4; ++s)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) Ls[i] += exp2_fast(__fmaf_rn(acc[t][s][i], kLog2eOver8, -M[i]));
+        for (int i = 0; i < 4; ++i)
+          dmax[i] = vmax3(vmax3(dmax[i], acc[t][0][i], acc[t][1][i]), acc[t][2][i], acc[t][3][i]);
+      }
     }
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      M[i] = __fmul_rn(row16_max_sel(dmax[i]), kLog2eOver8);
+      Ls[i] = 0.f;
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t)
+      if (t < nvis) add_terms(acc[t]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) Lr[i] = row16_sum(Ls[i]);
   }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    cq[i] = M[i] + __builtin_amdgcn_logf(row16_sum(Ls[i]));
+    cq[i] = M[i] + __builtin_amdgcn_logf(Lr[i]);
     cc[i] = colmax_offset<BAND>(c, rq, i, cq[i]);
   }
   store_row_c(p, c, cq);

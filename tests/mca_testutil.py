@@ -41,8 +41,11 @@ TOL_H = 1e-5
 #      range) + eps_exp (each exp2) + gamma_{n/16 + 6} (a lane adds its keys in sequence,
 #      then four butterfly levels combine 16 lanes), plus, in the streaming kernel, one
 #      rescale per visited key tile at most (eps_exp + u each, arguments summing to at
-#      most R) and four DPP combination levels; log2 L within 2u max(1, log2 L); the add
-#      M + log2 L rounds by |c| u / 2
+#      most R) and four DPP combination levels; log2 L within 2u max(1, log2 L), where L is
+#      the sum under the kernel's reference M (the row's largest logit in its first key
+#      tile, or a larger logit of the row once raised), so log2 L is at most the oracle's
+#      log2 of the sum under the row max plus (row max - largest logit of tile 0); the
+#      add M + log2 L rounds by |c| u / 2
 #   t: the fma rounds by |t| u / 2
 #   m: exp2 of the maximum: eps_exp; the maximum of perturbed values moves by at most
 #      the largest perturbation among the pairs that can be the maximum
@@ -93,6 +96,7 @@ def colmax_tolerance(L, importance="max", window=None):
             Ls = np.exp2(z - zmax[:, None]).sum(axis=1)
             c = zmax + np.log2(Ls)
             R = zmax - np.where(att, z, np.inf).min(axis=1)
+            lgL = np.log2(Ls) + (zmax - z[:, :64].max(axis=1))  # log2 of the sum under tile 0's max
             dL = ln2 * (U32 / 2) * (R + (16.0 if streaming else 0.0)) + EPS_EXP + _gamma(-(-n // 16) + 6)
             if streaming:
                 dL = dL + ntiles * (EPS_EXP + U32) + ln2 * (U32 / 2) * R + 4 * (EPS_EXP + 1.5 * U32) \
@@ -101,7 +105,7 @@ def colmax_tolerance(L, importance="max", window=None):
             P = np.exp2(z - c[:, None])  # the row's probabilities (0 off the pattern)
             dzmax = dz.max(axis=1)
             Ec = (P * dz).sum(axis=1) + (ln2 / 2) * dzmax ** 2 + dL / ln2 * (1 + 1e-6) \
-                + 2 * U32 * np.maximum(1.0, np.log2(Ls)) + np.abs(c) * U32 / 2
+                + 2 * U32 * np.maximum(1.0, lgL) + np.abs(c) * U32 / 2
             t = z - c[:, None]
             if window > 0:  # t = log2(|S_i| A[i, k]) against c~ - log2 |S_i|
                 lg = np.log2(nk)

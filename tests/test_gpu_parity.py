@@ -414,19 +414,23 @@ def test_streaming_passes_widest_rows(dev, dtype):
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
 @pytest.mark.parametrize("bump", [20.0, 30.0, 40.0, 100.0])
-def test_streaming_score_pass_raised_reference(dev, dtype, bump):
+@pytest.mark.parametrize("n", [700, 480, 250])
+def test_score_pass_raised_reference(dev, dtype, bump, n):
     # a few shared keys with a large logit bump (20 is about 29 in log2 units) at random
-    # places in rows of 700 keys: a query that meets one after its first tile adds terms far
-    # above its reference logit (its largest logit in tile 0). At bump 100 (144 log2 units)
-    # some of them pass the 127 log2 units a float32 term can take, so the streaming score
-    # pass must notice the overflow and redo its first sweep with a raised reference and
-    # rescaled sums. The large logits also stretch the float32 error of the column max (the
-    # row normaliser reaches |c| near 60 at bump 40), which the per-key bound must still
-    # cover.
-    L = wl.make_layer(2, 700, 128, 4, dtype, data_seed=12, lens=np.array([700, 555]), salient_keys=6,
+    # places in the rows: a query that meets one after its first tile adds terms far above
+    # its reference logit (its largest logit in tile 0). At bump 100 (144 log2 units) some
+    # of them pass the 127 log2 units a float32 term can take, so a score pass that sums
+    # under tile 0's largest logit must notice the overflow: the streaming kernel (n = 700)
+    # redoes its first sweep with a raised reference and rescaled sums, the one-sweep kernel
+    # that streams up to 8 key tiles (n = 480) sums its registers again under the row max.
+    # The kernel with every key tile resident (n = 250) takes the row max first. The large
+    # logits also stretch the float32 error of the column max (the row normaliser reaches
+    # |c| near 60 at bump 40), which the per-key bound must still cover.
+    lens = np.array([n, (n * 4) // 5 - 5])
+    L = wl.make_layer(2, n, 128, 4, dtype, data_seed=12, lens=lens, salient_keys=6,
                       salient_bump=bump, token_scale_sigma=0.5)
-    q = L.Q.astype(np.float64).reshape(2, 700, 4, 64)
-    k = L.K.astype(np.float64).reshape(2, 700, 4, 64)
+    q = L.Q.astype(np.float64).reshape(2, n, 4, 64)
+    k = L.K.astype(np.float64).reshape(2, n, 4, 64)
     lg = np.einsum("bqhd,bkhd->bhqk", q, k) * (np.log2(np.e) / 8)  # logits, log2 units
     if bump == 100.0:  # the input does reach the overflow: some query's logit lies > 127 above tile 0's
         assert np.any(lg.max(axis=3) - lg[..., :64].max(axis=3) > 127)
