@@ -512,6 +512,69 @@ def cpu_baseline(L, alpha, seed, seconds):
             "host": info}
 
 
+def issue_probe(rounds=20000):
+    """Issue costs on this GPU from libmca_probe.so (independent instruction chains per wave,
+    clock stamps per wave, spans taken over each workgroup's waves): cycles per wave64
+    instruction per SIMD for v_fma_f32, v_exp_f32, v_max3_f32 and the 16x16x32 bf16 MFMA with
+    1, 2 and 4 waves per SIMD, the chip-wide MFMA rate, and how far VALU work and MFMAs
+    overlap: in every wave (64 fma or 64 exp with 16 MFMAs per round) and split over the two
+    waves of a SIMD. Returns a dict."""
+    import ctypes
+
+    import torch
+
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "paper_2201_12854_amd", "libmca_probe.so")
+    if not os.path.exists(path):
+        raise SystemExit(f"{path} is missing: build it first (python -m paper_2201_12854_amd.build_lib)")
+    torch.cuda.init()
+    lib = ctypes.CDLL(path)
+    lib.mca_issue_probe.restype = ctypes.c_int
+    lib.mca_issue_probe.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_longlong),
+                                    ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
+    names = {0: "fma", 1: "exp", 2: "mfma", 3: "fma+mfma", 4: "fma|mfma", 5: "exp+mfma", 6: "exp|mfma", 7: "max3"}
+
+    def run(kind, w):
+        cap = 8192
+        buf = (ctypes.c_longlong * (4 * cap))()
+        nw = ctypes.c_int(0)
+        for _ in range(2):  # the first call warms the clocks up
+            rc = lib.mca_issue_probe(kind, w, rounds, buf, cap, ctypes.byref(nw))
+            if rc != 0:
+                raise SystemExit(f"mca_issue_probe({names[kind]}, {w}) failed with {rc}")
+        # [workgroup (one per CU)][wave][t0, t1, r0, r1]; spans from the first start to the
+        # last end over a workgroup's waves, so that waves which do not run side by side are
+        # not taken for overlap
+        st = np.frombuffer(buf, dtype=np.int64, count=4 * nw.value).reshape(-1, 4 * w, 4).astype(np.float64)
+        span_cyc = st[:, :, 1].max(axis=1) - st[:, :, 0].min(axis=1)
+        span_ns = (st[:, :, 3].max(axis=1) - st[:, :, 2].min(axis=1)) * 10.0
+        wave_cyc = st[:, :, 1] - st[:, :, 0]
+        chip_ns = (st[:, :, 3].max() - st[:, :, 2].min()) * 10.0
+        return {"span_cycles": float(np.median(span_cyc)), "clock_ghz": float(np.median(span_cyc / span_ns)),
+                "wave_share_of_span": float(np.median(wave_cyc.mean(axis=1) / span_cyc)), "chip_ns": float(chip_ns),
+                "waves": nw.value}
+
+    out = {"rounds": rounds, "cycles_per_instr_per_simd": {}, "clock_ghz": {}, "wave_share_of_span": {},
+           "mixed_cycles_per_round_per_simd": {}}
+    per_round = {0: 64, 1: 64, 2: 16, 7: 64}
+    for kind in (0, 1, 7, 2):
+        for w in (1, 2, 4):
+            r = run(kind, w)
+            key = f"{names[kind]}_w{w}"
+            out["cycles_per_instr_per_simd"][key] = r["span_cycles"] / (w * rounds * per_round[kind])
+            out["clock_ghz"][key] = r["clock_ghz"]
+            out["wave_share_of_span"][key] = r["wave_share_of_span"]
+            if kind == 2:
+                out[f"mfma_bf16_TFLOPs_w{w}"] = r["waves"] * rounds * 16 * 16384 / r["chip_ns"] / 1e3
+    # every wave runs 64 VALU and 16 MFMAs per round (w waves per SIMD), or the two halves of
+    # a SIMD's two waves do one each: cycles per SIMD for one round of each wave's work
+    for kind, ws in ((3, (1, 2, 4)), (5, (1, 2, 4)), (4, (2,)), (6, (2,))):
+        for w in ws:
+            r = run(kind, w)
+            out["mixed_cycles_per_round_per_simd"][f"{names[kind]}_w{w}"] = r["span_cycles"] / rounds
+            out["clock_ghz"][f"{names[kind]}_w{w}"] = r["clock_ghz"]
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -526,6 +589,8 @@ def main():
                     help="only time the MCA forward of one workload (for profiler runs; no JSON bench line)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="also run a plain copy of MIB MiB (for scaling rocprofv3 byte counters)")
+    ap.add_argument("--issue-probe", action="store_true",
+                    help="only measure VALU, exp2 and MFMA issue costs with libmca_probe.so (one JSON object)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): the multi-GPU layout is a design "
@@ -540,6 +605,9 @@ def main():
     if not torch.cuda.is_available():
         raise SystemExit("bench.py needs a HIP device")
     dev = torch.device("cuda:0")
+    if args.issue_probe:
+        print(json.dumps({"issue_probe": issue_probe()}), flush=True)
+        return
     if args.forward_only:
         L = wl.WORKLOADS[args.forward_only]()
         t = upload(L, dev)

@@ -1,9 +1,11 @@
-"""Build libmca.so (HIP kernels for gfx950 plus the C ABI) in the package directory.
+"""Build libmca.so (HIP kernels for gfx950 plus the C ABI) in the package directory,
+and beside it libmca_probe.so (issue-cost probes that back the roofline reasoning about
+the attention kernels; ``bench.py --issue-probe`` runs them, nothing else loads them).
 
 Usage: ``python -m paper_2201_12854_amd.build_lib`` or ``build()`` from Python.
 Compiles every source each time it is called (one hipcc per file, in parallel),
-links into ``paper_2201_12854_amd/libmca.so`` and replaces the old library
-atomically.
+links into ``paper_2201_12854_amd/libmca.so`` and ``libmca_probe.so`` and replaces
+the old libraries atomically.
 """
 from __future__ import annotations
 
@@ -18,9 +20,11 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build", "libmca")
 LIB = os.path.join(PKG, "libmca.so")
+PROBE_LIB = os.path.join(PKG, "libmca_probe.so")
 ARCH = "gfx950"
 
 SOURCES = ["k_attention.hip", "k_sample.hip", "k_gather.hip", "k_prepare.hip", "mca_api.cpp"]
+PROBE_SOURCES = ["issue_probe.hip"]
 
 CXXFLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -58,18 +62,24 @@ def _compile(src: str, verbose: bool) -> str:
     return obj
 
 
-def build(verbose: bool = False) -> str:
-    os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), SOURCES))
-    tmp = LIB + f".tmp{os.getpid()}"
+def _link(objs, lib: str, verbose: bool) -> None:
+    tmp = lib + f".tmp{os.getpid()}"
     cmd = [hipcc(), "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
-        raise RuntimeError("link of libmca.so failed:\n" + res.stdout + res.stderr)
-    os.replace(tmp, LIB)
+        raise RuntimeError(f"link of {os.path.basename(lib)} failed:\n" + res.stdout + res.stderr)
+    os.replace(tmp, lib)
+
+
+def build(verbose: bool = False) -> str:
+    os.makedirs(BUILD, exist_ok=True)
+    srcs = SOURCES + PROBE_SOURCES
+    with cf.ThreadPoolExecutor(max_workers=4) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
+    _link(objs[:len(SOURCES)], LIB, verbose)
+    _link(objs[len(SOURCES):], PROBE_LIB, verbose)
     return LIB
 
 

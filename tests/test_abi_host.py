@@ -211,3 +211,24 @@ def test_build_flags():
     i = flags.index("-packed-fp32-ops")
     assert flags[i - 3:i] == ["-Xclang", "-target-feature", "-Xclang"]
     assert "-amdgpu-mfma-vgpr-form" in flags
+
+
+def test_issue_probe_library_rejects_bad_arguments():
+    # the probe library (measurement support, include/mca_probe.h) loads without a GPU,
+    # exports its entry point, and rejects invalid arguments before any device work
+    path = os.path.join(ROOT, "paper_2201_12854_amd", "libmca_probe.so")
+    if not os.path.exists(path):
+        pytest.skip("libmca_probe.so not built")
+    lib = ctypes.CDLL(path)
+    f = lib.mca_issue_probe
+    f.restype = ctypes.c_int
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_longlong), ctypes.c_int,
+                  ctypes.POINTER(ctypes.c_int)]
+    buf = (ctypes.c_longlong * 16)()
+    nw = ctypes.c_int(-5)
+    for kind, w, rounds in [(8, 1, 10), (-1, 1, 10), (0, 3, 10), (0, 8, 10), (4, 1, 10), (6, 4, 10), (0, 1, 0),
+                            (2, 2, 1 << 21)]:
+        assert f(kind, w, rounds, buf, 4, ctypes.byref(nw)) == -1, (kind, w, rounds)
+    assert f(0, 1, 10, None, 4, ctypes.byref(nw)) == -1
+    assert f(0, 1, 10, buf, 4, None) == -1
+    assert nw.value == -5  # nothing written on rejection
