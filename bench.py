@@ -517,8 +517,8 @@ def issue_probe(rounds=20000):
     clock stamps per wave, spans taken over each workgroup's waves): cycles per wave64
     instruction per SIMD for v_fma_f32, v_exp_f32, v_max3_f32 and the 16x16x32 bf16 MFMA with
     1, 2 and 4 waves per SIMD, the chip-wide MFMA rate, and how far VALU work and MFMAs
-    overlap: in every wave (64 fma or 64 exp with 16 MFMAs per round) and split over the two
-    waves of a SIMD. Returns a dict."""
+    overlap: in every wave (64 fma or 64 exp with 16 MFMAs per round, 64 exp with 64 fma) and
+    split over the two waves of a SIMD. Returns a dict."""
     import ctypes
 
     import torch
@@ -531,7 +531,8 @@ def issue_probe(rounds=20000):
     lib.mca_issue_probe.restype = ctypes.c_int
     lib.mca_issue_probe.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.POINTER(ctypes.c_longlong),
                                     ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
-    names = {0: "fma", 1: "exp", 2: "mfma", 3: "fma+mfma", 4: "fma|mfma", 5: "exp+mfma", 6: "exp|mfma", 7: "max3"}
+    names = {0: "fma", 1: "exp", 2: "mfma", 3: "fma+mfma", 4: "fma|mfma", 5: "exp+mfma", 6: "exp|mfma", 7: "max3",
+             8: "exp+fma"}
 
     def run(kind, w):
         cap = 8192
@@ -567,7 +568,7 @@ def issue_probe(rounds=20000):
                 out[f"mfma_bf16_TFLOPs_w{w}"] = r["waves"] * rounds * 16 * 16384 / r["chip_ns"] / 1e3
     # every wave runs 64 VALU and 16 MFMAs per round (w waves per SIMD), or the two halves of
     # a SIMD's two waves do one each: cycles per SIMD for one round of each wave's work
-    for kind, ws in ((3, (1, 2, 4)), (5, (1, 2, 4)), (4, (2,)), (6, (2,))):
+    for kind, ws in ((3, (1, 2, 4)), (5, (1, 2, 4)), (8, (1, 2, 4)), (4, (2,)), (6, (2,))):
         for w in ws:
             r = run(kind, w)
             out["mixed_cycles_per_round_per_simd"][f"{names[kind]}_w{w}"] = r["span_cycles"] / rounds

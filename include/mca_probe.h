@@ -19,6 +19,7 @@ extern "C" {
  *                   5: kinds 1 and 2 in one wave
  *                   6: waves 0..3 of each workgroup run kind 1, waves 4..7 kind 2
  *                   7: 64 v_max3_f32 per round (eight independent chains)
+ *                   8: kind 1 and 64 v_fma_f32 (eight more chains) in one wave
  *   waves_per_simd  1, 2 or 4 (kinds 4 and 6: 2); the grid has one workgroup per CU of
  *                   256 * waves_per_simd threads
  *   rounds          1 .. 2^20

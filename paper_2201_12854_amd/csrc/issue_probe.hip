@@ -15,6 +15,7 @@
 //   5 exp+mfma  the 64 exp of kind 1 and the 16 mfma of kind 2 in one wave
 //   6 exp|mfma  waves 0..3 run kind 1, waves 4..7 kind 2 (as kind 4)
 //   7 max3  64 v_max3_f32 per round (eight independent chains of eight)
+//   8 exp+fma   the 64 exp of kind 1 and 64 fma (eight more chains) in one wave
 // One workgroup per CU: its dynamic LDS (kPadLds bytes, untouched) leaves no room for a
 // second. 256 w threads per workgroup put w waves on each of the CU's four SIMDs.
 #include <hip/hip_runtime.h>
@@ -28,7 +29,7 @@ namespace {
 typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 probe_bf16x8_t;
 typedef __attribute__((__vector_size__(4 * sizeof(float)))) float probe_f32x4_t;
 
-constexpr int kFma = 0, kExp = 1, kMfma = 2, kMix = 3, kSplit = 4, kExpMix = 5, kExpSplit = 6, kMax3 = 7;
+constexpr int kFma = 0, kExp = 1, kMfma = 2, kMix = 3, kSplit = 4, kExpMix = 5, kExpSplit = 6, kMax3 = 7, kExpFma = 8;
 constexpr int kPadLds = 96 * 1024;
 constexpr int kInputs = 128;  // floats of the input buffer
 
@@ -36,9 +37,12 @@ template <int KIND>
 __global__ __launch_bounds__(1024) void k_issue(const float* in, float* out, long long* stamps, int rounds) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const float x = in[lane], y = in[64 + lane];
-  float a[8];
+  float a[8], b[8];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) a[k] = x + (float)k;
+  for (int k = 0; k < 8; ++k) {
+    a[k] = x + (float)k;
+    b[k] = y + (float)k;
+  }
   probe_f32x4_t acc[8];
 #pragma unroll
   for (int k = 0; k < 8; ++k) acc[k] = probe_f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -46,7 +50,7 @@ __global__ __launch_bounds__(1024) void k_issue(const float* in, float* out, lon
   const probe_bf16x8_t A = __builtin_bit_cast(probe_bf16x8_t, make_uint4(xb, yb, xb, yb));
   const probe_bf16x8_t B = __builtin_bit_cast(probe_bf16x8_t, make_uint4(yb, xb, yb, xb));
   const bool do_fma = KIND == kFma || KIND == kMix || (KIND == kSplit && wave < 4);
-  const bool do_exp = KIND == kExp || KIND == kExpMix || (KIND == kExpSplit && wave < 4);
+  const bool do_exp = KIND == kExp || KIND == kExpMix || KIND == kExpFma || (KIND == kExpSplit && wave < 4);
   const bool do_mfma = KIND == kMfma || KIND == kMix || KIND == kExpMix || ((KIND == kSplit || KIND == kExpSplit) && wave >= 4);
 
   const long long t0 = (long long)__builtin_amdgcn_s_memtime();
@@ -57,6 +61,12 @@ __global__ __launch_bounds__(1024) void k_issue(const float* in, float* out, lon
       for (int j = 0; j < 8; ++j)
 #pragma unroll
         for (int k = 0; k < 8; ++k) a[k] = __builtin_amdgcn_exp2f(a[k]);
+    }
+    if (KIND == kExpFma) {
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int k = 0; k < 8; ++k) b[k] = fmaf(b[k], x, y);
     }
     if (KIND == kMax3) {
 #pragma unroll
@@ -82,7 +92,7 @@ __global__ __launch_bounds__(1024) void k_issue(const float* in, float* out, lon
 
   float s = 0.f;  // every result stays live
 #pragma unroll
-  for (int k = 0; k < 8; ++k) s += a[k] + acc[k][0] + acc[k][1] + acc[k][2] + acc[k][3];
+  for (int k = 0; k < 8; ++k) s += a[k] + b[k] + acc[k][0] + acc[k][1] + acc[k][2] + acc[k][3];
   out[(int64_t)blockIdx.x * blockDim.x + tid] = s;
   if (lane == 0) {
     long long* st = stamps + ((int64_t)blockIdx.x * (blockDim.x >> 6) + wave) * 4;
@@ -106,7 +116,7 @@ hipError_t launch_kind(dim3 grid, dim3 block, const float* in, float* out, long 
 // Runs one probe on the current device (arguments and results as declared in mca_probe.h).
 extern "C" int mca_issue_probe(int kind, int waves_per_simd, int rounds, long long* stamps, int max_waves,
                                int* nwaves) {
-  if (kind < 0 || kind > 7 || rounds < 1 || rounds > (1 << 20) || !stamps || !nwaves) return -1;
+  if (kind < 0 || kind > 8 || rounds < 1 || rounds > (1 << 20) || !stamps || !nwaves) return -1;
   if (waves_per_simd != 1 && waves_per_simd != 2 && waves_per_simd != 4) return -1;
   if ((kind == kSplit || kind == kExpSplit) && waves_per_simd != 2) return -1;
   int dev = 0, ncu = 0;
@@ -137,7 +147,8 @@ extern "C" int mca_issue_probe(int kind, int waves_per_simd, int rounds, long lo
       case kSplit: e = launch_kind<kSplit>(grid, block, in, out, st, rounds); break;
       case kExpMix: e = launch_kind<kExpMix>(grid, block, in, out, st, rounds); break;
       case kExpSplit: e = launch_kind<kExpSplit>(grid, block, in, out, st, rounds); break;
-      default: e = launch_kind<kMax3>(grid, block, in, out, st, rounds); break;
+      case kMax3: e = launch_kind<kMax3>(grid, block, in, out, st, rounds); break;
+      default: e = launch_kind<kExpFma>(grid, block, in, out, st, rounds); break;
     }
   }
   if (e == hipSuccess) e = hipDeviceSynchronize();

@@ -226,7 +226,7 @@ def test_issue_probe_library_rejects_bad_arguments():
                   ctypes.POINTER(ctypes.c_int)]
     buf = (ctypes.c_longlong * 16)()
     nw = ctypes.c_int(-5)
-    for kind, w, rounds in [(8, 1, 10), (-1, 1, 10), (0, 3, 10), (0, 8, 10), (4, 1, 10), (6, 4, 10), (0, 1, 0),
+    for kind, w, rounds in [(9, 1, 10), (-1, 1, 10), (0, 3, 10), (0, 8, 10), (4, 1, 10), (6, 4, 10), (0, 1, 0),
                             (2, 2, 1 << 21)]:
         assert f(kind, w, rounds, buf, 4, ctypes.byref(nw)) == -1, (kind, w, rounds)
     assert f(0, 1, 10, None, 4, ctypes.byref(nw)) == -1
