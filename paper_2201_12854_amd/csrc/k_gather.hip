@@ -687,16 +687,16 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated(FwdParams p) {
     }
 }
 
-// k_saturated_lds (16-byte x chunks): 32 NTW columns (256 with NTW = 8) and 32 MTW tokens
-// per block, a quarter of both per wave (2 x 2 waves: 16 MTW tokens x 16 NTW columns
-// each), the operands staged through LDS by direct global-to-LDS loads (16 bytes per lane,
-// no registers) with ST - 1 k steps in flight. Per k step the block stages its 2 MTW
-// 16-row A tiles and 2 NTW 16-column B tiles in fragment order (1 KB each; lane l's 16 bytes
-// at 16 l), and every wave reads its MTW A and NTW B fragments from there: with MTW = 4 a
-// wave's twelve fragment reads feed 32 MFMAs (MTW = 2: ten feed 16), so the LDS reads and
-// the loads into LDS per MFMA are what a 128 x 256 tile needs rather than a 64 x 256 one. A
-// chunk past the end of a row re-reads the row's last chunk: the prepared W_v^T is zero
-// there.
+// k_saturated_lds (16-byte x chunks): 16 WN NTW columns and 32 MTW tokens per block, 2 x WN
+// waves of 16 MTW tokens x 16 NTW columns each, the operands staged through LDS by direct
+// global-to-LDS loads (16 bytes per lane, no registers) with ST - 1 k steps in flight. Per k
+// step the block stages its 2 MTW 16-row A tiles and WN NTW 16-column B tiles in fragment
+// order (1 KB each; lane l's 16 bytes at 16 l), and every wave reads its MTW A and NTW B
+// fragments from there. bfloat16: 128 x 256 tiles in eight waves (MTW = NTW = 4, WN = 4),
+// two per SIMD, so that one wave's LDS reads and waits pass under the other's MFMAs (eight
+// fragment reads feed 16 MFMAs); float32: 64 x 256 tiles in four waves (MTW = 2, NTW = 8,
+// WN = 2: ten fragment reads feed 16). A chunk past the end of a row re-reads the row's
+// last chunk: the prepared W_v^T is zero there.
 constexpr int kSatStages = 3;
 
 // s_waitcnt for at most n outstanding vector memory operations (gfx9 encoding: vmcnt in
@@ -723,19 +723,20 @@ __device__ __forceinline__ void stage_barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <int BF, int NTW, int MTW, int ST>
-__global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
+template <int BF, int NTW, int MTW, int ST, int WN = 2>
+__global__ __launch_bounds__(128 * WN) void k_saturated_lds(FwdParams p) {
   using T = typename Elem<BF>::T;
   constexpr int E = BF ? 8 : 4;     // elements per 16 bytes
   constexpr int KS = BF ? 32 : 16;  // k per step
+  constexpr int WV = 2 * WN;        // waves: 2 along the tokens x WN along the columns
   constexpr int NA = 2 * MTW;       // A tiles per block (16 tokens each)
-  constexpr int NB = 2 * NTW;       // B tiles per block (16 columns each)
+  constexpr int NB = WN * NTW;      // B tiles per block (16 columns each)
   constexpr int TOK = 16 * NA;      // tokens per block
   constexpr int COLS = 16 * NB;     // columns per block
   constexpr int TILES = NA + NB;    // 1 KB tiles per step slot: the A tiles, then the B tiles
-  static_assert(NA % 4 == 0 && NB % 4 == 0, "every wave loads the same number of tiles");
+  static_assert(NA % WV == 0 && NB % WV == 0, "every wave loads the same number of tiles");
   static_assert(ST >= 2, "stages");
-  constexpr int kLoads = (NA + NB) / 4;  // direct loads per wave per step
+  constexpr int kLoads = (NA + NB) / WV;  // direct loads per wave per step
   constexpr int kSlot = TILES * 64 * 16;
   __shared__ int satl[TOK];
   __shared__ int nsat_s;
@@ -751,33 +752,33 @@ __global__ __launch_bounds__(kSatThreads) void k_saturated_lds(FwdParams p) {
   const int d_in = p.d_in;
   if (tid == 0) nsat_s = 0;
   __syncthreads();
-  for (int i = tid; i < TOK; i += kSatThreads)
+  for (int i = tid; i < TOK; i += 64 * WV)
     if (t0 + i < ntok && exact_token(p.r[t0 + i], d_in, p.exact_from)) satl[atomicAdd(&nsat_s, 1)] = i;
   __syncthreads();
   const int nsat = nsat_s;
   if (nsat == 0) return;  // block-uniform
   const int nks = p.din_pad / KS;
-  // this wave's loads: A tiles (NA / 4) wave + j (list rows 16 tile + r16, chunk E g of the
-  // step) and B tiles (NB / 4) wave + j of the block's columns
-  const T* xrow[NA / 4];
+  // this wave's loads: A tiles (NA / WV) wave + j (list rows 16 tile + r16, chunk E g of the
+  // step) and B tiles (NB / WV) wave + j of the block's columns
+  const T* xrow[NA / WV];
 #pragma unroll
-  for (int j = 0; j < NA / 4; ++j)
-    xrow[j] = static_cast<const T*>(p.X) + (t0 + satl[min(16 * ((NA / 4) * wave + j) + r16, nsat - 1)]) * d_in;
+  for (int j = 0; j < NA / WV; ++j)
+    xrow[j] = static_cast<const T*>(p.X) + (t0 + satl[min(16 * ((NA / WV) * wave + j) + r16, nsat - 1)]) * d_in;
   const int klast = d_in - E;  // last chunk of a row
   const T* wt = static_cast<const T*>(p.Wt) + ((int64_t)(cb * COLS / 16) * nks * 64 + lane) * E;
   const uint32_t st0 = lds_addr(stage);
   auto issue = [&](int ks) {
     const uint32_t slot = st0 + (uint32_t)(ks % ST) * kSlot;
 #pragma unroll
-    for (int j = 0; j < NA / 4; ++j)
-      load_lds16(xrow[j] + min(ks * KS + E * g, klast), slot + (uint32_t)((NA / 4) * wave + j) * 1024u);
+    for (int j = 0; j < NA / WV; ++j)
+      load_lds16(xrow[j] + min(ks * KS + E * g, klast), slot + (uint32_t)((NA / WV) * wave + j) * 1024u);
 #pragma unroll
-    for (int j = 0; j < NB / 4; ++j) {
-      const int nt = (NB / 4) * wave + j;
+    for (int j = 0; j < NB / WV; ++j) {
+      const int nt = (NB / WV) * wave + j;
       load_lds16(wt + ((int64_t)nt * nks + ks) * 64 * E, slot + (uint32_t)(NA + nt) * 1024u);
     }
   };
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const bool active = 16 * MTW * wm < nsat;  // wave-uniform
   f32x4_t acc[MTW][NTW];
 #pragma unroll
@@ -883,8 +884,8 @@ hipError_t launch_saturated(const FwdParams& p, hipStream_t s) {
   if (vec && p.d_out % 256 == 0) {  // 128 (bf16) or 64 (float32) tokens x 256 columns per block
     const int tok = p.bf16 ? 128 : 64;
     const dim3 g2((unsigned)(((ntok + tok - 1) / tok) * (p.d_out / 256)));
-    return p.bf16 ? launch_stage_kernel(k_saturated_lds<1, 8, 4, kSatStages>, g2, blk, 0, s, p)
-                  : launch_stage_kernel(k_saturated_lds<0, 8, 2, kSatStages>, g2, blk, 0, s, p);
+    return p.bf16 ? launch_stage_kernel(k_saturated_lds<1, 4, 4, kSatStages, 4>, g2, dim3(512), 0, s, p)
+                  : launch_stage_kernel(k_saturated_lds<0, 8, 2, kSatStages, 2>, g2, dim3(256), 0, s, p);
   }
   return p.bf16 ? launch_stage_kernel(k_saturated<1, false>, grid, blk, 0, s, p)
                 : launch_stage_kernel(k_saturated<0, false>, grid, blk, 0, s, p);
