@@ -708,11 +708,12 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 
 // One direct global-to-LDS load of 16 bytes per lane: lane l's bytes land at lds + 16 l
-// (lds wave-uniform, in M0). Issued through inline assembly so that the compiler does not
+// (lds wave-uniform, in M0: an input operand bound to that register, so the compiler sets
+// it and knows it is read). Issued through inline assembly so that the compiler does not
 // track it: the kernel waits for these loads itself (s_waitcnt vmcnt with the count of
 // loads issued after the one it needs) and publishes them with a barrier.
 __device__ __forceinline__ void load_lds16(const void* g, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(g), "{m0}"(lds) : "memory");
 }
 
 // Block barrier without a memory fence: LDS written by the direct loads is published by the
