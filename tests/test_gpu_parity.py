@@ -331,6 +331,19 @@ def test_sampled_d_in_1024_bf16(dev):
     assert n_tok > 0
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_saturated_kernel_d_in_1000(dev, dtype):
+    # d_in 1000 (above 768, a multiple of 8 but not of 32): the saturated tokens go to the
+    # separate staged MFMA kernel, whose last k step re-reads each row's final chunk against
+    # the zero padding of the prepared W_v^T. Its blocks of 128 tokens (bf16; 64 for float32)
+    # hold 31 to 76 saturated tokens of ragged rows, so some use one row of waves and some
+    # both, with partial tiles
+    L = wl.make_layer(3, 150, 1000, 8, dtype, data_seed=52, lens=np.array([150, 97, 130]), q_scale=4.0,
+                      token_scale_sigma=0.5)
+    amb, n_tok = _full_check(L, dev, 0.25, seed=7)
+    assert n_tok > 0
+
+
 def test_bf16_width_not_multiple_of_8(dev):
     # d_in 100: element-wise x loads in the gather, partial lane runs in the sampler
     L = wl.make_layer(2, 48, 100, 4, "bf16", data_seed=32, lens=np.array([48, 29]), q_scale=3.0,
