@@ -191,6 +191,8 @@ mca_status mca_workspace_size(const mca_forward_desc* desc, size_t* bytes);
  * Inputs Q, K, X, W_v (device, `desc->dtype`) and `prepared` (filled by
  * mca_prepare_weights from this W_v with the same dtype and sizes). Outputs Y (device [B, n, d_out] float32) and r (device [B, n]
  * int32). Rows of Y for padded queries are computed by the same formula.
+ * Q and K are expected to be finite: with a non-finite score, Y and r are unspecified
+ * (every count stays in [0, d_in] and every access within the buffers).
  * `workspace` must hold at least mca_workspace_size bytes; its contents on entry do not
  * matter and are overwritten.
  * Errors: MCA_ERR_INVALID_ARGUMENT (null required pointer, size < 1, non-finite or
